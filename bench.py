@@ -1,0 +1,309 @@
+#!/usr/bin/env python3
+"""Benchmark of the temporal neighbour sampler on one MI355X.
+
+Workload (default ``c4``): a MAG-shaped citation graph of 121.7M nodes and
+1.3B edges (timestamps = publication years), undirected T-CSR of 2.6B
+entries, 2-hop uniform sampling with fanouts 10x10, batches of 4,000 edges x 3
+roots.  A step is one call of the sampler (all hops: window search, selection,
+gather, compaction) over a super-batch of consecutive batches; the T-CSR is
+built once before timing, as the paper builds it once per graph, and its build
+time is reported beside the step rate.
+
+Printed: one JSON line with sampled neighbours/s (valid slots of every hop per
+second of sampler time), the roofline of the dominant kernel (the hop >= 2
+sampling kernel, HIP events on its own stream), and the CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0
+METRIC = "sampled neighbours/sec (2-hop 10x10 uniform) + achieved HBM GB/s vs peak"
+
+
+def log(msg):
+    print("[bench %7.1fs] %s" % (time.time() - T0, msg), file=sys.stderr, flush=True)
+
+
+T0 = time.time()
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
+    ap.add_argument("--batches-per-step", type=int, default=None,
+                    help="batches fused into one sampler call (default: 64 for c3/c4, 1 for c5, 263 for c2)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target duration of the CPU oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--small", action="store_true", help="reduced graph size (development only)")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2203_14883_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(kernel_hash, workload):
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary, if it was taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", "hop_kernel_%s_pmc.md" % workload)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    for line in open(path):
+        if line.startswith("- ") and ":" in line:
+            k, _, v = line[2:].partition(":")
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("kernel_source_hash") != kernel_hash:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def make_workload(name, small):
+    from paper_2203_14883_amd import workloads as W
+    if not small:
+        return W.make(name)
+    return {"c2": lambda: W.make_c2(),
+            "c3": lambda: W.make_c3(num_edges=20_000_000),
+            "c4": lambda: W.make_c4(num_nodes=12_170_000, num_edges=130_000_000),
+            "c5": lambda: W.make_c5(num_nodes=1_000_000, num_edges=10_000_000)}[name]()
+
+
+def step_positions(nb, B, n):
+    """n super-batch start positions spread evenly over the epoch."""
+    last = max(nb - B, 0)
+    if n <= 1:
+        return [last // 2]
+    return [int(round(i * last / (n - 1))) for i in range(n)]
+
+
+def cpu_baseline(w, target_s):
+    """The oracle, single-threaded, on a bounded sample: the roots of a few
+    consecutive batches from the middle of the epoch, sampled over an oracle
+    T-CSR of the sub-graph of edges touching every node the sample reaches
+    (which gives those nodes exactly their full runs)."""
+    import oracle
+    nb = w.num_batches()
+    b0 = nb // 2
+
+    def subgraph(nodes):
+        flag = np.zeros(w.num_nodes, dtype=bool)
+        flag[nodes] = True
+        keep = flag[w.src] | flag[w.dst]
+        idx = np.nonzero(keep)[0]
+        return oracle.build_tcsr(w.src[idx], w.dst[idx], w.ts[idx], idx.astype(np.int64),
+                                 w.num_nodes, w.undirected)
+
+    def one(nbatches):
+        roots, rts, base = w.batches(b0, b0 + nbatches)
+        g1 = subgraph(np.unique(roots))
+        h1 = oracle.sample(g1, roots, rts, w.fanouts[:1], w.mode, w.snapshots, w.snapshot_len,
+                           w.sample_seed, base)
+        reach = np.unique(np.concatenate([roots, h1[0].nbr[h1[0].nbr >= 0]]))
+        g = subgraph(reach)
+        t = time.perf_counter()
+        out = oracle.sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
+                            w.sample_seed, base)
+        dt = time.perf_counter() - t
+        nbrs = int(sum(int((h.nbr >= 0).sum()) for h in out))
+        return dt, nbrs, len(roots)
+
+    dt, nbrs, nroots = one(1)
+    nbatches = 1
+    if dt < target_s:
+        nbatches = int(min(64, max(1, math.floor(target_s / max(dt, 1e-3)))))
+        if nbatches > 1:
+            dt, nbrs, nroots = one(nbatches)
+    return dict(value=nbrs / dt, unit="neighbours/s", cores=1, kind="oracle",
+                sample="%d roots (%d consecutive batches from batch %d) of %s, 2 hops, %d neighbours, %.2f s single-threaded"
+                       % (nroots, nbatches, b0, w.name, nbrs, dt))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only (this build has no multi-GPU path); got --gpus %d"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2203_14883_amd as P
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    P.lib()   # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    log("generating workload %s%s" % (args.workload, " (small)" if args.small else ""))
+    w = make_workload(args.workload, args.small)
+    log("graph: %d nodes, %d edges" % (w.num_nodes, w.num_edges))
+
+    src, dst, ts, eid = w.build_input()
+    d_src = torch.from_numpy(src).to(dev)
+    d_dst = torch.from_numpy(dst).to(dev)
+    d_ts = torch.from_numpy(ts).to(dev)
+    d_eid = None if eid is None else torch.from_numpy(eid).to(dev)
+    torch.cuda.synchronize()
+    log("COO uploaded")
+
+    ws = torch.empty(P.tcsr_build_workspace(w.num_edges, w.num_nodes, w.undirected),
+                     dtype=torch.uint8, device=dev)
+    P.timer_enable(1 << 14)
+    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws)  # warm-up
+    del g
+    torch.cuda.synchronize()
+    P.timer_reset()
+    t = time.perf_counter()
+    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws)
+    torch.cuda.synchronize()
+    build_wall = time.perf_counter() - t
+    build_ms, _ = P.timer_read(P.binding.TIMER_BUILD)
+    del ws, d_src, d_dst, d_ts, d_eid
+    torch.cuda.empty_cache()
+    log("T-CSR built: %d entries, %.1f ms (events), %.1f ms wall" % (g.num_entries, build_ms, build_wall * 1e3))
+
+    B = args.batches_per_step or {"c2": w.num_batches(), "c3": 64, "c4": 64, "c5": 1}[args.workload]
+    B = min(B, w.num_batches())
+    # timed steps are spread evenly over the epoch; warm-up steps sit between them
+    timed_pos = step_positions(w.num_batches(), B, args.steps)
+    span = max(w.num_batches() - B, 1)
+    warm_pos = [(p + max(span // (2 * max(args.steps, 1)), 1)) % span for p in timed_pos[:args.warmup]]
+    inputs = {}
+    for b in sorted(set(timed_pos + warm_pos)):
+        r, t_, base = w.batches(b, b + B)
+        inputs[b] = (torch.from_numpy(r).to(dev), torch.from_numpy(t_).to(dev), base, len(r))
+    max_roots = max(v[3] for v in inputs.values())
+    smp = P.Sampler(max_roots, w.fanouts, w.snapshots, device=dev)
+    log("sampler buffers: %d roots per step, %.2f GB outputs+workspace"
+        % (max_roots, sum(x.numel() * x.element_size() for x in
+                          smp.nbr + smp.eid + smp.ts + smp.dt + [smp.workspace]) / 1e9))
+
+    def run(b):
+        r, t_, base, n = inputs[b]
+        smp.run(g, r, t_, w.mode, w.snapshot_len, w.sample_seed, base, num_roots=n)
+
+    for b in warm_pos:
+        run(b)
+    torch.cuda.synchronize()
+    P.timer_reset()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for b in timed_pos:
+        run(b)
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    hop1_ms, hop1_n = P.timer_read(P.binding.TIMER_HOP1)
+    hopn_ms, hopn_n = P.timer_read(P.binding.TIMER_HOPN)
+    comp_ms, comp_n = P.timer_read(P.binding.TIMER_COMPACT)
+    log("timed %d steps: %.2f ms total (hop1 %.2f, hopN %.2f, compaction %.2f ms)"
+        % (args.steps, total_ms, hop1_ms, hopn_ms, comp_ms))
+
+    # untimed pass over the same steps: valid slots (neighbours) and the
+    # algorithmic bytes of the hop >= 2 kernel
+    indptr = g.indptr
+    nbrs_total = 0
+    slots_total = 0
+    hopn_bytes = 0.0
+    for b in timed_pos:
+        run(b)
+        hs = smp.hops()
+        for h, hop in enumerate(hs):
+            valid = hop.nbr >= 0
+            nv = int(valid.sum())
+            nbrs_total += nv
+            slots_total += hop.nbr.numel()
+            if h >= 1:
+                roots2 = hs[h - 1].nbr[hs[h - 1].nbr >= 0].long()
+                deg = (indptr[roots2 + 1] - indptr[roots2]).double()
+                bounds = 1 if math.isinf(w.snapshot_len) else 2
+                search = float((torch.ceil(torch.log2(deg + 1.0)) * 4.0 * bounds).sum())
+                hopn_bytes += (hop.num_roots * (8 + 16) + search + nv * 16 + hop.nbr.numel() * 20)
+    hopn_bytes_per_launch = hopn_bytes / max(len(timed_pos), 1)
+    avg_hopn_ms = hopn_ms / max(hopn_n, 1)
+    achieved = hopn_bytes_per_launch / (avg_hopn_ms * 1e-3) / 1e9 if avg_hopn_ms > 0 else 0.0
+    value = nbrs_total / (total_ms * 1e-3)
+    khash = kernel_source_hash()
+    traffic = read_traffic(khash, args.workload) if not args.small else None
+    log("neighbours %d over %d slots; %.3g neighbours/s; hopN %.1f GB/s algorithmic"
+        % (nbrs_total, slots_total, value, achieved))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("CPU oracle baseline")
+        cpu = cpu_baseline(w, args.cpu_seconds)
+        log("CPU oracle: %.3g neighbours/s (%s)" % (cpu["value"], cpu["sample"]))
+
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "neighbours/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s%s: %d nodes, %d edges, undirected T-CSR of %d entries; %d-hop %s %s, %d snapshot(s)%s; %d batches of %d edges x 3 roots per step"
+                        % (w.name, " (reduced)" if args.small else "", w.num_nodes, w.num_edges,
+                           g.num_entries, len(w.fanouts), w.mode, "x".join(map(str, w.fanouts)),
+                           w.snapshots, "" if math.isinf(w.snapshot_len) else " of %g" % w.snapshot_len,
+                           B, w.batch_edges),
+            "roots_per_step": max_roots,
+            "neighbours_per_step": nbrs_total / args.steps,
+            "slots_per_step": slots_total / args.steps,
+            "tcsr_build_ms": build_ms,
+            "kernel_ms_per_step": {"hop1": hop1_ms / args.steps, "hopN": hopn_ms / args.steps,
+                                   "compaction": comp_ms / args.steps},
+        },
+        "roofline": {
+            "kernel": "hop_kernel (hops >= 2)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": hopn_bytes_per_launch,
+            "avg_launch_ms": avg_hopn_ms,
+            "kernel_source_hash": khash,
+        },
+        "cpu_baseline": cpu,
+    }
+    P.timer_disable()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

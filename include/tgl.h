@@ -1,0 +1,233 @@
+/*
+ * tgl.h -- C ABI of libtgl: a Temporal-CSR (T-CSR) build and a multi-hop
+ * temporal neighbour sampler on one AMD Instinct MI355X (gfx950) GPU.
+ *
+ * Method: "TGL: A General Framework for Temporal GNN Training on
+ * Billion-Scale Graphs" (Zhou et al., VLDB 2022), Section 3.1 (the T-CSR data
+ * structure, sampling, parallel sampling) and Algorithm 1 (Parallel Temporal
+ * Sampler), with dynamic snapshots as described at the start of Section 3.
+ *
+ * Conventions for every entry point:
+ *  - Array arguments marked [device] are device pointers on the current HIP
+ *    device; [host] pointers are ordinary host memory read during the call.
+ *  - The caller owns every buffer (inputs, T-CSR arrays, outputs and
+ *    workspace).  The library allocates no device memory in these calls.
+ *  - Work is enqueued on `stream` (a hipStream_t passed as void*; NULL means
+ *    the null stream).  Device inputs must stay valid, and outputs must not be
+ *    read, until that work completes.
+ *  - Functions return a tgl_status and never throw.  Argument checks run on
+ *    the host before anything is enqueued; a failed check enqueues nothing.
+ *  - Calls that overlap on one stream are ordered; calls on different
+ *    streams must not share outputs or workspace.
+ */
+#ifndef TGL_H
+#define TGL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t tgl_status;
+#define TGL_OK        0   /* success                                           */
+#define TGL_EINVAL   (-1) /* invalid argument (checked on the host)            */
+#define TGL_ERANGE   (-2) /* build input out of range: endpoint not in [0,N) or
+                             NaN timestamp (found on the device)                */
+#define TGL_ENOSPACE (-3) /* workspace smaller than the matching *_workspace() */
+#define TGL_EDEVICE  (-4) /* a HIP call or kernel launch failed                */
+
+#define TGL_MOST_RECENT 0 /* k newest candidates, newest first (Sec. 2.3)     */
+#define TGL_UNIFORM     1 /* k independent uniform draws from the candidates   */
+
+#define TGL_BUILD_UNDIRECTED 1u /* also insert every edge reversed             */
+
+#define TGL_MAX_HOPS      8
+#define TGL_MAX_FANOUT    1024
+#define TGL_MAX_SNAPSHOTS 64
+
+/*
+ * One T-CSR entry: an edge leaving the owner node (whose run contains the
+ * entry) towards `nbr`, at time `ts`, with the caller's edge id `eid`.
+ * Section 3.1 keeps indices and times as separate arrays; here they are
+ * interleaved into one 16-byte record so that a sampled slot is fetched with
+ * a single aligned 16-byte load.
+ */
+typedef struct tgl_entry {
+    int32_t nbr;
+    float ts;
+    int64_t eid;
+} tgl_entry;
+
+/*
+ * Non-owning view of a T-CSR (Section 3.1): node x owns entries
+ * [indptr[x], indptr[x+1]) of `entries`, sorted by ts ascending (ties in any
+ * fixed order; tgl_tcsr_build uses input order).  Timestamps must not be NaN.
+ *   indptr   [device] int64[num_nodes + 1], indptr[0] = 0, non-decreasing,
+ *                     indptr[num_nodes] = num_entries
+ *   entries  [device] tgl_entry[num_entries], 16-byte aligned
+ * The sampler clamps every indptr value into [0, num_entries], so a
+ * malformed view yields wrong samples but never an out-of-bounds access.
+ */
+typedef struct tgl_tcsr {
+    int64_t num_nodes;
+    int64_t num_entries;
+    const int64_t *indptr;
+    const tgl_entry *entries;
+} tgl_tcsr;
+
+/*
+ * Outputs of one hop (structure of arrays, one element per slot).
+ *   nbr, eid, ts, dt  [device] slot arrays with capacity
+ *                     tgl_sample_capacity(..., hop) elements each
+ *   parent            [device] int64, one per root of this hop: index of the
+ *                     previous hop's slot the root came from.  Capacity
+ *                     tgl_sample_capacity(..., hop - 1).  Unused (may be NULL)
+ *                     for hop 1.
+ * A missing neighbour (PAD) is nbr = -1, eid = -1, ts = -1.0f, dt = -1.0f.
+ */
+typedef struct tgl_hop_out {
+    int32_t *nbr;
+    int64_t *eid;
+    float *ts;
+    float *dt;
+    int64_t *parent;
+} tgl_hop_out;
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int32_t tgl_version(void);
+
+/* Static string naming a status code. */
+const char *tgl_status_str(tgl_status status);
+
+/* ------------------------------------------------------------------------ */
+/* T-CSR build (Section 3.1, "The T-CSR Data Structure"; Figure 3)          */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Bytes of workspace tgl_tcsr_build needs for `num_edges` input edges on
+ * `num_nodes` nodes with `flags`.  Returns 0 for arguments tgl_tcsr_build
+ * would reject with TGL_EINVAL.
+ */
+size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t flags);
+
+/*
+ * Builds the T-CSR of a temporal edge list.
+ *   src, dst   [device] int32[num_edges]   endpoints, each in [0, num_nodes)
+ *   ts         [device] float[num_edges]   timestamps, not NaN (-0 is stored
+ *                                           as +0)
+ *   eid        [device] int64[num_edges]   edge ids, or NULL for eid = index
+ *   num_edges  >= 0; entries M = num_edges, or 2*num_edges with
+ *              TGL_BUILD_UNDIRECTED; M must be < 2^32
+ *   num_nodes  in [1, 2^31 - 1]
+ *   flags      0 or TGL_BUILD_UNDIRECTED
+ *   indptr     [device] int64[num_nodes + 1]  output
+ *   entries    [device] tgl_entry[M]          output
+ *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
+ * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
+ * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
+ * dst[i], nbr src[i]).  Each node's run is sorted by (ts, entry index).
+ * Synchronises `stream` once, to read the device-side range check; returns
+ * TGL_ERANGE (outputs unspecified) if any endpoint or timestamp is invalid.
+ */
+tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
+                          const int64_t *eid, int64_t num_edges, int64_t num_nodes,
+                          uint32_t flags, int64_t *indptr, tgl_entry *entries,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Worst-case number of slots of hop `hop` (1..hops): num_roots * S * k_1 *
+ * ... * k_hop (S = num_snapshots).  hop = 0 gives num_roots.  Returns -1 for
+ * invalid arguments or if the product exceeds 2^62.
+ */
+int64_t tgl_sample_capacity(int64_t num_roots, int32_t hops, const int32_t *fanouts,
+                            int32_t num_snapshots, int32_t hop);
+
+/* Bytes of workspace tgl_sample needs (0 for invalid arguments). */
+size_t tgl_sample_workspace(int64_t num_roots, int32_t hops, const int32_t *fanouts,
+                            int32_t num_snapshots);
+
+/*
+ * Samples `hops` layers of temporal neighbours for `num_roots` roots.
+ *   g             [host] T-CSR view (arrays on the device)
+ *   roots         [device] int32[num_roots]  root nodes; a node outside
+ *                                            [0, num_nodes) gets only PAD
+ *   root_ts       [device] float[num_roots]  query times (NaN gets only PAD)
+ *   hops          1..TGL_MAX_HOPS
+ *   fanouts       [host] int32[hops], each 1..TGL_MAX_FANOUT
+ *   mode          TGL_MOST_RECENT or TGL_UNIFORM
+ *   num_snapshots S in 1..TGL_MAX_SNAPSHOTS
+ *   snapshot_len  D > 0; +inf means one unbounded window (then S must be 1)
+ *   seed          key of the uniform draws
+ *   root_base     global index of roots[0]; a call over roots [0, n) equals
+ *                 calls over sub-ranges with root_base advanced accordingly
+ *   outs          [host] tgl_hop_out[hops]
+ *   counts        [device] int64[hops]: counts[h-1] = number of roots of hop h
+ *   workspace     [device] at least tgl_sample_workspace(...) bytes
+ *
+ * Window s (0 = newest) of a root (x, t) holds the entries of x with
+ *   t - (s+1)*D <= ts < t - s*D,
+ * both bounds evaluated in double precision (upper bound t when s = 0, lower
+ * bound -inf when D is infinite).  Hop 1 samples every window of every root:
+ * slot (r, s, j) is at index (r*S + s)*k_1 + j.  The valid slots of hop h, in
+ * index order, become the roots of hop h+1 (node = slot nbr, time = slot ts)
+ * and sample only the window they came from, relative to their own time:
+ * slot (q, j) is at q*k_{h+1} + j.
+ *   TGL_MOST_RECENT: slot j is the j-th newest candidate, PAD if fewer.
+ *   TGL_UNIFORM:     slot j is candidate floor(H * n / 2^64) (n candidates,
+ *                    oldest first), all PAD if n = 0, where
+ *                    H = mix(mix(mix(seed ^ 0x9E3779B97F4A7C15) ^ path) ^
+ *                            (hop << 40 | s << 24 | j)),
+ *                    mix = the SplitMix64 finalizer, path = root_base + r
+ *                    for hop-1 roots, path*S*k_1 + s*k_1 + j for a child of
+ *                    hop-1 slot (r, s, j), path*k_h + j for a child of
+ *                    hop-h slot (q, j), all modulo 2^64.
+ *   dt = t - ts rounded to float.
+ * Never synchronises the stream; per-hop root counts stay on the device.
+ */
+tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
+                      int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
+                      int32_t num_snapshots, float snapshot_len, uint64_t seed,
+                      uint64_t root_base, const tgl_hop_out *outs, int64_t *counts,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel timers (instrumentation for benchmarks)                           */
+/* ------------------------------------------------------------------------ */
+
+#define TGL_TIMER_HOP1    0  /* first-hop sampling kernel                     */
+#define TGL_TIMER_HOPN    1  /* sampling kernel of hops >= 2                  */
+#define TGL_TIMER_COMPACT 2  /* next-hop root compaction (scan + emit)         */
+#define TGL_TIMER_BUILD   3  /* whole tgl_tcsr_build                          */
+#define TGL_TIMER_KINDS   4
+
+/*
+ * Starts recording HIP events around every kernel of the kinds above, on the
+ * stream each is launched on, for up to `capacity` launches (events are
+ * created here, so call this outside timed regions).  Resets all totals.
+ */
+tgl_status tgl_timer_enable(int32_t capacity);
+
+/* Stops recording and releases the events. */
+tgl_status tgl_timer_disable(void);
+
+/*
+ * Waits for the recorded events and returns, for one kind, the summed
+ * duration in milliseconds and the number of launches measured since the
+ * last tgl_timer_enable / tgl_timer_reset.
+ */
+tgl_status tgl_timer_read(int32_t kind, double *total_ms, int64_t *launches);
+
+/* Clears totals and recorded launches (keeps the events). */
+tgl_status tgl_timer_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TGL_H */

@@ -1,0 +1,315 @@
+"""ctypes binding of libtgl (include/tgl.h): argument marshalling only.
+
+Device memory comes from torch tensors and work goes on torch's current
+stream; every step of the build and the sampler runs in the HIP library.  If
+libtgl.so is missing the first call raises -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import math
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtgl.so")
+
+OK, EINVAL, ERANGE, ENOSPACE, EDEVICE = 0, -1, -2, -3, -4
+MOST_RECENT, UNIFORM = 0, 1
+BUILD_UNDIRECTED = 1
+MAX_HOPS, MAX_FANOUT, MAX_SNAPSHOTS = 8, 1024, 64
+TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD = 0, 1, 2, 3
+
+MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
+         MOST_RECENT: MOST_RECENT, UNIFORM: UNIFORM}
+
+# every function declared in include/tgl.h
+EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
+           "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample", "tgl_timer_enable",
+           "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
+
+
+class TglError(RuntimeError):
+    def __init__(self, status: int, what: str = ""):
+        self.status = status
+        super().__init__("%s: %s (%d)" % (what or "libtgl", status_str(status), status))
+
+
+class c_tcsr(C.Structure):
+    _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
+                ("indptr", C.c_void_p), ("entries", C.c_void_p)]
+
+
+class c_hop_out(C.Structure):
+    _fields_ = [("nbr", C.c_void_p), ("eid", C.c_void_p), ("ts", C.c_void_p),
+                ("dt", C.c_void_p), ("parent", C.c_void_p)]
+
+
+_lib: Optional[C.CDLL] = None
+
+
+def lib() -> C.CDLL:
+    """The loaded libtgl.  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libtgl.so not found at %s; build it with "
+                           "`python -m paper_2203_14883_amd.build_lib`" % LIB_PATH)
+    L = C.CDLL(LIB_PATH)
+    P, i32, i64, u32, u64, f32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32, C.c_uint64, C.c_float
+    L.tgl_version.restype = i32
+    L.tgl_version.argtypes = []
+    L.tgl_status_str.restype = C.c_char_p
+    L.tgl_status_str.argtypes = [i32]
+    L.tgl_tcsr_build_workspace.restype = C.c_size_t
+    L.tgl_tcsr_build_workspace.argtypes = [i64, i64, u32]
+    L.tgl_tcsr_build.restype = i32
+    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, C.c_size_t, P]
+    L.tgl_sample_capacity.restype = i64
+    L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
+    L.tgl_sample_workspace.restype = C.c_size_t
+    L.tgl_sample_workspace.argtypes = [i64, i32, P, i32]
+    L.tgl_sample.restype = i32
+    L.tgl_sample.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
+                             C.POINTER(c_hop_out), P, P, C.c_size_t, P]
+    L.tgl_timer_enable.restype = i32
+    L.tgl_timer_enable.argtypes = [i32]
+    L.tgl_timer_disable.restype = i32
+    L.tgl_timer_disable.argtypes = []
+    L.tgl_timer_reset.restype = i32
+    L.tgl_timer_reset.argtypes = []
+    L.tgl_timer_read.restype = i32
+    L.tgl_timer_read.argtypes = [i32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+    _lib = L
+    return L
+
+
+def status_str(s: int) -> str:
+    return lib().tgl_status_str(int(s)).decode()
+
+
+def _check(s: int, what: str):
+    if s != OK:
+        raise TglError(int(s), what)
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _i32_array(v: Sequence[int]):
+    a = np.ascontiguousarray(np.asarray(v, dtype=np.int32))
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+# --------------------------------------------------------------------------
+# T-CSR
+# --------------------------------------------------------------------------
+
+@dataclass
+class TCSR:
+    """Device T-CSR: indptr int64[N+1]; entries int64[M, 2] holding the 16-byte
+    records (int32 nbr, float32 ts | int64 eid)."""
+    indptr: torch.Tensor
+    entries: torch.Tensor
+    num_nodes: int
+
+    @property
+    def num_entries(self) -> int:
+        return int(self.entries.shape[0])
+
+    @property
+    def nbr(self) -> torch.Tensor:
+        return self.entries.view(torch.int32)[:, 0]
+
+    @property
+    def ts(self) -> torch.Tensor:
+        return self.entries.view(torch.float32)[:, 1]
+
+    @property
+    def eid(self) -> torch.Tensor:
+        return self.entries[:, 1]
+
+    def c_view(self) -> c_tcsr:
+        return c_tcsr(self.num_nodes, self.num_entries, self.indptr.data_ptr(),
+                      self.entries.data_ptr() if self.num_entries else None)
+
+
+def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray:
+    """Host-side packing of structure-of-arrays T-CSR fields into records."""
+    m = len(nbr)
+    rec = np.zeros((m, 4), dtype=np.int32)
+    rec[:, 0] = np.asarray(nbr, np.int32)
+    rec[:, 1] = np.asarray(ts, np.float32).view(np.int32)
+    rec.view(np.int64)[:, 1] = np.asarray(eid, np.int64)
+    return rec.view(np.int64).reshape(m, 2)
+
+
+def tcsr_from_host(indptr, nbr, ts, eid, device="cuda") -> TCSR:
+    """Uploads a T-CSR given as host arrays (e.g. one built elsewhere)."""
+    rec = pack_entries(nbr, ts, eid)
+    ent = torch.from_numpy(rec).to(device)
+    if ent.shape[0] == 0:
+        ent = torch.empty((0, 2), dtype=torch.int64, device=device)
+    return TCSR(torch.from_numpy(np.asarray(indptr, np.int64)).to(device), ent, len(indptr) - 1)
+
+
+def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:
+    return int(lib().tgl_tcsr_build_workspace(num_edges, num_nodes,
+                                              BUILD_UNDIRECTED if undirected else 0))
+
+
+def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
+               eid: Optional[torch.Tensor], num_nodes: int, undirected: bool = True,
+               workspace: Optional[torch.Tensor] = None, stream=None) -> TCSR:
+    """Builds the T-CSR of a device COO (int32 src/dst, float32 ts, int64 eid or None)."""
+    L = lib()
+    m0 = int(src.shape[0])
+    flags = BUILD_UNDIRECTED if undirected else 0
+    for t, dt in ((src, torch.int32), (dst, torch.int32), (ts, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous() or t.shape[0] != m0:
+            raise ValueError("src/dst must be int32, ts float32, contiguous, same length")
+    if eid is not None and (eid.dtype != torch.int64 or not eid.is_contiguous() or eid.shape[0] != m0):
+        raise ValueError("eid must be a contiguous int64 tensor of the same length")
+    M = 2 * m0 if undirected else m0
+    dev = src.device
+    indptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
+    entries = torch.empty((M, 2), dtype=torch.int64, device=dev)
+    need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
+    if need == 0:
+        raise TglError(EINVAL, "tgl_tcsr_build_workspace")
+    own_ws = workspace is None
+    if own_ws:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    s = L.tgl_tcsr_build(_p(src), _p(dst), _p(ts), _p(eid), m0, num_nodes, flags, _p(indptr),
+                         _p(entries) if M else None, _p(workspace), workspace.numel(), _stream(stream))
+    if own_ws:
+        del workspace
+    _check(s, "tgl_tcsr_build")
+    return TCSR(indptr, entries, num_nodes)
+
+
+# --------------------------------------------------------------------------
+# sampler
+# --------------------------------------------------------------------------
+
+@dataclass
+class Hop:
+    nbr: torch.Tensor
+    eid: torch.Tensor
+    ts: torch.Tensor
+    dt: torch.Tensor
+    parent: Optional[torch.Tensor]
+    num_roots: int
+
+
+def sample_capacity(num_roots: int, fanouts: Sequence[int], snapshots: int, hop: int) -> int:
+    fa, fp = _i32_array(fanouts)
+    return int(lib().tgl_sample_capacity(num_roots, len(fa), fp, snapshots, hop))
+
+
+class Sampler:
+    """Preallocated outputs and workspace for repeated calls with up to
+    ``max_roots`` roots and fixed fanouts / snapshots.  ``run`` enqueues one
+    call and returns without synchronising; ``hops`` slices the results."""
+
+    def __init__(self, max_roots: int, fanouts: Sequence[int], snapshots: int = 1,
+                 device="cuda"):
+        L = lib()
+        self.fanouts = tuple(int(k) for k in fanouts)
+        self.snapshots = int(snapshots)
+        self.max_roots = int(max_roots)
+        self._fa, self._fp = _i32_array(self.fanouts)
+        H = len(self.fanouts)
+        caps = [int(L.tgl_sample_capacity(self.max_roots, H, self._fp, self.snapshots, h))
+                for h in range(H + 1)]
+        if min(caps) < 0:
+            raise TglError(EINVAL, "tgl_sample_capacity")
+        self.caps = caps
+        dev = torch.device(device)
+        self.nbr = [torch.empty(max(caps[h + 1], 1), dtype=torch.int32, device=dev) for h in range(H)]
+        self.eid = [torch.empty(max(caps[h + 1], 1), dtype=torch.int64, device=dev) for h in range(H)]
+        self.ts = [torch.empty(max(caps[h + 1], 1), dtype=torch.float32, device=dev) for h in range(H)]
+        self.dt = [torch.empty(max(caps[h + 1], 1), dtype=torch.float32, device=dev) for h in range(H)]
+        self.parent = [None] + [torch.empty(max(caps[h], 1), dtype=torch.int64, device=dev)
+                                for h in range(1, H)]
+        self.counts = torch.zeros(H, dtype=torch.int64, device=dev)
+        ws = int(L.tgl_sample_workspace(self.max_roots, H, self._fp, self.snapshots))
+        self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
+        outs = (c_hop_out * H)()
+        for h in range(H):
+            outs[h] = c_hop_out(self.nbr[h].data_ptr(), self.eid[h].data_ptr(), self.ts[h].data_ptr(),
+                                self.dt[h].data_ptr(),
+                                None if self.parent[h] is None else self.parent[h].data_ptr())
+        self._outs = outs
+
+    def run(self, g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, mode="uniform",
+            snapshot_len: float = math.inf, seed: int = 0, root_base: int = 0, stream=None,
+            num_roots: Optional[int] = None):
+        n = int(roots.shape[0]) if num_roots is None else int(num_roots)
+        if n > self.max_roots:
+            raise ValueError("more roots than the sampler was sized for")
+        if roots.dtype != torch.int32 or root_ts.dtype != torch.float32:
+            raise ValueError("roots must be int32 and root_ts float32")
+        if not roots.is_contiguous() or not root_ts.is_contiguous():
+            raise ValueError("roots and root_ts must be contiguous")
+        view = g.c_view()
+        s = lib().tgl_sample(C.byref(view), _p(roots), _p(root_ts), n, len(self.fanouts), self._fp,
+                             MODES[mode], self.snapshots, C.c_float(snapshot_len),
+                             C.c_uint64(seed & (2**64 - 1)), C.c_uint64(root_base & (2**64 - 1)),
+                             self._outs, _p(self.counts), _p(self.workspace),
+                             self.workspace.numel(), _stream(stream))
+        _check(s, "tgl_sample")
+
+    def hops(self) -> List[Hop]:
+        """Slices the outputs of the last call by the per-hop root counts (syncs)."""
+        counts = self.counts.cpu().tolist()
+        out = []
+        for h, k in enumerate(self.fanouts):
+            nr = int(counts[h])
+            n = nr * (self.snapshots if h == 0 else 1) * k
+            out.append(Hop(self.nbr[h][:n], self.eid[h][:n], self.ts[h][:n], self.dt[h][:n],
+                           None if h == 0 else self.parent[h][:nr], nr))
+        return out
+
+
+def sample(g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, fanouts: Sequence[int],
+           mode="uniform", snapshots: int = 1, snapshot_len: float = math.inf, seed: int = 0,
+           root_base: int = 0, stream=None) -> List[Hop]:
+    """One-shot sampling call; returns per-hop outputs sliced to their sizes."""
+    smp = Sampler(max(int(roots.shape[0]), 0), fanouts, snapshots, device=roots.device)
+    smp.run(g, roots, root_ts, mode, snapshot_len, seed, root_base, stream)
+    return smp.hops()
+
+
+# --------------------------------------------------------------------------
+# kernel timers
+# --------------------------------------------------------------------------
+
+def timer_enable(capacity: int = 4096):
+    _check(lib().tgl_timer_enable(capacity), "tgl_timer_enable")
+
+
+def timer_disable():
+    _check(lib().tgl_timer_disable(), "tgl_timer_disable")
+
+
+def timer_reset():
+    _check(lib().tgl_timer_reset(), "tgl_timer_reset")
+
+
+def timer_read(kind: int):
+    ms = C.c_double()
+    n = C.c_int64()
+    _check(lib().tgl_timer_read(kind, C.byref(ms), C.byref(n)), "tgl_timer_read")
+    return ms.value, n.value

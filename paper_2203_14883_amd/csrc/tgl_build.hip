@@ -1,0 +1,375 @@
+// tgl_build.hip -- T-CSR build (Section 3.1, "The T-CSR Data Structure").
+//
+// Every directed entry i gets the 64-bit key (owner node << 32 | tskey),
+// where tskey maps a float timestamp to an unsigned integer with the same
+// order.  A stable least-significant-digit radix sort of (key, i) then leaves
+// each node's entries contiguous and sorted by (ts, i), which is the T-CSR
+// order.  The key-building kernel also OR- and AND-reduces all keys; digits on
+// which every key agrees are skipped (node ids above ceil(log2 N) bits, and
+// timestamp bytes that never change, e.g. the low mantissa bytes of integer
+// years).  Each radix pass is reduce-then-scan: per-tile digit counts, a
+// device-wide scan in digit-major order, and a scatter in which every
+// wavefront ranks its keys with ballots (stable within the tile), the tile is
+// reordered in LDS and written out bucket by bucket.
+//
+// The paper builds the T-CSR once on the host; here the same structure is
+// produced on the device from a COO that may be in any order.
+#include "tgl_internal.hpp"
+
+namespace tgl {
+namespace {
+
+constexpr int kRadixBits = 8;
+constexpr int kBins = 1 << kRadixBits;
+constexpr int kTileItems = 16;                    // keys per thread per radix tile
+constexpr int kTile = kBlock * kTileItems;        // 4096 keys
+constexpr int kWaves = kBlock / kWave;
+constexpr int kWaveTile = kTile / kWaves;         // 1024 keys per wavefront
+constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
+
+struct BuildFlags {
+    uint32_t err;
+    uint32_t pad;
+    uint64_t or_bits;
+    uint64_t and_bits;
+};
+
+__device__ __forceinline__ uint32_t ts_key(float t) {
+    const uint32_t b = __float_as_uint(t == 0.0f ? 0.0f : t);   // -0 -> +0
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ float key_ts(uint32_t k) {
+    const uint32_t b = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(b);
+}
+
+template <class T>
+__device__ __forceinline__ T wave_or(T v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) v |= __shfl_xor(v, d, kWave);
+    return v;
+}
+
+template <class T>
+__device__ __forceinline__ T wave_and(T v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) v &= __shfl_xor(v, d, kWave);
+    return v;
+}
+
+__global__ void init_flags_kernel(BuildFlags *f) {
+    f->err = 0;
+    f->pad = 0;
+    f->or_bits = 0;
+    f->and_bits = ~0ull;
+}
+
+// Entry i < m0: (src[i] -> dst[i]); entry m0 + i: (dst[i] -> src[i]).
+__global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict__ src,
+                                                      const int32_t *__restrict__ dst,
+                                                      const float *__restrict__ ts, int64_t m0,
+                                                      int64_t M, int64_t N,
+                                                      uint64_t *__restrict__ keys,
+                                                      uint32_t *__restrict__ vals,
+                                                      BuildFlags *__restrict__ flags) {
+    uint64_t o = 0, a = ~0ull;
+    bool bad = false;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < M; i += stride) {
+        const bool fwd = i < m0;
+        const int64_t k = fwd ? i : i - m0;
+        const int32_t u = fwd ? src[k] : dst[k];
+        const float t = ts[k];
+        if (fwd) {
+            const int32_t v = dst[k];
+            bad |= v < 0 || v >= N;
+        }
+        bad |= u < 0 || u >= N || t != t;
+        const uint64_t key = (static_cast<uint64_t>(static_cast<uint32_t>(u)) << 32) | ts_key(t);
+        keys[i] = key;
+        vals[i] = static_cast<uint32_t>(i);
+        o |= key;
+        a &= key;
+    }
+    o = wave_or(o);
+    a = wave_and(a);
+    const bool any_bad = __ballot(bad) != 0;
+    if (lane_id() == 0) {
+        atomicOr(reinterpret_cast<unsigned long long *>(&flags->or_bits), static_cast<unsigned long long>(o));
+        atomicAnd(reinterpret_cast<unsigned long long *>(&flags->and_bits), static_cast<unsigned long long>(a));
+        if (any_bad) atomicOr(&flags->err, 1u);
+    }
+}
+
+// Lanes of the wave whose (valid) digit equals this lane's digit.
+__device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < kRadixBits; b++) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t bb = __ballot(bit);
+        m &= bit ? bb : ~bb;
+    }
+    return m;
+}
+
+// Per-tile digit counts, stored digit-major: hist[d * ntiles + tile].
+__global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *__restrict__ keys,
+                                                               int64_t M, int shift,
+                                                               uint32_t *__restrict__ hist,
+                                                               int64_t ntiles) {
+    __shared__ uint32_t cnt[kBins];
+    cnt[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
+    const uint64_t lane_bit = 1ull << lane_id();
+#pragma unroll 4
+    for (int r = 0; r < kTileItems; r++) {
+        const int64_t idx = base + static_cast<int64_t>(r) * kBlock + threadIdx.x;
+        const bool valid = idx < M;
+        const uint32_t d = valid ? static_cast<uint32_t>(keys[idx] >> shift) & (kBins - 1) : 0u;
+        const uint64_t peers = match_digit(d, valid);
+        if (valid && (peers & (lane_bit - 1)) == 0) atomicAdd(&cnt[d], static_cast<uint32_t>(__popcll(peers)));
+    }
+    __syncthreads();
+    hist[static_cast<int64_t>(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
+}
+
+// Stable scatter of one tile by digit.  hist_off holds the exclusive scan of
+// hist (digit-major), i.e. where this tile's keys of digit d start.
+__global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
+    const uint64_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint64_t *__restrict__ kout,
+    uint32_t *__restrict__ vout, int64_t M, int shift, const uint32_t *__restrict__ hist_off,
+    int64_t ntiles) {
+    __shared__ uint64_t sk[kTile];
+    __shared__ uint32_t sv[kTile];
+    __shared__ uint32_t wcnt[kWaves][kBins];
+    __shared__ uint32_t bdo[kBins];
+    __shared__ uint32_t gofs[kBins];
+    __shared__ uint32_t scan_lds[kBlock / kWave];
+
+    const int w = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const uint64_t lane_bit = 1ull << lane;
+#pragma unroll
+    for (int i = 0; i < kWaves; i++) wcnt[i][threadIdx.x] = 0;
+    __syncthreads();
+
+    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kTile;
+    const int64_t base = tile0 + static_cast<int64_t>(w) * kWaveTile;
+    uint64_t key[kTileItems];
+    uint32_t val[kTileItems];
+    uint32_t rank[kTileItems];
+#pragma unroll
+    for (int r = 0; r < kTileItems; r++) {
+        const int64_t idx = base + static_cast<int64_t>(r) * kWave + lane;
+        const bool valid = idx < M;
+        key[r] = valid ? kin[idx] : ~0ull;
+        val[r] = valid ? vin[idx] : 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < kTileItems; r++) {
+        const int64_t idx = base + static_cast<int64_t>(r) * kWave + lane;
+        const bool valid = idx < M;
+        const uint32_t d = static_cast<uint32_t>(key[r] >> shift) & (kBins - 1);
+        const uint64_t peers = match_digit(d, valid);
+        const uint64_t below = peers & (lane_bit - 1);
+        const uint32_t prior = wcnt[w][d];
+        rank[r] = prior + static_cast<uint32_t>(__popcll(below));
+        if (valid && below == 0) wcnt[w][d] = prior + static_cast<uint32_t>(__popcll(peers));
+        // the next round's reads must follow this round's update
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    __syncthreads();
+
+    // per digit: exclusive bases across the waves, tile total, global offset
+    {
+        const int d = threadIdx.x;
+        uint32_t run = 0;
+#pragma unroll
+        for (int i = 0; i < kWaves; i++) {
+            const uint32_t c = wcnt[i][d];
+            wcnt[i][d] = run;
+            run += c;
+        }
+        gofs[d] = hist_off[static_cast<int64_t>(d) * ntiles + blockIdx.x];
+        uint32_t total;
+        bdo[d] = block_exclusive_sum<uint32_t>(run, scan_lds, &total);
+    }
+    __syncthreads();
+
+#pragma unroll
+    for (int r = 0; r < kTileItems; r++) {
+        const int64_t idx = base + static_cast<int64_t>(r) * kWave + lane;
+        if (idx < M) {
+            const uint32_t d = static_cast<uint32_t>(key[r] >> shift) & (kBins - 1);
+            const uint32_t pos = bdo[d] + wcnt[w][d] + rank[r];
+            sk[pos] = key[r];
+            sv[pos] = val[r];
+        }
+    }
+    __syncthreads();
+
+    const int64_t left = M - tile0;
+    const int n = left < kTile ? static_cast<int>(left) : kTile;
+    for (int i = threadIdx.x; i < n; i += kBlock) {
+        const uint64_t k = sk[i];
+        const uint32_t d = static_cast<uint32_t>(k >> shift) & (kBins - 1);
+        const int64_t g = static_cast<int64_t>(gofs[d]) + (i - static_cast<int64_t>(bdo[d]));
+        if (g >= 0 && g < M) {     // always true for consistent counts; keeps stores in bounds
+            kout[g] = k;
+            vout[g] = sv[i];
+        }
+    }
+}
+
+// Writes entries[p] from the sorted (key, i) and fills indptr: node x starts
+// at the first p whose owner is >= x.
+__global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict__ keys,
+                                                      const uint32_t *__restrict__ vals, int64_t M,
+                                                      int64_t m0, const int32_t *__restrict__ src,
+                                                      const int32_t *__restrict__ dst,
+                                                      const int64_t *__restrict__ eid, int64_t N,
+                                                      int64_t *__restrict__ indptr,
+                                                      int4 *__restrict__ ent) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
+        const uint64_t key = keys[p];
+        int64_t i = static_cast<int64_t>(vals[p]);
+        if (i >= M) i = 0;       // never taken for a permutation; keeps loads in bounds
+        const int64_t u = static_cast<int64_t>(key >> 32);
+        const float t = key_ts(static_cast<uint32_t>(key));
+        const bool fwd = i < m0;
+        const int64_t k = fwd ? i : i - m0;
+        const int32_t v = fwd ? dst[k] : src[k];
+        const int64_t e = eid ? eid[k] : k;
+        ent[p] = make_int4(v, __float_as_int(t), static_cast<int>(static_cast<uint32_t>(e)),
+                           static_cast<int>(static_cast<uint64_t>(e) >> 32));
+        // owners are in [0, N) after validation; the clamps only bound the stores
+        const int64_t uprev = p == 0 ? -1 : static_cast<int64_t>(keys[p - 1] >> 32);
+        const int64_t x1 = u < N ? u : N - 1;
+        for (int64_t x = uprev + 1; x <= x1; x++) indptr[x] = p;
+        if (p == M - 1)
+            for (int64_t x = (u < N ? u : N - 1) + 1; x <= N; x++) indptr[x] = M;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void fill_indptr_kernel(int64_t *__restrict__ indptr, int64_t n,
+                                                             int64_t value) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n; i += stride)
+        indptr[i] = value;
+}
+
+struct BuildWs {
+    BuildFlags *flags = nullptr;
+    uint64_t *keys[2] = {nullptr, nullptr};
+    uint32_t *vals[2] = {nullptr, nullptr};
+    uint32_t *hist = nullptr;
+    int64_t *partials = nullptr;
+    int64_t ntiles = 0;
+    size_t bytes = 0;
+};
+
+BuildWs carve_build_ws(void *base, int64_t M) {
+    BuildWs w;
+    Carver cv(base);
+    w.ntiles = (M + kTile - 1) / kTile;
+    w.flags = cv.take<BuildFlags>(1);
+    for (int i = 0; i < 2; i++) {
+        w.keys[i] = cv.take<uint64_t>(static_cast<size_t>(M));
+        w.vals[i] = cv.take<uint32_t>(static_cast<size_t>(M));
+    }
+    const int64_t nh = w.ntiles * kBins;
+    w.hist = cv.take<uint32_t>(static_cast<size_t>(nh));
+    w.partials = cv.take<int64_t>(static_cast<size_t>(scan_tiles(nh) + 1));
+    w.bytes = cv.size();
+    return w;
+}
+
+bool build_args_ok(int64_t num_edges, int64_t num_nodes, uint32_t flags) {
+    if (num_edges < 0 || num_nodes < 1 || num_nodes > INT32_MAX) return false;
+    if (flags & ~TGL_BUILD_UNDIRECTED) return false;
+    const int64_t M = (flags & TGL_BUILD_UNDIRECTED) ? 2 * num_edges : num_edges;
+    return M <= kMaxEntries && num_edges <= kMaxEntries;
+}
+
+unsigned grid_for(int64_t n, int64_t cap = 1 << 16) {
+    int64_t b = (n + kBlock - 1) / kBlock;
+    if (b < 1) b = 1;
+    if (b > cap) b = cap;
+    return static_cast<unsigned>(b);
+}
+
+}  // namespace
+}  // namespace tgl
+
+using namespace tgl;
+
+extern "C" {
+
+size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t flags) {
+    if (!build_args_ok(num_edges, num_nodes, flags)) return 0;
+    const int64_t M = (flags & TGL_BUILD_UNDIRECTED) ? 2 * num_edges : num_edges;
+    return carve_build_ws(nullptr, M).bytes;
+}
+
+tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
+                          const int64_t *eid, int64_t num_edges, int64_t num_nodes,
+                          uint32_t flags, int64_t *indptr, tgl_entry *entries,
+                          void *workspace, size_t workspace_bytes, void *stream) {
+    if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
+    if (num_edges > 0 && (!src || !dst || !ts || !entries)) return TGL_EINVAL;
+    if (!indptr) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
+    const int64_t m0 = num_edges;
+    const int64_t M = (flags & TGL_BUILD_UNDIRECTED) ? 2 * m0 : m0;
+    const BuildWs need = carve_build_ws(nullptr, M);
+    if (!workspace || workspace_bytes < need.bytes) return TGL_ENOSPACE;
+    const BuildWs w = carve_build_ws(workspace, M);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    ScopedTimer tm(TGL_TIMER_BUILD, st);
+
+    if (M == 0) {
+        fill_indptr_kernel<<<grid_for(num_nodes + 1), kBlock, 0, st>>>(indptr, num_nodes + 1, 0);
+        return launch_status();
+    }
+
+    init_flags_kernel<<<1, 1, 0, st>>>(w.flags);
+    keys_kernel<<<grid_for(M), kBlock, 0, st>>>(src, dst, ts, m0, M, num_nodes, w.keys[0], w.vals[0],
+                                                w.flags);
+    if (launch_status() != TGL_OK) return TGL_EDEVICE;
+    BuildFlags hf{};
+    if (hipMemcpyAsync(&hf, w.flags, sizeof(hf), hipMemcpyDeviceToHost, st) != hipSuccess)
+        return TGL_EDEVICE;
+    if (hipStreamSynchronize(st) != hipSuccess) return TGL_EDEVICE;
+    if (hf.err) return TGL_ERANGE;
+
+    const uint64_t varying = hf.or_bits ^ hf.and_bits;
+    int cur = 0;
+    const int64_t nh = w.ntiles * kBins;
+    const int64_t sc_tiles = scan_tiles(nh);
+    for (int shift = 0; shift < 64; shift += kRadixBits) {
+        if (((varying >> shift) & (kBins - 1)) == 0) continue;   // every key has this digit
+        radix_upsweep_kernel<<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift,
+                                                                                w.hist, w.ntiles);
+        scan_reduce_kernel<uint32_t><<<static_cast<unsigned>(sc_tiles), kBlock, 0, st>>>(
+            w.hist, nh, nullptr, w.partials);
+        launch_scan_partials(w.partials, sc_tiles, nullptr, st);
+        scan_apply_kernel<uint32_t, uint32_t><<<static_cast<unsigned>(sc_tiles), kBlock, 0, st>>>(
+            w.hist, w.hist, nh, nullptr, w.partials);
+        radix_downsweep_kernel<<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(
+            w.keys[cur], w.vals[cur], w.keys[cur ^ 1], w.vals[cur ^ 1], M, shift, w.hist, w.ntiles);
+        if (launch_status() != TGL_OK) return TGL_EDEVICE;
+        cur ^= 1;
+    }
+    emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes,
+                                               indptr, reinterpret_cast<int4 *>(entries));
+    return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,44 @@
+"""Helpers for GPU tests: device checks, uploads and host copies."""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+
+
+def announce(msg):
+    """Names the case about to run on the GPU (flushed, so a fault still shows it)."""
+    print("[gpu-case] " + msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch
+
+
+def upload(a, dtype=None):
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a if dtype is None else np.asarray(a, dtype)))
+    return t.cuda()
+
+
+def hops_to_numpy(hops):
+    return [dict(nbr=h.nbr.cpu().numpy(), eid=h.eid.cpu().numpy(), ts=h.ts.cpu().numpy(),
+                 dt=h.dt.cpu().numpy(), parent=None if h.parent is None else h.parent.cpu().numpy(),
+                 num_roots=h.num_roots) for h in hops]
+
+
+def tcsr_to_host(g):
+    ent = g.entries.cpu().numpy().reshape(-1, 2)
+    w = ent.view(np.int32).reshape(-1, 4)
+    return oracle.TCSR(g.indptr.cpu().numpy(), w[:, 0].copy(), ent[:, 1].copy(),
+                       w[:, 1].copy().view(np.float32))
+
+
+def upload_oracle_tcsr(g):
+    import paper_2203_14883_amd as P
+    return P.tcsr_from_host(g.indptr, g.nbr, g.ts, g.eid)

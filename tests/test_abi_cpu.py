@@ -1,0 +1,142 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports
+every function include/tgl.h declares, sizes its buffers consistently, and
+rejects invalid arguments before touching the device."""
+import ctypes as C
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2203_14883_amd as P
+from paper_2203_14883_amd import binding as B
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "tgl.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tgl_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTS)
+    L = P.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    assert L.tgl_version() == 10000
+
+
+def test_status_strings():
+    for s in (0, -1, -2, -3, -4):
+        assert P.status_str(s) and P.status_str(s) != "unknown status"
+    assert P.status_str(7) == "unknown status"
+
+
+def _fan(v):
+    a = np.asarray(v, np.int32)
+    return a, a.ctypes.data_as(C.c_void_p)
+
+
+def test_capacity_and_workspace():
+    L = P.lib()
+    a, p = _fan([10, 10])
+    assert L.tgl_sample_capacity(12000, 2, p, 1, 0) == 12000
+    assert L.tgl_sample_capacity(12000, 2, p, 1, 1) == 120000
+    assert L.tgl_sample_capacity(12000, 2, p, 1, 2) == 1200000
+    assert L.tgl_sample_capacity(180000, 2, p, 3, 2) == 180000 * 3 * 100
+    assert L.tgl_sample_capacity(10, 2, p, 1, 3) == -1
+    a, p = _fan([1024] * 8)
+    assert L.tgl_sample_capacity(10**6, 8, p, 1, 8) == -1          # beyond 2^62
+    assert L.tgl_sample_workspace(10**6, 8, p, 1) == 0
+    a, p = _fan([10])
+    assert L.tgl_sample_workspace(100, 1, p, 1) > 0                  # single hop: token size
+    a, p = _fan([10, 10, 10])
+    w2 = L.tgl_sample_workspace(1000, 2, _fan([10, 10])[1], 1)
+    w3 = L.tgl_sample_workspace(1000, 3, p, 1)
+    assert w3 > w2 > 0
+    assert L.tgl_tcsr_build_workspace(1000, 100, 1) > L.tgl_tcsr_build_workspace(1000, 100, 0) > 0
+    assert L.tgl_tcsr_build_workspace(-1, 100, 1) == 0
+    assert L.tgl_tcsr_build_workspace(10, 0, 1) == 0
+    assert L.tgl_tcsr_build_workspace(10, 10, 2) == 0
+    assert L.tgl_tcsr_build_workspace(2**31, 10, 1) == 0             # 2^32 entries
+    assert L.tgl_tcsr_build_workspace(2**31 - 1, 10, 1) > 0
+
+
+FAKE = 0x10000  # a non-null pointer value never dereferenced: every case fails a host check first
+
+
+def _sample_call(**kw):
+    L = P.lib()
+    args = dict(g=B.c_tcsr(10, 100, FAKE, FAKE), roots=FAKE, root_ts=FAKE, n=5, hops=2,
+                fan=[10, 10], mode=1, S=1, D=math.inf, ws=FAKE, ws_bytes=1 << 30)
+    args.update(kw)
+    fa, fp = _fan(args["fan"])
+    H = max(len(args["fan"]), 1)
+    outs = (B.c_hop_out * H)(*[B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE) for _ in range(H)])
+    if "outs" in kw:
+        outs = kw["outs"]
+    g = args["g"]
+    return L.tgl_sample(C.byref(g) if g is not None else None, args["roots"], args["root_ts"],
+                        args["n"], args["hops"], fp, args["mode"], args["S"], C.c_float(args["D"]),
+                        C.c_uint64(1), C.c_uint64(0), outs, kw.get("counts", FAKE), args["ws"],
+                        args["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(hops=0), dict(hops=9, fan=[1] * 9), dict(fan=[0, 10]), dict(fan=[10, 1025]),
+    dict(mode=2), dict(S=0), dict(S=65), dict(S=2, D=math.inf), dict(D=0.0), dict(D=-5.0),
+    dict(D=math.nan), dict(n=-1), dict(roots=None), dict(root_ts=None),
+    dict(g=B.c_tcsr(0, 100, FAKE, FAKE)), dict(g=B.c_tcsr(10, 100, None, FAKE)),
+    dict(g=B.c_tcsr(10, 100, FAKE, None)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE + 8)),
+    dict(g=B.c_tcsr(2**31, 100, FAKE, FAKE)), dict(g=None), dict(counts=None),
+])
+def test_sample_rejects_invalid_arguments(kw):
+    assert _sample_call(**kw) == B.EINVAL
+
+
+def test_sample_rejects_missing_outputs():
+    outs = (B.c_hop_out * 2)(B.c_hop_out(FAKE, FAKE, None, FAKE, None),
+                             B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE))
+    assert _sample_call(outs=outs) == B.EINVAL
+    outs = (B.c_hop_out * 2)(B.c_hop_out(FAKE, FAKE, FAKE, FAKE, None),
+                             B.c_hop_out(FAKE, FAKE, FAKE, FAKE, None))   # hop-2 parent missing
+    assert _sample_call(outs=outs) == B.EINVAL
+
+
+def test_sample_workspace_too_small():
+    assert _sample_call(ws_bytes=16) == B.ENOSPACE
+    assert _sample_call(ws=None) == B.ENOSPACE
+
+
+def _build_call(**kw):
+    L = P.lib()
+    a = dict(src=FAKE, dst=FAKE, ts=FAKE, eid=None, m=10, n=5, flags=1, indptr=FAKE,
+             ent=FAKE, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return L.tgl_tcsr_build(a["src"], a["dst"], a["ts"], a["eid"], a["m"], a["n"], a["flags"],
+                            a["indptr"], a["ent"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(m=-1), B.EINVAL), (dict(n=0), B.EINVAL), (dict(n=2**31), B.EINVAL),
+    (dict(flags=4), B.EINVAL), (dict(src=None), B.EINVAL), (dict(dst=None), B.EINVAL),
+    (dict(ts=None), B.EINVAL), (dict(ent=None), B.EINVAL), (dict(indptr=None), B.EINVAL),
+    (dict(ent=FAKE + 4), B.EINVAL), (dict(m=2**31), B.EINVAL),
+    (dict(ws_bytes=8), B.ENOSPACE), (dict(ws=None), B.ENOSPACE),
+])
+def test_build_rejects_invalid_arguments(kw, want):
+    assert _build_call(**kw) == want
+
+
+def test_timer_argument_checks():
+    L = P.lib()
+    ms, n = C.c_double(), C.c_int64()
+    assert L.tgl_timer_read(4, C.byref(ms), C.byref(n)) == B.EINVAL
+    assert L.tgl_timer_read(-1, C.byref(ms), C.byref(n)) == B.EINVAL
+    assert L.tgl_timer_read(0, None, C.byref(n)) == B.EINVAL
+    assert L.tgl_timer_enable(0) == B.EINVAL
+    assert L.tgl_timer_read(0, C.byref(ms), C.byref(n)) == 0 and n.value == 0
