@@ -43,13 +43,15 @@ T0 = time.time()
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
     ap.add_argument("--batches-per-step", type=int, default=None,
                     help="batches fused into one sampler call (default: 64 for c3/c4, 1 for c5, 263 for c2)")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="target duration of the CPU oracle baseline")
+    ap.add_argument("--cpu-batches", type=int, default=None,
+                    help="batches in the CPU oracle sample (default: one step)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="first run a plain 4 GiB device copy (for scaling byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--small", action="store_true", help="reduced graph size (development only)")
     return ap.parse_args()
@@ -101,46 +103,76 @@ def step_positions(nb, B, n):
     return [int(round(i * last / (n - 1))) for i in range(n)]
 
 
-def cpu_baseline(w, target_s):
-    """The oracle, single-threaded, on a bounded sample: the roots of a few
-    consecutive batches from the middle of the epoch, sampled over an oracle
-    T-CSR of the sub-graph of edges touching every node the sample reaches
-    (which gives those nodes exactly their full runs)."""
+def _owned_entries(w, nodes):
+    """Directed entries owned by ``nodes``: the forward entries of edges whose
+    source is in the set, then the reversed entries of edges whose destination
+    is in the set, each in input order.  Built into a T-CSR without the
+    undirected flag, this gives every node of the set exactly the run it has in
+    the full undirected T-CSR (same entries, same tie order)."""
+    from concurrent.futures import ThreadPoolExecutor
+    flag = np.zeros(w.num_nodes, dtype=bool)
+    flag[nodes] = True
+    n = w.num_edges
+    fwd = np.empty(n, dtype=bool)
+    rev = np.empty(n, dtype=bool)
+    chunk = 1 << 24
+
+    def f(c):
+        b, e = c * chunk, min(n, (c + 1) * chunk)
+        np.take(flag, w.src[b:e], out=fwd[b:e])
+        np.take(flag, w.dst[b:e], out=rev[b:e])
+
+    with ThreadPoolExecutor(16) as ex:
+        list(ex.map(f, range((n + chunk - 1) // chunk)))
+    fi = np.flatnonzero(fwd)
+    ri = np.flatnonzero(rev) if w.undirected else np.zeros(0, np.int64)
+    src = np.concatenate([w.src[fi], w.dst[ri]])
+    dst = np.concatenate([w.dst[fi], w.src[ri]])
+    ts = np.concatenate([w.ts[fi], w.ts[ri]])
+    eid = np.concatenate([fi, ri]).astype(np.int64)
+    return src, dst, ts, eid
+
+
+def cpu_baseline(w, nbatches):
+    """The oracle, single-threaded, on a bounded sample: the roots of
+    ``nbatches`` consecutive batches from the middle of the epoch (one GPU step
+    at the default size), over an oracle T-CSR that holds the full runs of every
+    node the sample reaches.  Only the oracle's sampling call is timed."""
     import oracle
-    nb = w.num_batches()
-    b0 = nb // 2
-
-    def subgraph(nodes):
-        flag = np.zeros(w.num_nodes, dtype=bool)
-        flag[nodes] = True
-        keep = flag[w.src] | flag[w.dst]
-        idx = np.nonzero(keep)[0]
-        return oracle.build_tcsr(w.src[idx], w.dst[idx], w.ts[idx], idx.astype(np.int64),
-                                 w.num_nodes, w.undirected)
-
-    def one(nbatches):
-        roots, rts, base = w.batches(b0, b0 + nbatches)
-        g1 = subgraph(np.unique(roots))
-        h1 = oracle.sample(g1, roots, rts, w.fanouts[:1], w.mode, w.snapshots, w.snapshot_len,
-                           w.sample_seed, base)
-        reach = np.unique(np.concatenate([roots, h1[0].nbr[h1[0].nbr >= 0]]))
-        g = subgraph(reach)
-        t = time.perf_counter()
-        out = oracle.sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
-                            w.sample_seed, base)
-        dt = time.perf_counter() - t
-        nbrs = int(sum(int((h.nbr >= 0).sum()) for h in out))
-        return dt, nbrs, len(roots)
-
-    dt, nbrs, nroots = one(1)
-    nbatches = 1
-    if dt < target_s:
-        nbatches = int(min(64, max(1, math.floor(target_s / max(dt, 1e-3)))))
-        if nbatches > 1:
-            dt, nbrs, nroots = one(nbatches)
+    b0 = w.num_batches() // 2
+    roots, rts, base = w.batches(b0, b0 + nbatches)
+    g1 = oracle.build_tcsr(*_owned_entries(w, np.unique(roots)), w.num_nodes, False)
+    reach = roots
+    for h in range(len(w.fanouts) - 1):      # nodes that become roots of the later hops
+        out = oracle.sample(g1, roots, rts, w.fanouts[:h + 1], w.mode, w.snapshots,
+                            w.snapshot_len, w.sample_seed, base)
+        reach = np.unique(np.concatenate([reach, out[h].nbr[out[h].nbr >= 0]]))
+        g1 = oracle.build_tcsr(*_owned_entries(w, reach), w.num_nodes, False)
+    t = time.perf_counter()
+    out = oracle.sample(g1, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
+                        w.sample_seed, base)
+    dt = time.perf_counter() - t
+    nbrs = int(sum(int((h.nbr >= 0).sum()) for h in out))
     return dict(value=nbrs / dt, unit="neighbours/s", cores=1, kind="oracle",
-                sample="%d roots (%d consecutive batches from batch %d) of %s, 2 hops, %d neighbours, %.2f s single-threaded"
-                       % (nroots, nbatches, b0, w.name, nbrs, dt))
+                sample="%d roots (%d consecutive batches from batch %d) of %s, %d hops, %d neighbours, "
+                       "%.2f s single-threaded (sampling call only; T-CSR of the reached sub-graph built beforehand)"
+                       % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, dt))
+
+
+def copy_calibration(dev, gib=4, reps=3):
+    """A plain device copy of known size, so byte counters can be scaled."""
+    import torch
+    n = gib << 30
+    a = torch.empty(n, dtype=torch.uint8, device=dev)
+    b = torch.empty_like(a)
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+    torch.cuda.empty_cache()
+    return dict(bytes_read=n, bytes_written=n, reps=reps)
 
 
 def main():
@@ -160,6 +192,8 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    if args.copy_calibration:
+        log("copy calibration: %s" % copy_calibration(dev))
     log("generating workload %s%s" % (args.workload, " (small)" if args.small else ""))
     w = make_workload(args.workload, args.small)
     log("graph: %d nodes, %d edges" % (w.num_nodes, w.num_edges))
@@ -258,7 +292,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("CPU oracle baseline")
-        cpu = cpu_baseline(w, args.cpu_seconds)
+        cpu = cpu_baseline(w, args.cpu_batches or B)
         log("CPU oracle: %.3g neighbours/s (%s)" % (cpu["value"], cpu["sample"]))
 
     line = {

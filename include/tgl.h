@@ -67,14 +67,19 @@ typedef struct tgl_entry {
  *   indptr   [device] int64[num_nodes + 1], indptr[0] = 0, non-decreasing,
  *                     indptr[num_nodes] = num_entries
  *   entries  [device] tgl_entry[num_entries], 16-byte aligned
- * The sampler clamps every indptr value into [0, num_entries], so a
- * malformed view yields wrong samples but never an out-of-bounds access.
+ *   ts       [device] float[num_entries], 16-byte aligned: ts[p] equals
+ *                     entries[p].ts.  The window search reads only this array
+ *                     (4 bytes per entry), the gather only `entries`.
+ * num_entries must be at most 2^32 - 1.  The sampler clamps every indptr
+ * value into [0, num_entries], so a malformed view yields wrong samples but
+ * never an out-of-bounds access.
  */
 typedef struct tgl_tcsr {
     int64_t num_nodes;
     int64_t num_entries;
     const int64_t *indptr;
     const tgl_entry *entries;
+    const float *ts;
 } tgl_tcsr;
 
 /*
@@ -123,7 +128,9 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  *   num_nodes  in [1, 2^31 - 1]
  *   flags      0 or TGL_BUILD_UNDIRECTED
  *   indptr     [device] int64[num_nodes + 1]  output
- *   entries    [device] tgl_entry[M]          output
+ *   entries    [device] tgl_entry[M]          output, 16-byte aligned
+ *   ts_out     [device] float[M]              output, 16-byte aligned: the
+ *                                             entries' timestamps again
  *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
  * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
  * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
@@ -133,7 +140,7 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  */
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
-                          uint32_t flags, int64_t *indptr, tgl_entry *entries,
+                          uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
                           void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */

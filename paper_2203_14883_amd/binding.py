@@ -41,7 +41,7 @@ class TglError(RuntimeError):
 
 class c_tcsr(C.Structure):
     _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
-                ("indptr", C.c_void_p), ("entries", C.c_void_p)]
+                ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p)]
 
 
 class c_hop_out(C.Structure):
@@ -69,7 +69,7 @@ def lib() -> C.CDLL:
     L.tgl_tcsr_build_workspace.restype = C.c_size_t
     L.tgl_tcsr_build_workspace.argtypes = [i64, i64, u32]
     L.tgl_tcsr_build.restype = i32
-    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, C.c_size_t, P]
+    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, C.c_size_t, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -119,9 +119,11 @@ def _i32_array(v: Sequence[int]):
 @dataclass
 class TCSR:
     """Device T-CSR: indptr int64[N+1]; entries int64[M, 2] holding the 16-byte
-    records (int32 nbr, float32 ts | int64 eid)."""
+    records (int32 nbr, float32 ts | int64 eid); ts float32[M], the entries'
+    timestamps as the separate search array."""
     indptr: torch.Tensor
     entries: torch.Tensor
+    ts: torch.Tensor
     num_nodes: int
 
     @property
@@ -133,7 +135,7 @@ class TCSR:
         return self.entries.view(torch.int32)[:, 0]
 
     @property
-    def ts(self) -> torch.Tensor:
+    def entry_ts(self) -> torch.Tensor:
         return self.entries.view(torch.float32)[:, 1]
 
     @property
@@ -141,8 +143,9 @@ class TCSR:
         return self.entries[:, 1]
 
     def c_view(self) -> c_tcsr:
-        return c_tcsr(self.num_nodes, self.num_entries, self.indptr.data_ptr(),
-                      self.entries.data_ptr() if self.num_entries else None)
+        m = self.num_entries
+        return c_tcsr(self.num_nodes, m, self.indptr.data_ptr(),
+                      self.entries.data_ptr() if m else None, self.ts.data_ptr() if m else None)
 
 
 def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray:
@@ -159,9 +162,11 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda") -> TCSR:
     """Uploads a T-CSR given as host arrays (e.g. one built elsewhere)."""
     rec = pack_entries(nbr, ts, eid)
     ent = torch.from_numpy(rec).to(device)
+    tsa = torch.from_numpy(np.ascontiguousarray(np.asarray(ts, np.float32))).to(device)
     if ent.shape[0] == 0:
         ent = torch.empty((0, 2), dtype=torch.int64, device=device)
-    return TCSR(torch.from_numpy(np.asarray(indptr, np.int64)).to(device), ent, len(indptr) - 1)
+        tsa = torch.empty(0, dtype=torch.float32, device=device)
+    return TCSR(torch.from_numpy(np.asarray(indptr, np.int64)).to(device), ent, tsa, len(indptr) - 1)
 
 
 def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:
@@ -185,6 +190,7 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     dev = src.device
     indptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
     entries = torch.empty((M, 2), dtype=torch.int64, device=dev)
+    tsa = torch.empty(M, dtype=torch.float32, device=dev)
     need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
     if need == 0:
         raise TglError(EINVAL, "tgl_tcsr_build_workspace")
@@ -192,11 +198,12 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     if own_ws:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     s = L.tgl_tcsr_build(_p(src), _p(dst), _p(ts), _p(eid), m0, num_nodes, flags, _p(indptr),
-                         _p(entries) if M else None, _p(workspace), workspace.numel(), _stream(stream))
+                         _p(entries) if M else None, _p(tsa) if M else None, _p(workspace),
+                         workspace.numel(), _stream(stream))
     if own_ws:
         del workspace
     _check(s, "tgl_tcsr_build")
-    return TCSR(indptr, entries, num_nodes)
+    return TCSR(indptr, entries, tsa, num_nodes)
 
 
 # --------------------------------------------------------------------------

@@ -234,7 +234,8 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
                                                       const int32_t *__restrict__ dst,
                                                       const int64_t *__restrict__ eid, int64_t N,
                                                       int64_t *__restrict__ indptr,
-                                                      int4 *__restrict__ ent) {
+                                                      int4 *__restrict__ ent,
+                                                      float *__restrict__ ts_out) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
     for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
         const uint64_t key = keys[p];
@@ -248,6 +249,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
         const int64_t e = eid ? eid[k] : k;
         ent[p] = make_int4(v, __float_as_int(t), static_cast<int>(static_cast<uint32_t>(e)),
                            static_cast<int>(static_cast<uint64_t>(e) >> 32));
+        ts_out[p] = t;
         // owners are in [0, N) after validation; the clamps only bound the stores
         const int64_t uprev = p == 0 ? -1 : static_cast<int64_t>(keys[p - 1] >> 32);
         const int64_t x1 = u < N ? u : N - 1;
@@ -319,12 +321,13 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
-                          uint32_t flags, int64_t *indptr, tgl_entry *entries,
+                          uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
                           void *workspace, size_t workspace_bytes, void *stream) {
     if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
-    if (num_edges > 0 && (!src || !dst || !ts || !entries)) return TGL_EINVAL;
+    if (num_edges > 0 && (!src || !dst || !ts || !entries || !ts_out)) return TGL_EINVAL;
     if (!indptr) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(ts_out) & 15u) != 0) return TGL_EINVAL;
     const int64_t m0 = num_edges;
     const int64_t M = (flags & TGL_BUILD_UNDIRECTED) ? 2 * m0 : m0;
     const BuildWs need = carve_build_ws(nullptr, M);
@@ -368,7 +371,7 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         cur ^= 1;
     }
     emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes,
-                                               indptr, reinterpret_cast<int4 *>(entries));
+                                               indptr, reinterpret_cast<int4 *>(entries), ts_out);
     return launch_status();
 }
 

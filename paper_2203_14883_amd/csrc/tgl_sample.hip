@@ -6,16 +6,22 @@
 // is its fallback for layers >= 2.  On the GPU every root is served by a group
 // of G lanes of one wavefront, with no shared mutable state:
 //
-//   1. window location: a G-ary search over the root's time-sorted run (G
-//      probes per round, combined with one ballot), so a run of d entries takes
-//      about log_{G+1}(d) dependent loads instead of log_2(d);
+//   1. window location: the root's run is [indptr[x], indptr[x+1]).  The
+//      search reads only the T-CSR's separate timestamp array.  A run of up to
+//      4G - 3 entries is loaded whole, four timestamps per lane (one 16-byte
+//      load each), and every window edge is a few ballots over it; a longer run
+//      is first narrowed G-ary (G probes per round, one ballot), about
+//      log_{G+1}(d / 4G) dependent loads, then finished the same way;
 //   2. selection: lane j of the group takes slot j (most recent: the j-th
 //      newest candidate; uniform: a counter-hash draw keyed by the root's path);
-//   3. gather + emit: one aligned 16-byte load of the T-CSR entry per slot,
-//      and structure-of-arrays stores of (nbr, eid, ts, dt);
-//   4. compaction: valid slots form a prefix of every (root, window) group, so
-//      a device-wide scan over per-group counts gives each next-hop root its
-//      index; the emit step writes the next hop's roots and parent indices.
+//   3. gather + emit: one aligned 16-byte load of the chosen T-CSR record per
+//      slot; slots are written as structure-of-arrays (nbr, eid, ts, dt);
+//   4. next hop: valid slots are a prefix of every (root, window) group, so an
+//      exclusive scan of the per-group counts gives every next-hop root its
+//      index.  The next hop's kernel walks the previous hop's slots directly
+//      ("virtual roots"): each wavefront loads 64 of them, compacts the valid
+//      ones through LDS, and serves them G lanes per root.  No list of next-hop
+//      roots is materialised.
 //
 // Nothing is synchronised with the host: per-hop root counts stay on the
 // device and the next hop's kernels read them.
@@ -26,6 +32,7 @@ namespace {
 
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
 constexpr int kMaxGrid = 1 << 16;     // cap on blocks of the grid-stride hop kernels
+constexpr int kWavesPerBlock = kBlock / kWave;
 
 __host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
     z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
@@ -36,57 +43,100 @@ __host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
 struct HopArgs {
     // graph
     const int64_t *indptr;
-    const int4 *ent;          // tgl_entry viewed as 16-byte vectors
+    const int4 *ent;            // tgl_entry viewed as 16-byte vectors
+    const float *tsa;           // timestamps of the entries (search array)
     int64_t num_nodes;
     int64_t num_entries;
-    // roots of this hop
+    // hop 1: dense roots
     const int32_t *rx;
     const float *rt;
-    const int32_t *rs;        // inherited window (hops >= 2), null on hop 1
-    const uint64_t *rpath;    // path of each root (hops >= 2), null on hop 1
-    uint64_t root_base;
-    int64_t count_static;
-    const int64_t *count_dyn; // number of roots, read on the device (hops >= 2)
+    int64_t num_roots;
+    // hops >= 2: the previous hop's slots are the candidate roots
+    const int32_t *p_nbr;
+    const float *p_ts;
+    const int64_t *p_off;       // exclusive offsets of the previous hop's groups
+    const int32_t *p_s;         // window of each previous-hop group (null: hop 1 groups)
+    const uint64_t *p_path;     // path of each previous-hop group (null: hop 1 groups)
+    int32_t p_k;                // fanout of the previous hop
+    int64_t p_groups_static;    // previous hop's groups (hop 1 groups: R*S) ...
+    const int64_t *p_groups_dyn; // ... or read on the device (roots of hop >= 2)
     // parameters
-    int32_t hop;              // 1-based
+    uint64_t root_base;
+    int32_t S;                  // snapshots
+    int32_t hop;                // 1-based
     int32_t k;
-    int32_t windows;          // windows per root: S on hop 1, 1 afterwards
+    int32_t windows;            // windows per root: S on hop 1, 1 afterwards
     float delta;
     int32_t delta_inf;
-    uint64_t seedmix;         // mix64(seed ^ golden)
+    uint64_t seedmix;           // mix64(seed ^ golden)
     // outputs
     int32_t *o_nbr;
     int64_t *o_eid;
     float *o_ts;
     float *o_dt;
-    int32_t *o_cnt;           // valid slots per (root, window) group, or null
-    int64_t *count0_out;      // hop 1 stores its root count here
+    int64_t *o_parent;          // hops >= 2
+    int32_t *o_cnt;             // valid slots per (root, window) group, or null (last hop)
+    int32_t *o_s;               // window of each root, for a later hop (or null)
+    uint64_t *o_path;           // path of each root, for a later hop (or null)
+    int64_t *count0_out;        // hop 1 stores its root count here
 };
 
-__device__ __forceinline__ float entry_ts(const int4 *ent, int64_t p) {
-    return __int_as_float(reinterpret_cast<const int *>(ent + p)[1]);
+// ts[p4 .. p4+3] for p4 a multiple of 4; entries at or past M read as +inf
+// (they are never inside a window).
+__device__ __forceinline__ float4 load_ts4(const float *__restrict__ tsa, uint32_t p4, uint32_t M) {
+    if (static_cast<uint64_t>(p4) + 3 < M) return *reinterpret_cast<const float4 *>(tsa + p4);
+    const float inf = __builtin_inff();
+    float4 r = make_float4(inf, inf, inf, inf);
+    if (p4 < M) r.x = tsa[p4];
+    if (static_cast<uint64_t>(p4) + 1 < M) r.y = tsa[p4 + 1];
+    if (static_cast<uint64_t>(p4) + 2 < M) r.z = tsa[p4 + 2];
+    return r;
+}
+
+// Entries [lo, hi) of a sorted run, held four per lane: lane gl holds
+// c4 + 4*gl .. c4 + 4*gl + 3.  Returns lo + #{p in [lo, hi): (double)ts[p] < v}.
+template <int G>
+__device__ __forceinline__ uint32_t count_held(float4 v4, uint32_t c4, uint32_t lo, uint32_t hi, double v, int gl) {
+    const uint32_t p = c4 + 4 * static_cast<uint32_t>(gl);
+    int c = __popcll(group_ballot<G>(p >= lo && p < hi && static_cast<double>(v4.x) < v));
+    c += __popcll(group_ballot<G>(p + 1 >= lo && p + 1 < hi && static_cast<double>(v4.y) < v));
+    c += __popcll(group_ballot<G>(p + 2 >= lo && p + 2 < hi && static_cast<double>(v4.z) < v));
+    c += __popcll(group_ballot<G>(p + 3 >= lo && p + 3 < hi && static_cast<double>(v4.w) < v));
+    return lo + c;
+}
+
+// Longest range [lo, hi) that one held load covers: c4 = lo & ~3 and
+// [c4, c4 + 4G) must contain it.
+template <int G>
+constexpr uint32_t held_span() { return 4 * G - 3; }
+
+template <int G>
+__device__ __forceinline__ float4 load_held(const float *__restrict__ tsa, uint32_t c4, uint32_t hi, uint32_t M, int gl) {
+    const uint32_t p4 = c4 + 4 * static_cast<uint32_t>(gl);
+    const float inf = __builtin_inff();
+    return p4 < hi ? load_ts4(tsa, p4, M) : make_float4(inf, inf, inf, inf);
 }
 
 // Number of entries p in [lo, hi) of a time-sorted run with (double)ts[p] < v,
-// found by the G lanes of one group together.  Each round probes G evenly
-// spaced positions; the probes below v form a prefix, whose length narrows the
-// range to one gap.  A NaN bound compares false everywhere and gives lo.
+// found by the G lanes of one group together.  While the range is longer than
+// one held load, each round probes G evenly spaced positions; the probes below
+// v form a prefix, whose length narrows the range to one gap.  A NaN bound
+// compares false everywhere and gives lo.
 template <int G>
-__device__ __forceinline__ int64_t count_below(const int4 *__restrict__ ent, int64_t lo, int64_t hi,
-                                               double v, int gl) {
-    while (hi - lo > G) {
-        const int64_t len = hi - lo;
-        const int64_t pos = lo + (static_cast<int64_t>(gl + 1) * len) / (G + 1);
-        const bool below = static_cast<double>(entry_ts(ent, pos)) < v;
+__device__ __forceinline__ uint32_t count_below(const float *__restrict__ tsa, uint32_t lo, uint32_t hi,
+                                                uint32_t M, double v, int gl) {
+    while (hi - lo > held_span<G>()) {
+        const uint64_t len = hi - lo;
+        const uint32_t pos = lo + static_cast<uint32_t>((static_cast<uint64_t>(gl + 1) * len) / (G + 1));
+        const bool below = static_cast<double>(tsa[pos]) < v;
         const int c = __popcll(group_ballot<G>(below));
-        const int64_t nlo = c > 0 ? lo + (static_cast<int64_t>(c) * len) / (G + 1) + 1 : lo;
-        const int64_t nhi = c < G ? lo + (static_cast<int64_t>(c + 1) * len) / (G + 1) : hi;
+        const uint32_t nlo = c > 0 ? lo + static_cast<uint32_t>((static_cast<uint64_t>(c) * len) / (G + 1)) + 1 : lo;
+        const uint32_t nhi = c < G ? lo + static_cast<uint32_t>((static_cast<uint64_t>(c + 1) * len) / (G + 1)) : hi;
         lo = nlo;
         hi = nhi;
     }
-    const int64_t pos = lo + gl;
-    const bool below = pos < hi && static_cast<double>(entry_ts(ent, pos)) < v;
-    return lo + __popcll(group_ballot<G>(below));
+    const uint32_t c4 = lo & ~3u;
+    return count_held<G>(load_held<G>(tsa, c4, hi, M, gl), c4, lo, hi, v, gl);
 }
 
 __device__ __forceinline__ double bound_value(float t, int32_t i, float delta) {
@@ -96,16 +146,14 @@ __device__ __forceinline__ double bound_value(float t, int32_t i, float delta) {
 }
 
 template <bool LAST>
-__device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, int64_t pick, float t) {
+__device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, bool valid, int4 v, float t) {
     int32_t nbr = -1;
     int64_t eid = -1;
     float ts = -1.0f, dt = -1.0f;
-    if (pick >= 0) {
-        const int4 v = p.ent[pick];
+    if (valid) {
         nbr = v.x;
         ts = __int_as_float(v.y);
-        eid = static_cast<int64_t>(static_cast<uint32_t>(v.z)) |
-              (static_cast<int64_t>(v.w) << 32);
+        eid = static_cast<int64_t>(static_cast<uint32_t>(v.z)) | (static_cast<int64_t>(v.w) << 32);
         dt = static_cast<float>(static_cast<double>(t) - static_cast<double>(ts));
     }
     if constexpr (LAST) {
@@ -121,206 +169,242 @@ __device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, int64_t p
     }
 }
 
-// One group of G lanes per root; MULTI: hop-1 roots with S > 1 windows (the
-// window edges live in LDS), otherwise one window per root in registers.
+__device__ __forceinline__ void wave_sync_lds() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Window location, selection and emission for one root whose run is
+// [a, b), queried at time t (window s0 unless MULTI, path) and whose slots
+// start at q * windows * k.  All G lanes of the group call it together.
 template <int G, int MODE, bool MULTI, bool LAST>
-__global__ __launch_bounds__(kBlock) void hop_kernel(const HopArgs p) {
-    constexpr int GPB = kBlock / G;
-    const int gl = threadIdx.x & (G - 1);
-    const int grp = threadIdx.x / G;
-    __shared__ int64_t edges[MULTI ? GPB * (TGL_MAX_SNAPSHOTS + 1) : 1];
-    int64_t *my_edges = edges + (MULTI ? grp * (TGL_MAX_SNAPSHOTS + 1) : 0);
+__device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32_t a, uint32_t b, float t,
+                                             int32_t s0, uint64_t hp, int gl, uint32_t *my_edges) {
+    const uint32_t M = static_cast<uint32_t>(p.num_entries);
+    // a run short enough is loaded once and serves every window edge
+    const bool held = b - a <= held_span<G>();        // group-uniform
+    const uint32_t c4 = a & ~3u;
+    float4 v4;
+    if (held) v4 = load_held<G>(p.tsa, c4, b, M, gl);
 
-    const int64_t count = p.count_dyn ? *p.count_dyn : p.count_static;
-    if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = count;
-    const int64_t M = p.num_entries;
-    const int W = p.windows;
+    const int W = MULTI ? p.windows : 1;
     const int k = p.k;
+    uint32_t lo = a, hi = a;
+    if constexpr (MULTI) {
+        // edges i = 0..W: window s spans [edge s+1, edge s)
+        for (int i = 0; i <= W; i++) {
+            const double v = bound_value(t, i, p.delta);
+            const uint32_t c = held ? count_held<G>(v4, c4, a, b, v, gl) : count_below<G>(p.tsa, a, b, M, v, gl);
+            if (gl == 0) my_edges[i] = c;
+        }
+        wave_sync_lds();
+    } else {
+        const double vh = bound_value(t, s0, p.delta);
+        hi = held ? count_held<G>(v4, c4, a, b, vh, gl) : count_below<G>(p.tsa, a, b, M, vh, gl);
+        if (!p.delta_inf) {
+            const double vl = bound_value(t, s0 + 1, p.delta);
+            lo = held ? count_held<G>(v4, c4, a, b, vl, gl) : count_below<G>(p.tsa, a, b, M, vl, gl);
+        }
+        if (lo > hi) lo = hi;
+    }
 
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * GPB + grp; q < count;
-         q += static_cast<int64_t>(gridDim.x) * GPB) {
-        const int32_t x = p.rx[q];
-        const float t = p.rt[q];
-        const int32_t s0 = p.rs ? p.rs[q] : 0;
-        const uint64_t path = p.rpath ? p.rpath[q] : p.root_base + static_cast<uint64_t>(q);
+    const int nslots = W * k;
+    const int64_t obase = q * static_cast<int64_t>(nslots);
+    for (int base = 0; base < nslots; base += G) {   // group-uniform trip count
+        const int e = base + gl;
+        int s, j;
+        uint32_t wlo, whi;
+        if constexpr (MULTI) {
+            const int ee = e < nslots ? e : nslots - 1;
+            s = ee / k;
+            j = ee - s * k;
+            whi = my_edges[s];
+            wlo = my_edges[s + 1];
+            if (wlo > whi) wlo = whi;
+        } else {
+            s = s0;
+            j = e;
+            whi = hi;
+            wlo = lo;
+        }
+        const uint32_t n = whi - wlo;
+        bool has = false;
+        uint32_t pick = 0;
+        if constexpr (MODE == TGL_MOST_RECENT) {
+            has = static_cast<uint32_t>(j) < n;
+            pick = whi - 1 - static_cast<uint32_t>(j);
+        } else {
+            has = n > 0;
+            const uint64_t key = (static_cast<uint64_t>(p.hop) << 40) |
+                                 (static_cast<uint64_t>(s) << 24) | static_cast<uint64_t>(j);
+            pick = wlo + static_cast<uint32_t>(__umul64hi(mix64(hp ^ key), static_cast<uint64_t>(n)));
+        }
+        const bool valid = e < nslots && has;
+        const int4 v = valid ? p.ent[pick] : make_int4(-1, -1, -1, -1);
+        if (e < nslots) emit_slot<LAST>(p, obase + e, valid, v, t);
+    }
 
+    if (p.o_cnt) {
+        for (int w = gl; w < W; w += G) {
+            uint32_t whi = MULTI ? my_edges[w] : hi;
+            uint32_t wlo = MULTI ? my_edges[w + 1] : lo;
+            if (wlo > whi) wlo = whi;
+            const uint32_t n = whi - wlo;
+            const int32_t c = MODE == TGL_MOST_RECENT ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
+                                                      : (n > 0 ? k : 0);
+            p.o_cnt[q * W + w] = c;
+        }
+    }
+    if constexpr (MULTI) wave_sync_lds();   // my_edges is rewritten by the next root
+}
+
+// One hop.  Each wavefront takes chunks of 64 candidate roots:
+//   phase 1, one lane per candidate: hop 1 takes root v as given; later hops
+//     take slot v of the previous hop, valid when its nbr >= 0, as the root
+//     with index off[v / k_prev] + v % k_prev (and write its parent index).
+//     Every lane loads its root's time and run bounds; the valid roots are
+//     packed, in order, into LDS;
+//   phase 2, G lanes per root, 64 / G roots per round: search, select, emit.
+template <int G, int MODE, bool MULTI, bool LAST, bool FIRST>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) void hop_kernel(const HopArgs p) {
+    constexpr int GPW = kWave / G;            // roots served per wavefront round
+    constexpr int GPB = kBlock / G;
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int gl = lane & (G - 1);
+    const int gw = lane / G;
+    __shared__ uint32_t r_a[kWavesPerBlock][kWave];
+    __shared__ uint32_t r_b[kWavesPerBlock][kWave];
+    __shared__ int64_t r_q[kWavesPerBlock][kWave];
+    __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
+    __shared__ float r_t[kWavesPerBlock][kWave];
+    __shared__ int32_t r_s[kWavesPerBlock][kWave];
+    __shared__ uint32_t edges[MULTI ? GPB * (TGL_MAX_SNAPSHOTS + 1) : 1];
+    uint32_t *my_edges = edges + (MULTI ? (w * GPW + gw) * (TGL_MAX_SNAPSHOTS + 1) : 0);
+
+    const int64_t M = p.num_entries;
+    const int64_t pk = FIRST ? 1 : p.p_k;
+    int64_t nv;
+    if constexpr (FIRST) {
+        nv = p.num_roots;
+        if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = nv;
+    } else {
+        const int64_t groups = p.p_groups_dyn ? *p.p_groups_dyn : p.p_groups_static;
+        nv = groups * pk;
+    }
+    const int64_t nchunks = (nv + kWave - 1) / kWave;
+    const uint64_t S = static_cast<uint64_t>(p.S);
+    const uint64_t path1 = p.root_base * S * static_cast<uint64_t>(pk);   // hop-1 children: + v
+    const uint64_t lane_bit = 1ull << lane;
+
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w; c < nchunks;
+         c += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
+        // ---- phase 1: one lane per candidate root ----
+        const int64_t v = c * kWave + lane;
+        bool valid;
+        int32_t x = -1;
+        float t = 0.0f;
+        int64_t q = 0;
+        int32_t s = 0;
+        uint64_t path = 0;
+        if constexpr (FIRST) {
+            valid = v < nv;
+            if (valid) {
+                x = p.rx[v];
+                t = p.rt[v];
+                q = v;
+                path = p.root_base + static_cast<uint64_t>(v);
+            }
+        } else {
+            x = v < nv ? p.p_nbr[v] : -1;
+            valid = x >= 0;
+            if (valid) {
+                t = p.p_ts[v];
+                const int64_t g = v / pk;
+                const int64_t j = v - g * pk;
+                q = p.p_off[g] + j;
+                if (p.p_s) {
+                    s = p.p_s[g];
+                    path = p.p_path[g] * static_cast<uint64_t>(pk) + static_cast<uint64_t>(j);
+                } else {
+                    s = static_cast<int32_t>(static_cast<uint64_t>(g) % S);
+                    path = path1 + static_cast<uint64_t>(v);
+                }
+                p.o_parent[q] = v;
+                if (p.o_s) {
+                    p.o_s[q] = s;
+                    p.o_path[q] = path;
+                }
+            }
+        }
         int64_t a = 0, b = 0;
-        if (x >= 0 && x < p.num_nodes) {
+        if (valid && x >= 0 && x < p.num_nodes) {
             a = p.indptr[x];
             b = p.indptr[x + 1];
             a = a < 0 ? 0 : (a > M ? M : a);
             b = b < a ? a : (b > M ? M : b);
         }
-
-        int64_t lo = a, hi = a;
-        if constexpr (MULTI) {
-            // edges i = 0..W: window s spans [edge s+1, edge s)
-            for (int i = 0; i <= W; i++) {
-                const int64_t c = count_below<G>(p.ent, a, b, bound_value(t, i, p.delta), gl);
-                if (gl == 0) my_edges[i] = c;
-            }
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        } else {
-            hi = count_below<G>(p.ent, a, b, bound_value(t, s0, p.delta), gl);
-            if (!p.delta_inf) lo = count_below<G>(p.ent, a, b, bound_value(t, s0 + 1, p.delta), gl);
-            if (lo > hi) lo = hi;
+        const uint64_t mask = __ballot(valid);
+        if (valid) {
+            const int r = __popcll(mask & (lane_bit - 1));
+            r_a[w][r] = static_cast<uint32_t>(a);
+            r_b[w][r] = static_cast<uint32_t>(b);
+            r_q[w][r] = q;
+            r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
+            r_t[w][r] = t;
+            r_s[w][r] = s;
         }
-
-        const uint64_t hp = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
-        const int64_t obase = q * static_cast<int64_t>(W) * k;
-        for (int e = gl; e < W * k; e += G) {
-            int s, j;
-            int64_t wlo, whi;
-            if constexpr (MULTI) {
-                s = e / k;
-                j = e - s * k;
-                whi = my_edges[s];
-                wlo = my_edges[s + 1];
-                if (wlo > whi) wlo = whi;
-            } else {
-                s = s0;
-                j = e;
-                whi = hi;
-                wlo = lo;
-            }
-            const int64_t n = whi - wlo;
-            int64_t pick = -1;
-            if constexpr (MODE == TGL_MOST_RECENT) {
-                if (j < n) pick = whi - 1 - j;
-            } else {
-                if (n > 0) {
-                    const uint64_t key = (static_cast<uint64_t>(p.hop) << 40) |
-                                         (static_cast<uint64_t>(s) << 24) | static_cast<uint64_t>(j);
-                    pick = wlo + static_cast<int64_t>(__umul64hi(mix64(hp ^ key), static_cast<uint64_t>(n)));
-                }
-            }
-            emit_slot<LAST>(p, obase + e, pick, t);
-        }
-
-        if (p.o_cnt) {
-            for (int w = gl; w < W; w += G) {
-                int64_t whi = MULTI ? my_edges[w] : hi;
-                int64_t wlo = MULTI ? my_edges[w + 1] : lo;
-                if (wlo > whi) wlo = whi;
-                const int64_t n = whi - wlo;
-                const int32_t c = MODE == TGL_MOST_RECENT ? static_cast<int32_t>(n < k ? n : k)
-                                                          : (n > 0 ? k : 0);
-                p.o_cnt[q * W + w] = c;
+        wave_sync_lds();
+        // ---- phase 2: G lanes per root ----
+        const int nvalid = __popcll(mask);
+        for (int base = 0; base < nvalid; base += GPW) {
+            const int i = base + gw;
+            if (i < nvalid) {                       // group-uniform
+                process_root<G, MODE, MULTI, LAST>(p, r_q[w][i], r_a[w][i], r_b[w][i], r_t[w][i], r_s[w][i],
+                                                   r_hp[w][i], gl, my_edges);
             }
         }
-        if constexpr (MULTI) {
-            // the next root of this group rewrites my_edges
-            __builtin_amdgcn_wave_barrier();
-        }
-    }
-}
-
-struct EmitArgs {
-    const int32_t *cnt;       // valid slots per group of hop h
-    const int64_t *partials;  // exclusive tile offsets
-    int64_t n_static;
-    const int64_t *n_dyn;     // number of groups (hops >= 2: roots of hop h)
-    int32_t k;                // fanout of hop h
-    int32_t windows;          // S on hop 1, else 1
-    int32_t hop;              // h
-    uint64_t root_base;
-    // hop-h slots and roots
-    const int32_t *h_nbr;
-    const float *h_ts;
-    const int32_t *h_rs;      // hop >= 2: window of each hop-h root
-    const uint64_t *h_rpath;  // hop >= 2: path of each hop-h root
-    // next-hop roots
-    int32_t *nx;
-    float *nt;
-    int32_t *ns;
-    uint64_t *npath;
-    int64_t *parent;
-};
-
-// Exclusive offsets of the per-group counts, then one next-hop root per valid
-// slot: group g holds slots g*k .. g*k + cnt[g] - 1 (valid slots are a prefix).
-__global__ __launch_bounds__(kBlock) void compact_emit_kernel(const EmitArgs p) {
-    __shared__ int64_t lds[kBlock / kWave];
-    const int64_t n = p.n_dyn ? *p.n_dyn : p.n_static;
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile +
-                         static_cast<int64_t>(threadIdx.x) * kScanItems;
-    int32_t c[kScanItems];
-    int64_t sum = 0;
-#pragma unroll
-    for (int i = 0; i < kScanItems; i++) {
-        const int64_t g = base + i;
-        c[i] = g < n ? p.cnt[g] : 0;
-        sum += c[i];
-    }
-    int64_t total;
-    int64_t q = block_exclusive_sum<int64_t>(sum, lds, &total) + p.partials[blockIdx.x];
-    const uint64_t S = static_cast<uint64_t>(p.windows);
-    const uint64_t k = static_cast<uint64_t>(p.k);
-#pragma unroll
-    for (int i = 0; i < kScanItems; i++) {
-        const int64_t g = base + i;
-        if (g >= n) break;
-        int32_t s;
-        uint64_t child0;   // path of the child of slot j is child0 + j
-        if (p.hop == 1) {
-            const uint64_t r = static_cast<uint64_t>(g) / S;
-            s = static_cast<int32_t>(static_cast<uint64_t>(g) - r * S);
-            child0 = (p.root_base + r) * S * k + static_cast<uint64_t>(s) * k;
-        } else {
-            s = p.h_rs[g];
-            child0 = p.h_rpath[g] * k;
-        }
-        for (int j = 0; j < c[i]; j++) {
-            const int64_t slot = g * p.k + j;
-            p.nx[q] = p.h_nbr[slot];
-            p.nt[q] = p.h_ts[slot];
-            p.ns[q] = s;
-            p.npath[q] = child0 + static_cast<uint64_t>(j);
-            p.parent[q] = slot;
-            q++;
-        }
+        wave_sync_lds();                            // the next chunk rewrites the LDS rows
     }
 }
 
 template <int G, int MODE, bool MULTI, bool LAST>
-void launch_hop_g(const HopArgs &a, int64_t groups_cap, hipStream_t st) {
-    constexpr int GPB = kBlock / G;
-    int64_t blocks = (groups_cap + GPB - 1) / GPB;
+void launch_g(bool first, const HopArgs &a, int64_t work, hipStream_t st) {
+    // `work` candidate roots (hop 1: roots; later hops: previous slots), 64 per wavefront
+    int64_t blocks = (work + kBlock - 1) / kBlock;
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxGrid) blocks = kMaxGrid;
-    hop_kernel<G, MODE, MULTI, LAST><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(a);
+    if (first) {
+        hop_kernel<G, MODE, MULTI, LAST, true><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(a);
+    } else if constexpr (!MULTI) {
+        hop_kernel<G, MODE, false, LAST, false><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(a);
+    }
 }
 
 template <int MODE, bool MULTI, bool LAST>
-void launch_hop_m(int G, const HopArgs &a, int64_t cap, hipStream_t st) {
+void launch_m(int G, bool first, const HopArgs &a, int64_t work, hipStream_t st) {
     switch (G) {
-        case 8: launch_hop_g<8, MODE, MULTI, LAST>(a, cap, st); break;
-        case 16: launch_hop_g<16, MODE, MULTI, LAST>(a, cap, st); break;
-        case 32: launch_hop_g<32, MODE, MULTI, LAST>(a, cap, st); break;
-        default: launch_hop_g<64, MODE, MULTI, LAST>(a, cap, st); break;
+        case 8: launch_g<8, MODE, MULTI, LAST>(first, a, work, st); break;
+        case 16: launch_g<16, MODE, MULTI, LAST>(first, a, work, st); break;
+        case 32: launch_g<32, MODE, MULTI, LAST>(first, a, work, st); break;
+        default: launch_g<64, MODE, MULTI, LAST>(first, a, work, st); break;
     }
 }
 
-void launch_hop(int G, int mode, bool multi, bool last, const HopArgs &a, int64_t cap, hipStream_t st) {
-    if (mode == TGL_MOST_RECENT) {
-        if (multi) {
-            last ? launch_hop_m<TGL_MOST_RECENT, true, true>(G, a, cap, st)
-                 : launch_hop_m<TGL_MOST_RECENT, true, false>(G, a, cap, st);
-        } else {
-            last ? launch_hop_m<TGL_MOST_RECENT, false, true>(G, a, cap, st)
-                 : launch_hop_m<TGL_MOST_RECENT, false, false>(G, a, cap, st);
-        }
+template <int MODE>
+void launch_mode(int G, bool first, bool multi, bool last, const HopArgs &a, int64_t work, hipStream_t st) {
+    if (multi) {
+        last ? launch_m<MODE, true, true>(G, first, a, work, st) : launch_m<MODE, true, false>(G, first, a, work, st);
     } else {
-        if (multi) {
-            last ? launch_hop_m<TGL_UNIFORM, true, true>(G, a, cap, st)
-                 : launch_hop_m<TGL_UNIFORM, true, false>(G, a, cap, st);
-        } else {
-            last ? launch_hop_m<TGL_UNIFORM, false, true>(G, a, cap, st)
-                 : launch_hop_m<TGL_UNIFORM, false, false>(G, a, cap, st);
-        }
+        last ? launch_m<MODE, false, true>(G, first, a, work, st) : launch_m<MODE, false, false>(G, first, a, work, st);
     }
+}
+
+void launch_hop(int G, int mode, bool first, bool multi, bool last, const HopArgs &a, int64_t work,
+                hipStream_t st) {
+    if (mode == TGL_MOST_RECENT) launch_mode<TGL_MOST_RECENT>(G, first, multi, last, a, work, st);
+    else launch_mode<TGL_UNIFORM>(G, first, multi, last, a, work, st);
 }
 
 // lanes per root: the slot count rounded up to a power of two, in [8, 64]
@@ -355,35 +439,33 @@ bool sample_args_ok(int64_t R, int32_t hops, const int32_t *fanouts, int32_t S) 
 }
 
 struct SampleWs {
-    int32_t *cnt = nullptr;
+    int32_t *cnt = nullptr;          // valid slots per group of the current hop
+    int64_t *off = nullptr;          // their exclusive scan
     int64_t *partials = nullptr;
-    int32_t *nx[2] = {nullptr, nullptr};
-    float *nt[2] = {nullptr, nullptr};
-    int32_t *ns[2] = {nullptr, nullptr};
-    uint64_t *npath[2] = {nullptr, nullptr};
+    int32_t *s[2] = {nullptr, nullptr};       // window per root (hops 2..L-1)
+    uint64_t *path[2] = {nullptr, nullptr};   // path per root (hops 2..L-1)
     size_t bytes = 0;
 };
 
-// Workspace: per-group counts and tile partials (largest hop h < L), and one
-// (two when L >= 3) buffers of next-hop roots sized for the largest hop >= 2.
+// Workspace: per-group counts, offsets and scan partials for the largest hop
+// h < L; window and path of the roots of hops 2..L-1 (two alternating buffers).
 SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S) {
     SampleWs w;
     Carver cv(base);
     if (hops >= 2) {
         int64_t max_groups = cap[0] * S;      // hop-1 groups
-        int64_t max_roots = 0;                 // roots of hops 2..L
-        for (int h = 2; h <= hops; h++) {
-            max_roots = cap[h - 1] > max_roots ? cap[h - 1] : max_roots;
-            if (h < hops) max_groups = cap[h - 1] > max_groups ? cap[h - 1] : max_groups;
-        }
+        for (int h = 2; h < hops; h++) max_groups = cap[h - 1] > max_groups ? cap[h - 1] : max_groups;
         w.cnt = cv.take<int32_t>(static_cast<size_t>(max_groups));
+        w.off = cv.take<int64_t>(static_cast<size_t>(max_groups));
         w.partials = cv.take<int64_t>(static_cast<size_t>(scan_tiles(max_groups) + 1));
-        const int nbuf = hops >= 3 ? 2 : 1;
-        for (int i = 0; i < nbuf; i++) {
-            w.nx[i] = cv.take<int32_t>(static_cast<size_t>(max_roots));
-            w.nt[i] = cv.take<float>(static_cast<size_t>(max_roots));
-            w.ns[i] = cv.take<int32_t>(static_cast<size_t>(max_roots));
-            w.npath[i] = cv.take<uint64_t>(static_cast<size_t>(max_roots));
+        if (hops >= 3) {
+            int64_t max_mid = 0;               // roots of hops 2..L-1
+            for (int h = 2; h < hops; h++) max_mid = cap[h - 1] > max_mid ? cap[h - 1] : max_mid;
+            const int nbuf = hops >= 4 ? 2 : 1;
+            for (int i = 0; i < nbuf; i++) {
+                w.s[i] = cv.take<int32_t>(static_cast<size_t>(max_mid));
+                w.path[i] = cv.take<uint64_t>(static_cast<size_t>(max_mid));
+            }
         }
     }
     w.bytes = cv.size();
@@ -426,9 +508,12 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     if (snapshot_len != snapshot_len || !(snapshot_len > 0.0f)) return TGL_EINVAL;
     const bool dinf = __builtin_isinf(snapshot_len);
     if (dinf && num_snapshots != 1) return TGL_EINVAL;
-    if (g->num_nodes < 1 || g->num_nodes > INT32_MAX || g->num_entries < 0) return TGL_EINVAL;
+    if (g->num_nodes < 1 || g->num_nodes > INT32_MAX) return TGL_EINVAL;
+    if (g->num_entries < 0 || g->num_entries > static_cast<int64_t>(UINT32_MAX)) return TGL_EINVAL;
     if (!g->indptr || (g->num_entries > 0 && !g->entries)) return TGL_EINVAL;
+    if (g->num_entries > 0 && !g->ts) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
     if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
     int64_t cap[TGL_MAX_HOPS + 1];
     if (!capacities(num_roots, hops, fanouts, num_snapshots, cap)) return TGL_EINVAL;
@@ -447,9 +532,14 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     HopArgs a{};
     a.indptr = g->indptr;
     a.ent = reinterpret_cast<const int4 *>(g->entries);
+    a.tsa = g->ts;
     a.num_nodes = g->num_nodes;
     a.num_entries = g->num_entries;
+    a.rx = roots;
+    a.rt = root_ts;
+    a.num_roots = num_roots;
     a.root_base = root_base;
+    a.S = num_snapshots;
     a.delta = snapshot_len;
     a.delta_inf = dinf ? 1 : 0;
     a.seedmix = mix64(seed ^ kGolden);
@@ -459,7 +549,6 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
         const bool last = h == hops;
         const int32_t k = fanouts[h - 1];
         const tgl_hop_out &o = outs[h - 1];
-        const int buf = (h - 2) & 1;          // next-root buffer holding hop-h roots (h >= 2)
         a.hop = h;
         a.k = k;
         a.windows = h == 1 ? S : 1;
@@ -467,61 +556,45 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
         a.o_eid = o.eid;
         a.o_ts = o.ts;
         a.o_dt = o.dt;
+        a.o_parent = h >= 2 ? o.parent : nullptr;
         a.o_cnt = last ? nullptr : ws.cnt;
-        if (h == 1) {
-            a.rx = roots;
-            a.rt = root_ts;
-            a.rs = nullptr;
-            a.rpath = nullptr;
-            a.count_static = num_roots;
-            a.count_dyn = nullptr;
-            a.count0_out = counts;
-        } else {
-            a.rx = ws.nx[buf];
-            a.rt = ws.nt[buf];
-            a.rs = ws.ns[buf];
-            a.rpath = ws.npath[buf];
-            a.count_static = 0;
-            a.count_dyn = counts + (h - 1);
-            a.count0_out = nullptr;
+        // window and path of this hop's roots are kept for hop h + 1 (hop-1
+        // children derive them from their slot index instead)
+        const bool keep = h >= 2 && h < hops;
+        a.o_s = keep ? ws.s[h & 1] : nullptr;
+        a.o_path = keep ? ws.path[h & 1] : nullptr;
+        a.count0_out = h == 1 ? counts : nullptr;
+        if (h >= 2) {
+            const tgl_hop_out &po = outs[h - 2];
+            a.p_nbr = po.nbr;
+            a.p_ts = po.ts;
+            a.p_off = ws.off;
+            a.p_k = fanouts[h - 2];
+            a.p_s = h >= 3 ? ws.s[(h - 1) & 1] : nullptr;
+            a.p_path = h >= 3 ? ws.path[(h - 1) & 1] : nullptr;
+            a.p_groups_static = h == 2 ? num_roots * S : 0;
+            a.p_groups_dyn = h == 2 ? nullptr : counts + (h - 2);
         }
         const bool multi = h == 1 && S > 1;
         const int G = pick_group(static_cast<int64_t>(a.windows) * k);
+        const int64_t work = h == 1 ? num_roots : cap[h - 1];
         {
             ScopedTimer tm(h == 1 ? TGL_TIMER_HOP1 : TGL_TIMER_HOPN, st);
-            launch_hop(G, mode, multi, last, a, cap[h - 1], st);
+            launch_hop(G, mode, h == 1, multi, last, a, work, st);
         }
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
         if (last) break;
 
-        // ---- compaction: hop-h valid slots -> hop-(h+1) roots ----
-        const int64_t groups_cap = h == 1 ? cap[0] * S : cap[h - 1];
+        // ---- exclusive scan of this hop's group counts -> next hop's indices ----
+        const int64_t groups_cap = h == 1 ? num_roots * S : cap[h - 1];
         const int64_t *groups_dyn = h == 1 ? nullptr : counts + (h - 1);
         const int64_t tiles = scan_tiles(groups_cap) > 0 ? scan_tiles(groups_cap) : 1;
-        const int nb = (h - 1) & 1;           // buffer receiving hop-(h+1) roots
         ScopedTimer tm(TGL_TIMER_COMPACT, st);
         scan_reduce_kernel<int32_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
             ws.cnt, groups_cap, groups_dyn, ws.partials);
         launch_scan_partials(ws.partials, tiles, counts + h, st);
-        EmitArgs e{};
-        e.cnt = ws.cnt;
-        e.partials = ws.partials;
-        e.n_static = groups_cap;
-        e.n_dyn = groups_dyn;
-        e.k = k;
-        e.windows = a.windows;
-        e.hop = h;
-        e.root_base = root_base;
-        e.h_nbr = o.nbr;
-        e.h_ts = o.ts;
-        e.h_rs = h == 1 ? nullptr : ws.ns[buf];
-        e.h_rpath = h == 1 ? nullptr : ws.npath[buf];
-        e.nx = ws.nx[nb];
-        e.nt = ws.nt[nb];
-        e.ns = ws.ns[nb];
-        e.npath = ws.npath[nb];
-        e.parent = outs[h].parent;
-        compact_emit_kernel<<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(e);
+        scan_apply_kernel<int32_t, int64_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
+            ws.cnt, ws.off, groups_cap, groups_dyn, ws.partials);
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
     }
     return TGL_OK;

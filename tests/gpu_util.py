@@ -33,8 +33,12 @@ def hops_to_numpy(hops):
 
 
 def tcsr_to_host(g):
+    """Host copy of a device T-CSR; checks that the separate timestamp array
+    equals the records' timestamps bit for bit."""
     ent = g.entries.cpu().numpy().reshape(-1, 2)
     w = ent.view(np.int32).reshape(-1, 4)
+    ts = g.ts.cpu().numpy()
+    assert np.array_equal(ts.view(np.int32), w[:, 1]), "ts array differs from the records"
     return oracle.TCSR(g.indptr.cpu().numpy(), w[:, 0].copy(), ent[:, 1].copy(),
                        w[:, 1].copy().view(np.float32))
 

@@ -56,8 +56,9 @@ def _rand_case(rng):
     rts = rng.integers(-5, 45, R).astype(np.float32)
     if R > 6:
         rts[:6] = [np.nan, np.inf, -np.inf, -0.0, 1e-41, 3.25]
-    hops = int(rng.integers(1, 4))
-    fan = [int(rng.choice([1, 2, 5, 10, 16, 33, 70])) for _ in range(hops)]
+    hops = int(rng.integers(1, 5))
+    choices = [1, 2, 5, 10, 16, 33, 70] if hops <= 2 else [1, 2, 3, 5]
+    fan = [int(rng.choice(choices)) for _ in range(hops)]
     mode = ["recent", "uniform"][int(rng.integers(0, 2))]
     S = int(rng.choice([1, 1, 2, 3, 5]))
     D = float(rng.choice([1.0, 2.5, 9.0])) if (S > 1 or rng.integers(0, 2)) else math.inf
@@ -67,9 +68,9 @@ def _rand_case(rng):
 def test_random_small_graphs(torch):
     """GPU build and GPU sampling on random small graphs with ties, -0, +-inf and
     denormal timestamps, self-loops, duplicate / out-of-range roots, NaN and
-    infinite query times, 1-3 hops, fanouts 1..70 and 1..5 snapshots."""
+    infinite query times, 1-4 hops, fanouts 1..70 and 1..5 snapshots."""
     rng = np.random.default_rng(2024)
-    for trial in range(120):
+    for trial in range(160):
         N, src, dst, ts, eid, und, roots, rts, fan, mode, S, D, seed, base = _rand_case(rng)
         announce("random trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s" % (trial, N, len(src), len(roots), fan, mode, S, D))
         want_g = oracle.build_tcsr(src, dst, ts, eid, N, und)
