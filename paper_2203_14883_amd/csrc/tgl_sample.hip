@@ -93,39 +93,65 @@ __device__ __forceinline__ float4 load_ts4(const float *__restrict__ tsa, uint32
     return r;
 }
 
-// Entries [lo, hi) of a sorted run, held four per lane: lane gl holds
-// c4 + 4*gl .. c4 + 4*gl + 3.  Returns lo + #{p in [lo, hi): (double)ts[p] < v}.
+// A stretch of a time-sorted run held in the registers of one G-lane group:
+// lane gl holds the H timestamps p0 .. p0 + H - 1, p0 = (lo & ~3) + H * gl,
+// loaded as H / 4 aligned float4.  One load covers any [lo, hi) of at most
+// `span` entries.
 template <int G>
-__device__ __forceinline__ uint32_t count_held(float4 v4, uint32_t c4, uint32_t lo, uint32_t hi, double v, int gl) {
-    const uint32_t p = c4 + 4 * static_cast<uint32_t>(gl);
-    int c = __popcll(group_ballot<G>(p >= lo && p < hi && static_cast<double>(v4.x) < v));
-    c += __popcll(group_ballot<G>(p + 1 >= lo && p + 1 < hi && static_cast<double>(v4.y) < v));
-    c += __popcll(group_ballot<G>(p + 2 >= lo && p + 2 < hi && static_cast<double>(v4.z) < v));
-    c += __popcll(group_ballot<G>(p + 3 >= lo && p + 3 < hi && static_cast<double>(v4.w) < v));
-    return lo + c;
+struct HeldRun {
+    static constexpr int NV = G >= 16 ? 1 : 16 / G;     // float4 per lane
+    static constexpr uint32_t H = 4 * NV;               // timestamps per lane
+    static constexpr uint32_t span = H * G - 3;
+    float4 v[NV];
+    uint32_t p0;
+};
+
+template <int G>
+__device__ __forceinline__ HeldRun<G> load_run(const float *__restrict__ tsa, uint32_t lo, uint32_t hi,
+                                               uint32_t M, int gl) {
+    HeldRun<G> r;
+    r.p0 = (lo & ~3u) + HeldRun<G>::H * static_cast<uint32_t>(gl);
+    const float inf = __builtin_inff();
+#pragma unroll
+    for (int m = 0; m < HeldRun<G>::NV; m++) {
+        const uint32_t p4 = r.p0 + 4 * m;
+        r.v[m] = p4 < hi ? load_ts4(tsa, p4, M) : make_float4(inf, inf, inf, inf);
+    }
+    return r;
 }
 
-// Longest range [lo, hi) that one held load covers: c4 = lo & ~3 and
-// [c4, c4 + 4G) must contain it.
+// Sum over the G lanes of the calling lane's group.
 template <int G>
-constexpr uint32_t held_span() { return 4 * G - 3; }
+__device__ __forceinline__ int group_sum(int c) {
+#pragma unroll
+    for (int off = G / 2; off >= 1; off >>= 1) c += __shfl_xor(c, off, kWave);
+    return c;
+}
 
+// lo + #{p in [lo, hi): (double)ts[p] < v} for [lo, hi) inside the held stretch.
 template <int G>
-__device__ __forceinline__ float4 load_held(const float *__restrict__ tsa, uint32_t c4, uint32_t hi, uint32_t M, int gl) {
-    const uint32_t p4 = c4 + 4 * static_cast<uint32_t>(gl);
-    const float inf = __builtin_inff();
-    return p4 < hi ? load_ts4(tsa, p4, M) : make_float4(inf, inf, inf, inf);
+__device__ __forceinline__ uint32_t count_in(const HeldRun<G> &r, uint32_t lo, uint32_t hi, double v) {
+    int c = 0;
+#pragma unroll
+    for (int m = 0; m < HeldRun<G>::NV; m++) {
+        const uint32_t p = r.p0 + 4 * m;
+        c += (p >= lo && p < hi && static_cast<double>(r.v[m].x) < v);
+        c += (p + 1 >= lo && p + 1 < hi && static_cast<double>(r.v[m].y) < v);
+        c += (p + 2 >= lo && p + 2 < hi && static_cast<double>(r.v[m].z) < v);
+        c += (p + 3 >= lo && p + 3 < hi && static_cast<double>(r.v[m].w) < v);
+    }
+    return lo + static_cast<uint32_t>(group_sum<G>(c));
 }
 
 // Number of entries p in [lo, hi) of a time-sorted run with (double)ts[p] < v,
 // found by the G lanes of one group together.  While the range is longer than
-// one held load, each round probes G evenly spaced positions; the probes below
-// v form a prefix, whose length narrows the range to one gap.  A NaN bound
-// compares false everywhere and gives lo.
+// one held stretch, each round probes G evenly spaced positions; the probes
+// below v form a prefix, whose length narrows the range to one gap.  A NaN
+// bound compares false everywhere and gives lo.
 template <int G>
 __device__ __forceinline__ uint32_t count_below(const float *__restrict__ tsa, uint32_t lo, uint32_t hi,
                                                 uint32_t M, double v, int gl) {
-    while (hi - lo > held_span<G>()) {
+    while (hi - lo > HeldRun<G>::span) {
         const uint64_t len = hi - lo;
         const uint32_t pos = lo + static_cast<uint32_t>((static_cast<uint64_t>(gl + 1) * len) / (G + 1));
         const bool below = static_cast<double>(tsa[pos]) < v;
@@ -135,8 +161,7 @@ __device__ __forceinline__ uint32_t count_below(const float *__restrict__ tsa, u
         lo = nlo;
         hi = nhi;
     }
-    const uint32_t c4 = lo & ~3u;
-    return count_held<G>(load_held<G>(tsa, c4, hi, M, gl), c4, lo, hi, v, gl);
+    return count_in<G>(load_run<G>(tsa, lo, hi, M, gl), lo, hi, v);
 }
 
 __device__ __forceinline__ double bound_value(float t, int32_t i, float delta) {
@@ -183,10 +208,9 @@ __device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32
                                              int32_t s0, uint64_t hp, int gl, uint32_t *my_edges) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     // a run short enough is loaded once and serves every window edge
-    const bool held = b - a <= held_span<G>();        // group-uniform
-    const uint32_t c4 = a & ~3u;
-    float4 v4;
-    if (held) v4 = load_held<G>(p.tsa, c4, b, M, gl);
+    const bool held = b - a <= HeldRun<G>::span;      // group-uniform
+    HeldRun<G> run;
+    if (held) run = load_run<G>(p.tsa, a, b, M, gl);
 
     const int W = MULTI ? p.windows : 1;
     const int k = p.k;
@@ -195,16 +219,16 @@ __device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32
         // edges i = 0..W: window s spans [edge s+1, edge s)
         for (int i = 0; i <= W; i++) {
             const double v = bound_value(t, i, p.delta);
-            const uint32_t c = held ? count_held<G>(v4, c4, a, b, v, gl) : count_below<G>(p.tsa, a, b, M, v, gl);
+            const uint32_t c = held ? count_in<G>(run, a, b, v) : count_below<G>(p.tsa, a, b, M, v, gl);
             if (gl == 0) my_edges[i] = c;
         }
         wave_sync_lds();
     } else {
         const double vh = bound_value(t, s0, p.delta);
-        hi = held ? count_held<G>(v4, c4, a, b, vh, gl) : count_below<G>(p.tsa, a, b, M, vh, gl);
+        hi = held ? count_in<G>(run, a, b, vh) : count_below<G>(p.tsa, a, b, M, vh, gl);
         if (!p.delta_inf) {
             const double vl = bound_value(t, s0 + 1, p.delta);
-            lo = held ? count_held<G>(v4, c4, a, b, vl, gl) : count_below<G>(p.tsa, a, b, M, vl, gl);
+            lo = held ? count_in<G>(run, a, b, vl) : count_below<G>(p.tsa, a, b, M, vl, gl);
         }
         if (lo > hi) lo = hi;
     }
@@ -369,23 +393,205 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
     }
 }
 
+// Window [lo, hi) of a root with run [a, b) at time t in window s0 (one
+// window per root), by the G lanes of its group.
+template <int G>
+__device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint32_t b, float t, int32_t s0,
+                                              int gl, uint32_t &lo, uint32_t &hi) {
+    const uint32_t M = static_cast<uint32_t>(p.num_entries);
+    const double vh = bound_value(t, s0, p.delta);
+    if (b - a <= HeldRun<G>::span) {                 // group-uniform
+        const HeldRun<G> run = load_run<G>(p.tsa, a, b, M, gl);
+        hi = count_in<G>(run, a, b, vh);
+        lo = p.delta_inf ? a : count_in<G>(run, a, b, bound_value(t, s0 + 1, p.delta));
+    } else {
+        hi = count_below<G>(p.tsa, a, b, M, vh, gl);
+        lo = p.delta_inf ? a : count_below<G>(p.tsa, a, b, M, bound_value(t, s0 + 1, p.delta), gl);
+    }
+    if (lo > hi) lo = hi;
+}
+
+// One hop with one window per root (every hop except a first hop with several
+// snapshots).  Each wavefront takes chunks of 64 candidate roots:
+//   phase 1, one lane per candidate: hop 1 takes root v as given; later hops
+//     take slot v of the previous hop, valid when its nbr >= 0, as the root
+//     with index off[v / k_prev] + v % k_prev (and write its parent index).
+//     Every lane loads its root's time and run bounds; the valid roots are
+//     packed, in order, into LDS;
+//   phase 2, G lanes per root, 64 / G roots per round: the window [lo, hi);
+//   phase 3, one lane per slot: selection, gather and emit.  The packed roots
+//     have consecutive indices, so the slots of a chunk are one contiguous
+//     range of the output and the stores coalesce.
+template <int G, int MODE, bool LAST, bool FIRST>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) void hop_single_kernel(const HopArgs p) {
+    constexpr int GPW = kWave / G;            // roots located per wavefront round
+    constexpr int U = 4;                      // slots per lane whose loads are in flight together
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int gl = lane & (G - 1);
+    const int gw = lane / G;
+    __shared__ uint32_t r_lo[kWavesPerBlock][kWave];   // run start, then window start
+    __shared__ uint32_t r_n[kWavesPerBlock][kWave];    // run end, then window size
+    __shared__ int64_t r_q[kWavesPerBlock][kWave];
+    __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
+    __shared__ float r_t[kWavesPerBlock][kWave];
+    __shared__ int32_t r_s[kWavesPerBlock][kWave];
+
+    const int64_t M = p.num_entries;
+    const int64_t pk = FIRST ? 1 : p.p_k;
+    int64_t nv;
+    if constexpr (FIRST) {
+        nv = p.num_roots;
+        if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = nv;
+    } else {
+        const int64_t groups = p.p_groups_dyn ? *p.p_groups_dyn : p.p_groups_static;
+        nv = groups * pk;
+    }
+    const int64_t nchunks = (nv + kWave - 1) / kWave;
+    const uint64_t S = static_cast<uint64_t>(p.S);
+    const uint64_t path1 = p.root_base * S * static_cast<uint64_t>(pk);   // hop-1 children: + v
+    const uint64_t lane_bit = 1ull << lane;
+    const int k = p.k;
+    const uint64_t hop_key = static_cast<uint64_t>(p.hop) << 40;
+
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w; c < nchunks;
+         c += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
+        // ---- phase 1: one lane per candidate root ----
+        const int64_t v = c * kWave + lane;
+        bool valid;
+        int32_t x = -1;
+        float t = 0.0f;
+        int64_t q = 0;
+        int32_t s = 0;
+        uint64_t path = 0;
+        if constexpr (FIRST) {
+            valid = v < nv;
+            if (valid) {
+                x = p.rx[v];
+                t = p.rt[v];
+                q = v;
+                path = p.root_base + static_cast<uint64_t>(v);
+            }
+        } else {
+            x = v < nv ? p.p_nbr[v] : -1;
+            valid = x >= 0;
+            if (valid) {
+                t = p.p_ts[v];
+                const int64_t g = v / pk;
+                const int64_t j = v - g * pk;
+                q = p.p_off[g] + j;
+                if (p.p_s) {
+                    s = p.p_s[g];
+                    path = p.p_path[g] * static_cast<uint64_t>(pk) + static_cast<uint64_t>(j);
+                } else {
+                    s = static_cast<int32_t>(static_cast<uint64_t>(g) % S);
+                    path = path1 + static_cast<uint64_t>(v);
+                }
+                p.o_parent[q] = v;
+                if (p.o_s) {
+                    p.o_s[q] = s;
+                    p.o_path[q] = path;
+                }
+            }
+        }
+        int64_t a = 0, b = 0;
+        if (valid && x >= 0 && x < p.num_nodes) {
+            a = p.indptr[x];
+            b = p.indptr[x + 1];
+            a = a < 0 ? 0 : (a > M ? M : a);
+            b = b < a ? a : (b > M ? M : b);
+        }
+        const uint64_t mask = __ballot(valid);
+        if (valid) {
+            const int r = __popcll(mask & (lane_bit - 1));
+            r_lo[w][r] = static_cast<uint32_t>(a);
+            r_n[w][r] = static_cast<uint32_t>(b);
+            r_q[w][r] = q;
+            r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
+            r_t[w][r] = t;
+            r_s[w][r] = s;
+        }
+        wave_sync_lds();
+        const int nvalid = __popcll(mask);
+
+        // ---- phase 2: G lanes per root locate its window ----
+        for (int base = 0; base < nvalid; base += GPW) {
+            const int i = base + gw;
+            if (i < nvalid) {                       // group-uniform
+                uint32_t lo, hi;
+                locate_window<G>(p, r_lo[w][i], r_n[w][i], r_t[w][i], r_s[w][i], gl, lo, hi);
+                if (gl == 0) {
+                    r_lo[w][i] = lo;
+                    r_n[w][i] = hi - lo;
+                    if (p.o_cnt) {
+                        const uint32_t n = hi - lo;
+                        p.o_cnt[r_q[w][i]] = MODE == TGL_MOST_RECENT
+                                                 ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
+                                                 : (n > 0 ? k : 0);
+                    }
+                }
+            }
+        }
+        wave_sync_lds();
+
+        // ---- phase 3: one lane per slot ----
+        const int total = nvalid * k;
+        for (int e0 = 0; e0 < total; e0 += U * kWave) {
+            uint32_t pick[U];                       // UINT32_MAX: PAD slot
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int e = e0 + u * kWave + lane;
+                const bool act = e < total;
+                const int i = act ? e / k : 0;
+                const int j = e - i * k;
+                const uint32_t lo = r_lo[w][i];
+                const uint32_t n = r_n[w][i];
+                if constexpr (MODE == TGL_MOST_RECENT) {
+                    pick[u] = act && static_cast<uint32_t>(j) < n ? lo + n - 1 - static_cast<uint32_t>(j) : UINT32_MAX;
+                } else {
+                    const uint64_t key = hop_key | (static_cast<uint64_t>(r_s[w][i]) << 24) | static_cast<uint64_t>(j);
+                    pick[u] = act && n > 0
+                                  ? lo + static_cast<uint32_t>(__umul64hi(mix64(r_hp[w][i] ^ key), static_cast<uint64_t>(n)))
+                                  : UINT32_MAX;
+                }
+            }
+            int4 rec[U];
+#pragma unroll
+            for (int u = 0; u < U; u++)
+                rec[u] = pick[u] != UINT32_MAX ? p.ent[pick[u]] : make_int4(-1, -1, -1, -1);
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int e = e0 + u * kWave + lane;
+                if (e < total) {
+                    const int i = e / k;
+                    const int j = e - i * k;
+                    emit_slot<LAST>(p, r_q[w][i] * k + j, pick[u] != UINT32_MAX, rec[u], r_t[w][i]);
+                }
+            }
+        }
+        wave_sync_lds();                            // the next chunk rewrites the LDS rows
+    }
+}
+
 template <int G, int MODE, bool MULTI, bool LAST>
 void launch_g(bool first, const HopArgs &a, int64_t work, hipStream_t st) {
     // `work` candidate roots (hop 1: roots; later hops: previous slots), 64 per wavefront
     int64_t blocks = (work + kBlock - 1) / kBlock;
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxGrid) blocks = kMaxGrid;
-    if (first) {
-        hop_kernel<G, MODE, MULTI, LAST, true><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(a);
-    } else if constexpr (!MULTI) {
-        hop_kernel<G, MODE, false, LAST, false><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(a);
+    const unsigned nb = static_cast<unsigned>(blocks);
+    if constexpr (MULTI) {
+        if (first) hop_kernel<G, MODE, true, LAST, true><<<nb, kBlock, 0, st>>>(a);
+    } else {
+        // the window search uses 8 lanes per root whatever the fanout
+        if (first) hop_single_kernel<8, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a);
+        else hop_single_kernel<8, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a);
     }
 }
 
 template <int MODE, bool MULTI, bool LAST>
 void launch_m(int G, bool first, const HopArgs &a, int64_t work, hipStream_t st) {
     switch (G) {
-        case 8: launch_g<8, MODE, MULTI, LAST>(first, a, work, st); break;
         case 16: launch_g<16, MODE, MULTI, LAST>(first, a, work, st); break;
         case 32: launch_g<32, MODE, MULTI, LAST>(first, a, work, st); break;
         default: launch_g<64, MODE, MULTI, LAST>(first, a, work, st); break;
@@ -407,9 +613,10 @@ void launch_hop(int G, int mode, bool first, bool multi, bool last, const HopArg
     else launch_mode<TGL_UNIFORM>(G, first, multi, last, a, work, st);
 }
 
-// lanes per root: the slot count rounded up to a power of two, in [8, 64]
+// lanes per root for first hops with several windows: the slot count rounded
+// up to a power of two, in [16, 64]
 int pick_group(int64_t slots_per_root) {
-    int g = 8;
+    int g = 16;
     while (g < 64 && g < slots_per_root) g <<= 1;
     return g;
 }
