@@ -58,9 +58,10 @@ def parse():
 
 
 def kernel_source_hash():
+    """Hash of the sources that define the sampling kernels."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2203_14883_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
+    for f in ("tgl_internal.hpp", "tgl_sample.hip"):
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
@@ -279,7 +280,9 @@ def main():
                 deg = (indptr[roots2 + 1] - indptr[roots2]).double()
                 bounds = 1 if math.isinf(w.snapshot_len) else 2
                 search = float((torch.ceil(torch.log2(deg + 1.0)) * 4.0 * bounds).sum())
-                hopn_bytes += (hop.num_roots * (8 + 16) + search + nv * 16 + hop.nbr.numel() * 20)
+                # per root: node + time read, run bounds read, parent index written;
+                # per slot: 16-byte entry read when valid, 20 bytes written
+                hopn_bytes += (hop.num_roots * (8 + 16 + 8) + search + nv * 16 + hop.nbr.numel() * 20)
     hopn_bytes_per_launch = hopn_bytes / max(len(timed_pos), 1)
     avg_hopn_ms = hopn_ms / max(hopn_n, 1)
     achieved = hopn_bytes_per_launch / (avg_hopn_ms * 1e-3) / 1e9 if avg_hopn_ms > 0 else 0.0
