@@ -104,53 +104,20 @@ def step_positions(nb, B, n):
     return [int(round(i * last / (n - 1))) for i in range(n)]
 
 
-def _owned_entries(w, nodes):
-    """Directed entries owned by ``nodes``: the forward entries of edges whose
-    source is in the set, then the reversed entries of edges whose destination
-    is in the set, each in input order.  Built into a T-CSR without the
-    undirected flag, this gives every node of the set exactly the run it has in
-    the full undirected T-CSR (same entries, same tie order)."""
-    from concurrent.futures import ThreadPoolExecutor
-    flag = np.zeros(w.num_nodes, dtype=bool)
-    flag[nodes] = True
-    n = w.num_edges
-    fwd = np.empty(n, dtype=bool)
-    rev = np.empty(n, dtype=bool)
-    chunk = 1 << 24
-
-    def f(c):
-        b, e = c * chunk, min(n, (c + 1) * chunk)
-        np.take(flag, w.src[b:e], out=fwd[b:e])
-        np.take(flag, w.dst[b:e], out=rev[b:e])
-
-    with ThreadPoolExecutor(16) as ex:
-        list(ex.map(f, range((n + chunk - 1) // chunk)))
-    fi = np.flatnonzero(fwd)
-    ri = np.flatnonzero(rev) if w.undirected else np.zeros(0, np.int64)
-    src = np.concatenate([w.src[fi], w.dst[ri]])
-    dst = np.concatenate([w.dst[fi], w.src[ri]])
-    ts = np.concatenate([w.ts[fi], w.ts[ri]])
-    eid = np.concatenate([fi, ri]).astype(np.int64)
-    return src, dst, ts, eid
-
-
 def cpu_baseline(w, nbatches):
     """The oracle, single-threaded, on a bounded sample: the roots of
     ``nbatches`` consecutive batches from the middle of the epoch (one GPU step
     at the default size), over an oracle T-CSR that holds the full runs of every
     node the sample reaches.  Only the oracle's sampling call is timed."""
     import oracle
+    from oracle import subgraph
     b0 = w.num_batches() // 2
     roots, rts, base = w.batches(b0, b0 + nbatches)
-    g1 = oracle.build_tcsr(*_owned_entries(w, np.unique(roots)), w.num_nodes, False)
-    reach = roots
-    for h in range(len(w.fanouts) - 1):      # nodes that become roots of the later hops
-        out = oracle.sample(g1, roots, rts, w.fanouts[:h + 1], w.mode, w.snapshots,
-                            w.snapshot_len, w.sample_seed, base)
-        reach = np.unique(np.concatenate([reach, out[h].nbr[out[h].nbr >= 0]]))
-        g1 = oracle.build_tcsr(*_owned_entries(w, reach), w.num_nodes, False)
+    src, dst, ts, eid = w.build_input()
+    g = subgraph.reach_tcsr(src, dst, ts, eid, w.num_nodes, w.undirected, roots, rts, w.fanouts,
+                            w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
     t = time.perf_counter()
-    out = oracle.sample(g1, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
+    out = oracle.sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
                         w.sample_seed, base)
     dt = time.perf_counter() - t
     nbrs = int(sum(int((h.nbr >= 0).sum()) for h in out))

@@ -13,7 +13,9 @@
  *  oracle_build  -- the T-CSR of Section 3.1 ("The T-CSR Data Structure"):
  *                   an indptr array of |V|+1 offsets and, per node, its
  *                   outgoing edges (neighbour, edge id, timestamp) sorted by
- *                   timestamp.  Ties in timestamp keep input order.
+ *                   timestamp.  Ties in timestamp keep input order.  Plain
+ *                   stable counting sort by node, then a stable merge sort of
+ *                   each run by timestamp.
  *  oracle_locate -- the candidate window of a root inside one snapshot:
  *                   the edges of node x with  t - (s+1)*D <= ts < t - s*D
  *                   (Section 3 on dynamic snapshots built from the target
@@ -62,28 +64,41 @@
 /* T-CSR build (Section 3.1, "The T-CSR Data Structure")                    */
 /* ------------------------------------------------------------------------ */
 
+/* One directed entry of the T-CSR before ordering. */
 typedef struct {
-    int32_t u;      /* owner node (the edge leaves u)            */
     int32_t v;      /* neighbour                                 */
     float   t;      /* timestamp                                 */
     int64_t e;      /* caller's edge id                          */
-    int64_t pos;    /* input position: forward i, reversed m0+i  */
 } oracle_entry;
 
-/* Order of the T-CSR: by owner node, then timestamp, then input position. */
-static int entry_cmp(const void *pa, const void *pb)
+/* Stable merge sort of ent[0..n) by timestamp (tmp has room for n).  Equal
+ * timestamps keep their relative order.  Halves that are already in order
+ * are not merged again. */
+static void merge_sort_by_time(oracle_entry *ent, oracle_entry *tmp, int64_t n)
 {
-    const oracle_entry *a = (const oracle_entry *)pa;
-    const oracle_entry *b = (const oracle_entry *)pb;
-    if (a->u != b->u) return a->u < b->u ? -1 : 1;
-    if (a->t != b->t) return a->t < b->t ? -1 : 1;
-    if (a->pos != b->pos) return a->pos < b->pos ? -1 : 1;
-    return 0;
+    for (int64_t width = 1; width < n; width *= 2) {
+        for (int64_t lo = 0; lo + width < n; lo += 2 * width) {
+            int64_t mid = lo + width;
+            int64_t hi = lo + 2 * width < n ? lo + 2 * width : n;
+            if (!(ent[mid].t < ent[mid - 1].t)) continue;     /* already in order */
+            int64_t i = lo, j = mid, k = 0;
+            while (i < mid && j < hi) {
+                if (ent[j].t < ent[i].t) tmp[k++] = ent[j++];  /* ties: left first */
+                else tmp[k++] = ent[i++];
+            }
+            while (i < mid) tmp[k++] = ent[i++];
+            while (j < hi) tmp[k++] = ent[j++];
+            memcpy(ent + lo, tmp, (size_t)k * sizeof(oracle_entry));
+        }
+    }
 }
 
-/* Entries: the m0 given edges (u=src, v=dst), then, when undirected, the same
- * edges reversed (u=dst, v=src) at positions m0..2*m0-1.  Returns the number
- * of entries written, or a negative status. */
+/* Entries: the m0 given edges (owner src, neighbour dst), then, when
+ * undirected, the same edges reversed (owner dst, neighbour src) at positions
+ * m0..2*m0-1.  The T-CSR orders them by owner node, then timestamp, then
+ * position: a stable counting sort by owner (so each run keeps position
+ * order) followed by a stable sort of every run by timestamp.  Returns the
+ * number of entries written, or a negative status. */
 int64_t oracle_build(int64_t m0, const int32_t *src, const int32_t *dst,
                      const float *ts, const int64_t *eid, int64_t num_nodes,
                      int undirected, int64_t *indptr, int32_t *nbr,
@@ -99,23 +114,31 @@ int64_t oracle_build(int64_t m0, const int32_t *src, const int32_t *dst,
         if (isnan(ts[i])) return ORACLE_ERANGE;
     }
 
-    oracle_entry *ent = (oracle_entry *)malloc((size_t)(m > 0 ? m : 1) * sizeof(oracle_entry));
-    if (!ent) return ORACLE_ENOMEM;
-    for (int64_t i = 0; i < m; i++) {
-        int64_t k = i < m0 ? i : i - m0;
-        int fwd = i < m0;
-        ent[i].u = fwd ? src[k] : dst[k];
-        ent[i].v = fwd ? dst[k] : src[k];
-        ent[i].t = ts[k] == 0.0f ? 0.0f : ts[k];   /* -0 is stored as +0 */
-        ent[i].e = eid ? eid[k] : k;
-        ent[i].pos = i;
-    }
-    qsort(ent, (size_t)m, sizeof(oracle_entry), entry_cmp);
-
     /* indptr[x] = number of entries whose owner is < x */
     memset(indptr, 0, (size_t)(num_nodes + 1) * sizeof(int64_t));
-    for (int64_t i = 0; i < m; i++) indptr[ent[i].u + 1] += 1;
+    for (int64_t i = 0; i < m; i++) {
+        int32_t u = i < m0 ? src[i] : dst[i - m0];
+        indptr[u + 1] += 1;
+    }
     for (int64_t x = 0; x < num_nodes; x++) indptr[x + 1] += indptr[x];
+
+    oracle_entry *ent = (oracle_entry *)malloc((size_t)(m > 0 ? m : 1) * sizeof(oracle_entry));
+    oracle_entry *tmp = (oracle_entry *)malloc((size_t)(m > 0 ? m : 1) * sizeof(oracle_entry));
+    int64_t *fill = (int64_t *)malloc((size_t)num_nodes * sizeof(int64_t));
+    if (!ent || !tmp || !fill) { free(ent); free(tmp); free(fill); return ORACLE_ENOMEM; }
+    memcpy(fill, indptr, (size_t)num_nodes * sizeof(int64_t));
+    for (int64_t i = 0; i < m; i++) {           /* in position order */
+        int64_t k = i < m0 ? i : i - m0;
+        int fwd = i < m0;
+        int32_t u = fwd ? src[k] : dst[k];
+        oracle_entry en;
+        en.v = fwd ? dst[k] : src[k];
+        en.t = ts[k] == 0.0f ? 0.0f : ts[k];   /* -0 is stored as +0 */
+        en.e = eid ? eid[k] : k;
+        ent[fill[u]++] = en;
+    }
+    for (int64_t x = 0; x < num_nodes; x++)
+        merge_sort_by_time(ent + indptr[x], tmp, indptr[x + 1] - indptr[x]);
 
     for (int64_t p = 0; p < m; p++) {
         nbr[p] = ent[p].v;
@@ -123,6 +146,8 @@ int64_t oracle_build(int64_t m0, const int32_t *src, const int32_t *dst,
         ts_out[p] = ent[p].t;
     }
     free(ent);
+    free(tmp);
+    free(fill);
     return m;
 }
 

@@ -1,0 +1,176 @@
+"""GPU path against the oracle at the full preset sizes, in the launch
+configuration bench.py times.
+
+* c4 (121.7M nodes, 1.3B edges, 2.6B T-CSR entries): one whole benchmark
+  step (64 batches, 768,000 roots, 2 hops) is compared slot for slot with the
+  oracle, which builds the full runs of every node the step reaches.
+* c3 (191M edges, runs up to ~4.6e7 entries) and c5 (200M entries built from a
+  shuffled COO, 2 hops inside 3 snapshots): the whole step runs on the GPU and
+  a sample of its roots -- including roots on the hottest nodes -- is compared
+  root by root (hop-1 slots and the hop-2 slots of that root's children).
+* For all three, the GPU T-CSR is checked in full on the device (indptr,
+  degrees, sortedness of every run, the timestamp array) and the runs of the
+  sampled nodes bit for bit against the oracle's.
+"""
+import gc
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2203_14883_amd as P
+from oracle import subgraph
+from paper_2203_14883_amd import workloads as W
+from checks import assert_hops_equal, same_bits
+from gpu_util import announce, hops_to_numpy, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    return require_gpu()
+
+
+def build_on_gpu(torch, w):
+    src, dst, ts, eid = w.build_input()
+    dev = torch.device("cuda")
+    d = [torch.from_numpy(a).to(dev) for a in (src, dst, ts)]
+    de = None if eid is None else torch.from_numpy(eid).to(dev)
+    g = P.tcsr_build(d[0], d[1], d[2], de, w.num_nodes, w.undirected)
+    # device-side invariants of the whole structure
+    M = g.num_entries
+    ip = g.indptr
+    assert int(ip[0]) == 0 and int(ip[-1]) == M and bool((ip[1:] >= ip[:-1]).all())
+    deg = torch.bincount(d[0].long(), minlength=w.num_nodes)
+    if w.undirected:
+        deg += torch.bincount(d[1].long(), minlength=w.num_nodes)
+    assert torch.equal(deg, ip[1:] - ip[:-1]), "degrees differ from the edge list"
+    del d, de, deg
+    start = torch.zeros(M, dtype=torch.bool, device=dev)
+    start[ip[:-1][ip[:-1] < M]] = True
+    ts_arr = g.ts
+    bad = (ts_arr[1:] < ts_arr[:-1]) & ~start[1:]
+    assert int(bad.sum()) == 0, "a run is not sorted by time"
+    assert torch.equal(ts_arr.view(torch.int32), g.entries.view(torch.int32)[:, 1]), "ts array differs"
+    del start, bad
+    torch.cuda.empty_cache()
+    return g
+
+
+def check_runs(g, og, nodes):
+    """GPU runs of ``nodes`` equal the oracle's runs bit for bit."""
+    ip = g.indptr.cpu().numpy()
+    for x in nodes:
+        a, b = int(ip[x]), int(ip[x + 1])
+        c, d = int(og.indptr[x]), int(og.indptr[x + 1])
+        assert b - a == d - c, "run length of node %d" % x
+        ent = g.entries[a:b].cpu().numpy()
+        w4 = ent.view(np.int32).reshape(-1, 4)
+        assert np.array_equal(w4[:, 0], og.nbr[c:d]), "nbr of node %d" % x
+        assert np.array_equal(ent[:, 1], og.eid[c:d]), "eid of node %d" % x
+        assert same_bits(w4[:, 1].copy().view(np.float32), og.ts[c:d]), "ts of node %d" % x
+
+
+def gpu_step(torch, g, w, b0, B):
+    roots, rts, base = w.batches(b0, b0 + B)
+    smp = P.Sampler(len(roots), w.fanouts, w.snapshots)
+    r, t = torch.from_numpy(roots).cuda(), torch.from_numpy(rts).cuda()
+    smp.run(g, r, t, w.mode, w.snapshot_len, w.sample_seed, base)
+    return roots, rts, base, hops_to_numpy(smp.hops())
+
+
+def per_root(out, r, S, fan):
+    """Slots of root r in a GPU step: its hop-1 slots and the hop-2 slots of its
+    children (found through the parent indices)."""
+    k1 = fan[0]
+    lo, hi = r * S * k1, (r + 1) * S * k1
+    res = [{f: out[0][f][lo:hi] for f in ("nbr", "eid", "ts", "dt")}]
+    if len(fan) > 1:
+        par = out[1]["parent"]
+        q = np.nonzero((par >= lo) & (par < hi))[0]
+        k2 = fan[1]
+        idx = (q[:, None] * k2 + np.arange(k2)[None, :]).reshape(-1)
+        res.append({f: out[1][f][idx] for f in ("nbr", "eid", "ts", "dt")})
+        res[1]["parent"] = par[q] - lo
+    return res
+
+
+def oracle_per_root(og, roots, rts, r, w, base):
+    o = oracle.sample(og, roots[r:r + 1], rts[r:r + 1], w.fanouts, w.mode, w.snapshots,
+                      w.snapshot_len, w.sample_seed, base + r)
+    res = [dict(nbr=h.nbr, eid=h.eid, ts=h.ts, dt=h.dt, parent=h.parent) for h in o]
+    return res
+
+
+def test_c4_full_step(torch):
+    announce("c4 full size: generate")
+    w = W.make_c4()
+    announce("c4 full size: GPU build of %d edges" % w.num_edges)
+    g = build_on_gpu(torch, w)
+    B = 64
+    for b0 in (0, w.num_batches() // 2):
+        announce("c4 step at batch %d: GPU sample" % b0)
+        roots, rts, base, got = gpu_step(torch, g, w, b0, B)
+        announce("c4 step at batch %d: oracle on the reached sub-graph" % b0)
+        src, dst, ts, eid = w.build_input()
+        og = subgraph.reach_tcsr(src, dst, ts, eid, w.num_nodes, True, roots, rts, w.fanouts, w.mode,
+                                 w.snapshots, w.snapshot_len, w.sample_seed, base)
+        want = oracle.sample(og, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
+                             w.sample_seed, base)
+        assert_hops_equal(got, want, "c4 step at batch %d" % b0)
+        rng = np.random.default_rng(b0)
+        check_runs(g, og, rng.choice(np.unique(roots), 300, replace=False))
+    del g
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _hot_and_random_roots(w, roots, n_random, n_hot, seed):
+    deg = np.bincount(np.concatenate([w.src, w.dst]), minlength=w.num_nodes)
+    hot = np.argsort(deg)[::-1][:n_hot]
+    pick = []
+    for x in hot:
+        where = np.nonzero(roots == x)[0]
+        if len(where):
+            pick.append(int(where[len(where) // 2]))
+    rng = np.random.default_rng(seed)
+    # random roots among the negatives (uniform nodes) keep the oracle's work
+    # bounded; every batch contributes [src; dst; neg] blocks of E roots each
+    E = w.batch_edges
+    blocks = len(roots) // (3 * E)
+    neg = (np.arange(blocks)[:, None] * 3 * E + 2 * E + np.arange(E)[None, :]).reshape(-1)
+    pick += [int(i) for i in rng.choice(neg, n_random, replace=False)]
+    return sorted(set(pick)), hot
+
+
+@pytest.mark.parametrize("name", ["c3", "c5"])
+def test_hot_runs_full_size(torch, name):
+    announce("%s full size: generate" % name)
+    w = W.make(name)
+    announce("%s full size: GPU build of %d edges" % (name, w.num_edges))
+    g = build_on_gpu(torch, w)
+    B = 64 if name == "c3" else 1
+    b0 = w.num_batches() // 2
+    announce("%s step at batch %d: GPU sample" % (name, b0))
+    roots, rts, base, got = gpu_step(torch, g, w, b0, B)
+    picks, hot = _hot_and_random_roots(w, roots, 24, 2, seed=7)
+    announce("%s: oracle for %d roots (%d on the hottest nodes)" % (name, len(picks), len(picks) - 24))
+    src, dst, ts, eid = w.build_input()
+    reach = np.unique(roots[picks])
+    og = subgraph.owned_tcsr(src, dst, ts, eid, w.num_nodes, reach)
+    if len(w.fanouts) > 1:
+        kids = []
+        for r in picks:
+            o = oracle.sample(og, roots[r:r + 1], rts[r:r + 1], w.fanouts[:1], w.mode, w.snapshots,
+                              w.snapshot_len, w.sample_seed, base + r)
+            kids.append(o[0].nbr[o[0].nbr >= 0])
+        reach = np.unique(np.concatenate([reach] + kids))
+        og = subgraph.owned_tcsr(src, dst, ts, eid, w.num_nodes, reach)
+    for r in picks:
+        assert_hops_equal(per_root(got, r, w.snapshots, w.fanouts),
+                          oracle_per_root(og, roots, rts, r, w, base), "%s root %d" % (name, r))
+    check_runs(g, og, np.unique(roots[picks]))
+    del g
+    gc.collect()
+    torch.cuda.empty_cache()

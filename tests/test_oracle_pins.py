@@ -257,3 +257,26 @@ def test_snapshot_windows_partition_history():
         assert np.array_equal(los[s], his[s + 1])
     lo_all, hi_all = oracle.locate(g, roots, rts, np.zeros(len(roots)), S * D)
     assert np.array_equal(los[S - 1], lo_all) and np.array_equal(his[0], hi_all)
+
+
+@pytest.mark.parametrize("name,kw", [
+    ("c4", dict(num_nodes=300_000, num_edges=3_200_000)),
+    ("c5", dict(num_nodes=30_000, num_edges=300_000, batch_edges=2_000)),
+])
+def test_reached_subgraph_equals_full_graph(name, kw):
+    """The oracle on the owned-entry sub-graph of the nodes a sample reaches
+    (used for checks at full size) gives exactly the full-graph result."""
+    from oracle import subgraph
+    w = W.make(name, **kw)
+    src, dst, ts, eid = w.build_input()
+    full = oracle.build_tcsr(src, dst, ts, eid, w.num_nodes, True)
+    b0 = w.num_batches() // 2
+    roots, rts, base = w.batches(b0, b0 + 3)
+    args = (w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
+    g = subgraph.reach_tcsr(src, dst, ts, eid, w.num_nodes, True, roots, rts, *args)
+    assert_hops_equal(oracle.sample(g, roots, rts, *args), oracle.sample(full, roots, rts, *args))
+    # the runs of the sampled nodes are identical
+    for x in np.unique(roots)[:200]:
+        a, b = full.indptr[x], full.indptr[x + 1]
+        c, d = g.indptr[x], g.indptr[x + 1]
+        assert np.array_equal(full.eid[a:b], g.eid[c:d]) and np.array_equal(full.ts[a:b], g.ts[c:d])
