@@ -61,6 +61,22 @@ typedef struct tgl_entry {
 } tgl_entry;
 
 /*
+ * Summary of one node's run, one 16-byte record per node: the run occupies
+ * entries [start, end); first_ts and last_ts are the timestamps of its first
+ * and last entry (+inf and -inf for an empty run).  The sampler reads it in
+ * place of the indptr pair.  A window edge at or below first_ts, or above
+ * last_ts, is then resolved without reading the run -- the O(1) candidate
+ * location that Section 3.1 obtains from per-node pointer arrays, kept here
+ * as stateless per-node data.
+ */
+typedef struct tgl_node {
+    uint32_t start;
+    uint32_t end;
+    float first_ts;
+    float last_ts;
+} tgl_node;
+
+/*
  * Non-owning view of a T-CSR (Section 3.1): node x owns entries
  * [indptr[x], indptr[x+1]) of `entries`, sorted by ts ascending (ties in any
  * fixed order; tgl_tcsr_build uses input order).  Timestamps must not be NaN.
@@ -70,6 +86,9 @@ typedef struct tgl_entry {
  *   ts       [device] float[num_entries], 16-byte aligned: ts[p] equals
  *                     entries[p].ts.  The window search reads only this array
  *                     (4 bytes per entry), the gather only `entries`.
+ *   nodes    [device] tgl_node[num_nodes], 16-byte aligned: the summary of
+ *                     each run (start = indptr[x], end = indptr[x+1]); see
+ *                     tgl_tcsr_nodes for a T-CSR built elsewhere.
  * num_entries must be at most 2^32 - 1.  The sampler clamps every indptr
  * value into [0, num_entries], so a malformed view yields wrong samples but
  * never an out-of-bounds access.
@@ -80,6 +99,7 @@ typedef struct tgl_tcsr {
     const int64_t *indptr;
     const tgl_entry *entries;
     const float *ts;
+    const tgl_node *nodes;
 } tgl_tcsr;
 
 /*
@@ -131,6 +151,7 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  *   entries    [device] tgl_entry[M]          output, 16-byte aligned
  *   ts_out     [device] float[M]              output, 16-byte aligned: the
  *                                             entries' timestamps again
+ *   nodes_out  [device] tgl_node[num_nodes]   output, 16-byte aligned
  *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
  * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
  * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
@@ -141,7 +162,20 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          void *workspace, size_t workspace_bytes, void *stream);
+                          tgl_node *nodes_out, void *workspace, size_t workspace_bytes,
+                          void *stream);
+
+/*
+ * Writes the per-node summaries of a T-CSR given by its indptr and timestamp
+ * arrays (for a T-CSR built elsewhere and uploaded).
+ *   indptr     [device] int64[num_nodes + 1]
+ *   ts         [device] float[num_entries]
+ *   num_nodes  in [1, 2^31 - 1];  num_entries in [0, 2^32 - 1]
+ *   nodes      [device] tgl_node[num_nodes], 16-byte aligned, output
+ * indptr values are clamped into [0, num_entries].  Never synchronises.
+ */
+tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
+                          int64_t num_entries, tgl_node *nodes, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */

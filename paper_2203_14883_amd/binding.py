@@ -29,7 +29,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
-           "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample", "tgl_timer_enable",
+           "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
 
@@ -41,7 +41,8 @@ class TglError(RuntimeError):
 
 class c_tcsr(C.Structure):
     _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
-                ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p)]
+                ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p),
+                ("nodes", C.c_void_p)]
 
 
 class c_hop_out(C.Structure):
@@ -69,7 +70,9 @@ def lib() -> C.CDLL:
     L.tgl_tcsr_build_workspace.restype = C.c_size_t
     L.tgl_tcsr_build_workspace.argtypes = [i64, i64, u32]
     L.tgl_tcsr_build.restype = i32
-    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, C.c_size_t, P]
+    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, C.c_size_t, P]
+    L.tgl_tcsr_nodes.restype = i32
+    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -120,10 +123,12 @@ def _i32_array(v: Sequence[int]):
 class TCSR:
     """Device T-CSR: indptr int64[N+1]; entries int64[M, 2] holding the 16-byte
     records (int32 nbr, float32 ts | int64 eid); ts float32[M], the entries'
-    timestamps as the separate search array."""
+    timestamps as the separate search array; nodes int32[N, 4], the per-node
+    run summaries (uint32 start, uint32 end, float32 first ts, float32 last ts)."""
     indptr: torch.Tensor
     entries: torch.Tensor
     ts: torch.Tensor
+    nodes: torch.Tensor
     num_nodes: int
 
     @property
@@ -145,7 +150,8 @@ class TCSR:
     def c_view(self) -> c_tcsr:
         m = self.num_entries
         return c_tcsr(self.num_nodes, m, self.indptr.data_ptr(),
-                      self.entries.data_ptr() if m else None, self.ts.data_ptr() if m else None)
+                      self.entries.data_ptr() if m else None, self.ts.data_ptr() if m else None,
+                      self.nodes.data_ptr())
 
 
 def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray:
@@ -166,7 +172,12 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda") -> TCSR:
     if ent.shape[0] == 0:
         ent = torch.empty((0, 2), dtype=torch.int64, device=device)
         tsa = torch.empty(0, dtype=torch.float32, device=device)
-    return TCSR(torch.from_numpy(np.asarray(indptr, np.int64)).to(device), ent, tsa, len(indptr) - 1)
+    n = len(indptr) - 1
+    ip = torch.from_numpy(np.asarray(indptr, np.int64)).to(device)
+    nodes = torch.empty((n, 4), dtype=torch.int32, device=device)
+    _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if tsa.numel() else None, n, int(ent.shape[0]),
+                                _p(nodes), _stream()), "tgl_tcsr_nodes")
+    return TCSR(ip, ent, tsa, nodes, n)
 
 
 def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:
@@ -191,6 +202,7 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     indptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
     entries = torch.empty((M, 2), dtype=torch.int64, device=dev)
     tsa = torch.empty(M, dtype=torch.float32, device=dev)
+    nodes = torch.empty((num_nodes, 4), dtype=torch.int32, device=dev)
     need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
     if need == 0:
         raise TglError(EINVAL, "tgl_tcsr_build_workspace")
@@ -198,12 +210,12 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     if own_ws:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     s = L.tgl_tcsr_build(_p(src), _p(dst), _p(ts), _p(eid), m0, num_nodes, flags, _p(indptr),
-                         _p(entries) if M else None, _p(tsa) if M else None, _p(workspace),
-                         workspace.numel(), _stream(stream))
+                         _p(entries) if M else None, _p(tsa) if M else None, _p(nodes),
+                         _p(workspace), workspace.numel(), _stream(stream))
     if own_ws:
         del workspace
     _check(s, "tgl_tcsr_build")
-    return TCSR(indptr, entries, tsa, num_nodes)
+    return TCSR(indptr, entries, tsa, nodes, num_nodes)
 
 
 # --------------------------------------------------------------------------

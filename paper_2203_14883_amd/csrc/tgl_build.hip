@@ -259,6 +259,23 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
     }
 }
 
+// Per-node run summaries {start, end, first ts, last ts}.
+__global__ __launch_bounds__(kBlock) void nodes_kernel(const int64_t *__restrict__ indptr,
+                                                       const float *__restrict__ ts, int64_t N, int64_t M,
+                                                       int4 *__restrict__ nodes) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < N; x += stride) {
+        int64_t a = indptr[x];
+        int64_t b = indptr[x + 1];
+        a = a < 0 ? 0 : (a > M ? M : a);
+        b = b < a ? a : (b > M ? M : b);
+        const float first = b > a ? ts[a] : __builtin_inff();
+        const float last = b > a ? ts[b - 1] : -__builtin_inff();
+        nodes[x] = make_int4(static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>(static_cast<uint32_t>(b)),
+                             __float_as_int(first), __float_as_int(last));
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void fill_indptr_kernel(int64_t *__restrict__ indptr, int64_t n,
                                                              int64_t value) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
@@ -322,10 +339,12 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          void *workspace, size_t workspace_bytes, void *stream) {
+                          tgl_node *nodes_out, void *workspace, size_t workspace_bytes,
+                          void *stream) {
     if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
     if (num_edges > 0 && (!src || !dst || !ts || !entries || !ts_out)) return TGL_EINVAL;
-    if (!indptr) return TGL_EINVAL;
+    if (!indptr || !nodes_out) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(nodes_out) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_out) & 15u) != 0) return TGL_EINVAL;
     const int64_t m0 = num_edges;
@@ -339,6 +358,8 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
 
     if (M == 0) {
         fill_indptr_kernel<<<grid_for(num_nodes + 1), kBlock, 0, st>>>(indptr, num_nodes + 1, 0);
+        nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts_out, num_nodes, 0,
+                                                             reinterpret_cast<int4 *>(nodes_out));
         return launch_status();
     }
 
@@ -372,6 +393,21 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     }
     emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes,
                                                indptr, reinterpret_cast<int4 *>(entries), ts_out);
+    nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
+                                                         reinterpret_cast<int4 *>(nodes_out));
+    return launch_status();
+}
+
+tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
+                          int64_t num_entries, tgl_node *nodes, void *stream) {
+    if (num_nodes < 1 || num_nodes > INT32_MAX) return TGL_EINVAL;
+    if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
+    if (!indptr || !nodes || (num_entries > 0 && !ts)) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(nodes) & 15u) != 0) return TGL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
+                                                         reinterpret_cast<int4 *>(nodes));
     return launch_status();
 }
 

@@ -45,6 +45,7 @@ struct HopArgs {
     const int64_t *indptr;
     const int4 *ent;            // tgl_entry viewed as 16-byte vectors
     const float *tsa;           // timestamps of the entries (search array)
+    const int4 *nodes;          // tgl_node per node: run start, end, first ts, last ts
     int64_t num_nodes;
     int64_t num_entries;
     // hop 1: dense roots
@@ -170,6 +171,46 @@ __device__ __forceinline__ double bound_value(float t, int32_t i, float delta) {
                   : static_cast<double>(t) - static_cast<double>(i) * static_cast<double>(delta);
 }
 
+// a + #{p in [a, b): ts[p] < v} when the run's first and last timestamps
+// decide it alone (the run is sorted): a if first >= v (or v is NaN), b if
+// last < v.  Returns false when the edge falls inside the run.
+__device__ __forceinline__ bool edge_from_summary(uint32_t a, uint32_t b, float first, float last, double v,
+                                                  uint32_t &c) {
+    if (!(static_cast<double>(first) < v)) {
+        c = a;
+        return true;
+    }
+    if (static_cast<double>(last) < v) {
+        c = b;
+        return true;
+    }
+    return false;
+}
+
+struct NodeRun {
+    uint32_t a, b;
+    float first, last;
+};
+
+// Run of node x from its summary record, clamped into [0, M]; an out-of-range
+// node has an empty run.
+__device__ __forceinline__ NodeRun node_run(const HopArgs &p, int32_t x, bool valid) {
+    NodeRun r{0u, 0u, __builtin_inff(), -__builtin_inff()};
+    if (valid && x >= 0 && x < p.num_nodes) {
+        const int4 nd = p.nodes[x];
+        const uint32_t M = static_cast<uint32_t>(p.num_entries);
+        uint32_t a = static_cast<uint32_t>(nd.x);
+        uint32_t b = static_cast<uint32_t>(nd.y);
+        a = a > M ? M : a;
+        b = b < a ? a : (b > M ? M : b);
+        r.a = a;
+        r.b = b;
+        r.first = __int_as_float(nd.z);
+        r.last = __int_as_float(nd.w);
+    }
+    return r;
+}
+
 template <bool LAST>
 __device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, bool valid, int4 v, float t) {
     int32_t nbr = -1;
@@ -204,32 +245,44 @@ __device__ __forceinline__ void wave_sync_lds() {
 // [a, b), queried at time t (window s0 unless MULTI, path) and whose slots
 // start at q * windows * k.  All G lanes of the group call it together.
 template <int G, int MODE, bool MULTI, bool LAST>
-__device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32_t a, uint32_t b, float t,
-                                             int32_t s0, uint64_t hp, int gl, uint32_t *my_edges) {
+__device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32_t a, uint32_t b, float first,
+                                             float last, float t, int32_t s0, uint64_t hp, int gl,
+                                             uint32_t *my_edges) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
-    // a run short enough is loaded once and serves every window edge
-    const bool held = b - a <= HeldRun<G>::span;      // group-uniform
-    HeldRun<G> run;
-    if (held) run = load_run<G>(p.tsa, a, b, M, gl);
-
     const int W = MULTI ? p.windows : 1;
     const int k = p.k;
+    // does any window edge fall inside the run? (group-uniform)
+    bool need = false;
+    {
+        uint32_t c;
+        if constexpr (MULTI) {
+            for (int i = 0; i <= W; i++) need |= !edge_from_summary(a, b, first, last, bound_value(t, i, p.delta), c);
+        } else {
+            need = !edge_from_summary(a, b, first, last, bound_value(t, s0, p.delta), c);
+            if (!p.delta_inf) need |= !edge_from_summary(a, b, first, last, bound_value(t, s0 + 1, p.delta), c);
+        }
+    }
+    // a run short enough is loaded once and serves every window edge
+    const bool held = need && b - a <= HeldRun<G>::span;      // group-uniform
+    HeldRun<G> run;
+    if (held) run = load_run<G>(p.tsa, a, b, M, gl);
+    auto edge = [&](double v) -> uint32_t {
+        uint32_t c;
+        if (edge_from_summary(a, b, first, last, v, c)) return c;
+        return held ? count_in<G>(run, a, b, v) : count_below<G>(p.tsa, a, b, M, v, gl);
+    };
+
     uint32_t lo = a, hi = a;
     if constexpr (MULTI) {
         // edges i = 0..W: window s spans [edge s+1, edge s)
         for (int i = 0; i <= W; i++) {
-            const double v = bound_value(t, i, p.delta);
-            const uint32_t c = held ? count_in<G>(run, a, b, v) : count_below<G>(p.tsa, a, b, M, v, gl);
+            const uint32_t c = edge(bound_value(t, i, p.delta));
             if (gl == 0) my_edges[i] = c;
         }
         wave_sync_lds();
     } else {
-        const double vh = bound_value(t, s0, p.delta);
-        hi = held ? count_in<G>(run, a, b, vh) : count_below<G>(p.tsa, a, b, M, vh, gl);
-        if (!p.delta_inf) {
-            const double vl = bound_value(t, s0 + 1, p.delta);
-            lo = held ? count_in<G>(run, a, b, vl) : count_below<G>(p.tsa, a, b, M, vl, gl);
-        }
+        hi = edge(bound_value(t, s0, p.delta));
+        if (!p.delta_inf) lo = edge(bound_value(t, s0 + 1, p.delta));
         if (lo > hi) lo = hi;
     }
 
@@ -291,7 +344,7 @@ __device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32
 //     packed, in order, into LDS;
 //   phase 2, G lanes per root, 64 / G roots per round: search, select, emit.
 template <int G, int MODE, bool MULTI, bool LAST, bool FIRST>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) void hop_kernel(const HopArgs p) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void hop_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots served per wavefront round
     constexpr int GPB = kBlock / G;
     const int lane = lane_id();
@@ -300,6 +353,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
     const int gw = lane / G;
     __shared__ uint32_t r_a[kWavesPerBlock][kWave];
     __shared__ uint32_t r_b[kWavesPerBlock][kWave];
+    __shared__ float r_f[kWavesPerBlock][kWave];
+    __shared__ float r_l[kWavesPerBlock][kWave];
     __shared__ int64_t r_q[kWavesPerBlock][kWave];
     __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
     __shared__ float r_t[kWavesPerBlock][kWave];
@@ -307,7 +362,6 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
     __shared__ uint32_t edges[MULTI ? GPB * (TGL_MAX_SNAPSHOTS + 1) : 1];
     uint32_t *my_edges = edges + (MULTI ? (w * GPW + gw) * (TGL_MAX_SNAPSHOTS + 1) : 0);
 
-    const int64_t M = p.num_entries;
     const int64_t pk = FIRST ? 1 : p.p_k;
     int64_t nv;
     if constexpr (FIRST) {
@@ -362,18 +416,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
                 }
             }
         }
-        int64_t a = 0, b = 0;
-        if (valid && x >= 0 && x < p.num_nodes) {
-            a = p.indptr[x];
-            b = p.indptr[x + 1];
-            a = a < 0 ? 0 : (a > M ? M : a);
-            b = b < a ? a : (b > M ? M : b);
-        }
+        const NodeRun run = node_run(p, x, valid);
         const uint64_t mask = __ballot(valid);
         if (valid) {
             const int r = __popcll(mask & (lane_bit - 1));
-            r_a[w][r] = static_cast<uint32_t>(a);
-            r_b[w][r] = static_cast<uint32_t>(b);
+            r_a[w][r] = run.a;
+            r_b[w][r] = run.b;
+            r_f[w][r] = run.first;
+            r_l[w][r] = run.last;
             r_q[w][r] = q;
             r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
             r_t[w][r] = t;
@@ -385,8 +435,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
         for (int base = 0; base < nvalid; base += GPW) {
             const int i = base + gw;
             if (i < nvalid) {                       // group-uniform
-                process_root<G, MODE, MULTI, LAST>(p, r_q[w][i], r_a[w][i], r_b[w][i], r_t[w][i], r_s[w][i],
-                                                   r_hp[w][i], gl, my_edges);
+                process_root<G, MODE, MULTI, LAST>(p, r_q[w][i], r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i],
+                                                   r_t[w][i], r_s[w][i], r_hp[w][i], gl, my_edges);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows
@@ -394,19 +444,24 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
 }
 
 // Window [lo, hi) of a root with run [a, b) at time t in window s0 (one
-// window per root), by the G lanes of its group.
+// window per root), by the G lanes of its group.  An edge that the run's
+// first and last timestamps decide is not searched.
 template <int G>
-__device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint32_t b, float t, int32_t s0,
-                                              int gl, uint32_t &lo, uint32_t &hi) {
+__device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint32_t b, float first, float last,
+                                              float t, int32_t s0, int gl, uint32_t &lo, uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     const double vh = bound_value(t, s0, p.delta);
+    const double vl = p.delta_inf ? 0.0 : bound_value(t, s0 + 1, p.delta);
+    uint32_t ch = a, cl = a;
+    const bool kh = edge_from_summary(a, b, first, last, vh, ch);
+    const bool kl = p.delta_inf || edge_from_summary(a, b, first, last, vl, cl);
     if (b - a <= HeldRun<G>::span) {                 // group-uniform
         const HeldRun<G> run = load_run<G>(p.tsa, a, b, M, gl);
-        hi = count_in<G>(run, a, b, vh);
-        lo = p.delta_inf ? a : count_in<G>(run, a, b, bound_value(t, s0 + 1, p.delta));
+        hi = kh ? ch : count_in<G>(run, a, b, vh);
+        lo = kl ? cl : count_in<G>(run, a, b, vl);
     } else {
-        hi = count_below<G>(p.tsa, a, b, M, vh, gl);
-        lo = p.delta_inf ? a : count_below<G>(p.tsa, a, b, M, bound_value(t, s0 + 1, p.delta), gl);
+        hi = kh ? ch : count_below<G>(p.tsa, a, b, M, vh, gl);
+        lo = kl ? cl : count_below<G>(p.tsa, a, b, M, vl, gl);
     }
     if (lo > hi) lo = hi;
 }
@@ -423,7 +478,7 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint
 //     have consecutive indices, so the slots of a chunk are one contiguous
 //     range of the output and the stores coalesce.
 template <int G, int MODE, bool LAST, bool FIRST>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) void hop_single_kernel(const HopArgs p) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) void hop_single_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots located per wavefront round
     constexpr int U = 4;                      // slots per lane whose loads are in flight together
     const int lane = lane_id();
@@ -432,12 +487,14 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
     const int gw = lane / G;
     __shared__ uint32_t r_lo[kWavesPerBlock][kWave];   // run start, then window start
     __shared__ uint32_t r_n[kWavesPerBlock][kWave];    // run end, then window size
+    __shared__ float r_f[kWavesPerBlock][kWave];       // first and last timestamp of the run
+    __shared__ float r_l[kWavesPerBlock][kWave];
     __shared__ int64_t r_q[kWavesPerBlock][kWave];
     __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
     __shared__ float r_t[kWavesPerBlock][kWave];
     __shared__ int32_t r_s[kWavesPerBlock][kWave];
+    __shared__ uint8_t r_need[kWavesPerBlock][kWave];  // packed roots whose window needs a search
 
-    const int64_t M = p.num_entries;
     const int64_t pk = FIRST ? 1 : p.p_k;
     int64_t nv;
     if constexpr (FIRST) {
@@ -494,37 +551,51 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(8))) voi
                 }
             }
         }
-        int64_t a = 0, b = 0;
-        if (valid && x >= 0 && x < p.num_nodes) {
-            a = p.indptr[x];
-            b = p.indptr[x + 1];
-            a = a < 0 ? 0 : (a > M ? M : a);
-            b = b < a ? a : (b > M ? M : b);
+        const NodeRun run = node_run(p, x, valid);
+        // window edges the run's first and last timestamps decide
+        uint32_t lo = run.a, hi = run.a;
+        bool need = false;
+        if (valid) {
+            need = !edge_from_summary(run.a, run.b, run.first, run.last, bound_value(t, s, p.delta), hi);
+            if (!p.delta_inf)
+                need |= !edge_from_summary(run.a, run.b, run.first, run.last, bound_value(t, s + 1, p.delta), lo);
+            if (lo > hi) lo = hi;
         }
         const uint64_t mask = __ballot(valid);
+        const uint64_t need_mask = __ballot(valid && need);
         if (valid) {
             const int r = __popcll(mask & (lane_bit - 1));
-            r_lo[w][r] = static_cast<uint32_t>(a);
-            r_n[w][r] = static_cast<uint32_t>(b);
+            r_lo[w][r] = need ? run.a : lo;
+            r_n[w][r] = need ? run.b : hi - lo;
+            r_f[w][r] = run.first;
+            r_l[w][r] = run.last;
             r_q[w][r] = q;
             r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
             r_t[w][r] = t;
             r_s[w][r] = s;
+            if (need) r_need[w][__popcll(need_mask & (lane_bit - 1))] = static_cast<uint8_t>(r);
+            if (!need && p.o_cnt) {
+                const uint32_t n = hi - lo;
+                p.o_cnt[q] = MODE == TGL_MOST_RECENT ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
+                                                     : (n > 0 ? k : 0);
+            }
         }
         wave_sync_lds();
         const int nvalid = __popcll(mask);
+        const int nneed = __popcll(need_mask);
 
-        // ---- phase 2: G lanes per root locate its window ----
-        for (int base = 0; base < nvalid; base += GPW) {
-            const int i = base + gw;
-            if (i < nvalid) {                       // group-uniform
-                uint32_t lo, hi;
-                locate_window<G>(p, r_lo[w][i], r_n[w][i], r_t[w][i], r_s[w][i], gl, lo, hi);
+        // ---- phase 2: G lanes per root search the windows phase 1 left open ----
+        for (int base = 0; base < nneed; base += GPW) {
+            if (base + gw < nneed) {                // group-uniform
+                const int i = r_need[w][base + gw];
+                uint32_t wlo, whi;
+                locate_window<G>(p, r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_t[w][i], r_s[w][i], gl,
+                                 wlo, whi);
                 if (gl == 0) {
-                    r_lo[w][i] = lo;
-                    r_n[w][i] = hi - lo;
+                    r_lo[w][i] = wlo;
+                    r_n[w][i] = whi - wlo;
                     if (p.o_cnt) {
-                        const uint32_t n = hi - lo;
+                        const uint32_t n = whi - wlo;
                         p.o_cnt[r_q[w][i]] = MODE == TGL_MOST_RECENT
                                                  ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
                                                  : (n > 0 ? k : 0);
@@ -719,6 +790,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     if (g->num_entries < 0 || g->num_entries > static_cast<int64_t>(UINT32_MAX)) return TGL_EINVAL;
     if (!g->indptr || (g->num_entries > 0 && !g->entries)) return TGL_EINVAL;
     if (g->num_entries > 0 && !g->ts) return TGL_EINVAL;
+    if (!g->nodes || (reinterpret_cast<uintptr_t>(g->nodes) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
     if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
@@ -740,6 +812,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     a.indptr = g->indptr;
     a.ent = reinterpret_cast<const int4 *>(g->entries);
     a.tsa = g->ts;
+    a.nodes = reinterpret_cast<const int4 *>(g->nodes);
     a.num_nodes = g->num_nodes;
     a.num_entries = g->num_entries;
     a.rx = roots;

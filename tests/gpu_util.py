@@ -39,6 +39,15 @@ def tcsr_to_host(g):
     w = ent.view(np.int32).reshape(-1, 4)
     ts = g.ts.cpu().numpy()
     assert np.array_equal(ts.view(np.int32), w[:, 1]), "ts array differs from the records"
+    ip = g.indptr.cpu().numpy()
+    nodes = g.nodes.cpu().numpy()
+    assert np.array_equal(nodes[:, 0].view(np.uint32), ip[:-1]), "node summary start"
+    assert np.array_equal(nodes[:, 1].view(np.uint32), ip[1:]), "node summary end"
+    nonempty = ip[1:] > ip[:-1]
+    first = np.where(nonempty, ts[np.minimum(ip[:-1], max(len(ts) - 1, 0))] if len(ts) else np.inf, np.inf).astype(np.float32)
+    last = np.where(nonempty, ts[np.maximum(ip[1:] - 1, 0)] if len(ts) else -np.inf, -np.inf).astype(np.float32)
+    assert np.array_equal(nodes[:, 2].view(np.float32).view(np.uint32), first.view(np.uint32)), "node summary first ts"
+    assert np.array_equal(nodes[:, 3].view(np.float32).view(np.uint32), last.view(np.uint32)), "node summary last ts"
     return oracle.TCSR(g.indptr.cpu().numpy(), w[:, 0].copy(), ent[:, 1].copy(),
                        w[:, 1].copy().view(np.float32))
 

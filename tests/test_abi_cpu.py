@@ -71,7 +71,7 @@ FAKE = 0x10000  # a non-null pointer value never dereferenced: every case fails 
 
 def _sample_call(**kw):
     L = P.lib()
-    args = dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE), roots=FAKE, root_ts=FAKE, n=5, hops=2,
+    args = dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE), roots=FAKE, root_ts=FAKE, n=5, hops=2,
                 fan=[10, 10], mode=1, S=1, D=math.inf, ws=FAKE, ws_bytes=1 << 30)
     args.update(kw)
     fa, fp = _fan(args["fan"])
@@ -90,10 +90,12 @@ def _sample_call(**kw):
     dict(hops=0), dict(hops=9, fan=[1] * 9), dict(fan=[0, 10]), dict(fan=[10, 1025]),
     dict(mode=2), dict(S=0), dict(S=65), dict(S=2, D=math.inf), dict(D=0.0), dict(D=-5.0),
     dict(D=math.nan), dict(n=-1), dict(roots=None), dict(root_ts=None),
-    dict(g=B.c_tcsr(0, 100, FAKE, FAKE, FAKE)), dict(g=B.c_tcsr(10, 100, None, FAKE, FAKE)),
-    dict(g=B.c_tcsr(10, 100, FAKE, None, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE + 8, FAKE)),
-    dict(g=B.c_tcsr(10, 100, FAKE, FAKE, None)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE + 4)),
-    dict(g=B.c_tcsr(2**31, 100, FAKE, FAKE, FAKE)), dict(g=None), dict(counts=None),
+    dict(g=B.c_tcsr(0, 100, FAKE, FAKE, FAKE, FAKE)), dict(g=B.c_tcsr(10, 100, None, FAKE, FAKE, FAKE)),
+    dict(g=B.c_tcsr(10, 100, FAKE, None, FAKE, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE + 8, FAKE, FAKE)),
+    dict(g=B.c_tcsr(10, 100, FAKE, FAKE, None, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE + 4, FAKE)),
+    dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, None)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE + 8)),
+    dict(g=B.c_tcsr(10, 2**32, FAKE, FAKE, FAKE, FAKE)),
+    dict(g=B.c_tcsr(2**31, 100, FAKE, FAKE, FAKE, FAKE)), dict(g=None), dict(counts=None),
 ])
 def test_sample_rejects_invalid_arguments(kw):
     assert _sample_call(**kw) == B.EINVAL
@@ -116,10 +118,10 @@ def test_sample_workspace_too_small():
 def _build_call(**kw):
     L = P.lib()
     a = dict(src=FAKE, dst=FAKE, ts=FAKE, eid=None, m=10, n=5, flags=1, indptr=FAKE,
-             ent=FAKE, ts_out=FAKE, ws=FAKE, ws_bytes=1 << 30)
+             ent=FAKE, ts_out=FAKE, nodes=FAKE, ws=FAKE, ws_bytes=1 << 30)
     a.update(kw)
     return L.tgl_tcsr_build(a["src"], a["dst"], a["ts"], a["eid"], a["m"], a["n"], a["flags"],
-                            a["indptr"], a["ent"], a["ts_out"], a["ws"], a["ws_bytes"], None)
+                            a["indptr"], a["ent"], a["ts_out"], a["nodes"], a["ws"], a["ws_bytes"], None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -128,10 +130,19 @@ def _build_call(**kw):
     (dict(ts=None), B.EINVAL), (dict(ent=None), B.EINVAL), (dict(indptr=None), B.EINVAL),
     (dict(ent=FAKE + 4), B.EINVAL), (dict(m=2**31), B.EINVAL),
     (dict(ts_out=None), B.EINVAL), (dict(ts_out=FAKE + 8), B.EINVAL),
+    (dict(nodes=None), B.EINVAL), (dict(nodes=FAKE + 4), B.EINVAL),
     (dict(ws_bytes=8), B.ENOSPACE), (dict(ws=None), B.ENOSPACE),
 ])
 def test_build_rejects_invalid_arguments(kw, want):
     assert _build_call(**kw) == want
+
+
+def test_nodes_rejects_invalid_arguments():
+    L = P.lib()
+    for args in [(FAKE, FAKE, 0, 10, FAKE), (FAKE, FAKE, 2**31, 10, FAKE), (FAKE, FAKE, 5, -1, FAKE),
+                 (FAKE, FAKE, 5, 2**32, FAKE), (None, FAKE, 5, 10, FAKE), (FAKE, None, 5, 10, FAKE),
+                 (FAKE, FAKE, 5, 10, None), (FAKE, FAKE, 5, 10, FAKE + 4)]:
+        assert L.tgl_tcsr_nodes(*args, None) == B.EINVAL, args
 
 
 def test_timer_argument_checks():
