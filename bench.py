@@ -111,7 +111,8 @@ def cpu_baseline(w, nbatches):
     node the sample reaches.  Only the oracle's sampling call is timed."""
     import oracle
     from oracle import subgraph
-    b0 = w.num_batches() // 2
+    nbatches = min(nbatches, w.num_batches())
+    b0 = min(w.num_batches() // 2, w.num_batches() - nbatches)
     roots, rts, base = w.batches(b0, b0 + nbatches)
     src, dst, ts, eid = w.build_input()
     g = subgraph.reach_tcsr(src, dst, ts, eid, w.num_nodes, w.undirected, roots, rts, w.fanouts,
