@@ -46,6 +46,7 @@ typedef int32_t tgl_status;
 #define TGL_MAX_HOPS      8
 #define TGL_MAX_FANOUT    1024
 #define TGL_MAX_SNAPSHOTS 64
+#define TGL_INDEX_STRIDE  32   /* entries per sample of the search index */
 
 /*
  * One T-CSR entry: an edge leaving the owner node (whose run contains the
@@ -89,6 +90,12 @@ typedef struct tgl_node {
  *   nodes    [device] tgl_node[num_nodes], 16-byte aligned: the summary of
  *                     each run (start = indptr[x], end = indptr[x+1]); see
  *                     tgl_tcsr_nodes for a T-CSR built elsewhere.
+ *   ts_index [device] float[tgl_index_len(num_entries)], 16-byte aligned, or
+ *                     NULL: ts_index[j] = ts[j * TGL_INDEX_STRIDE].  A search
+ *                     over a long run first narrows on this array (1/32 of the
+ *                     timestamps, small enough to stay in cache), then reads
+ *                     at most TGL_INDEX_STRIDE - 1 timestamps of the run.
+ *                     Results are the same with or without it.
  * num_entries must be at most 2^32 - 1.  The sampler clamps every indptr
  * value into [0, num_entries], so a malformed view yields wrong samples but
  * never an out-of-bounds access.
@@ -100,6 +107,7 @@ typedef struct tgl_tcsr {
     const tgl_entry *entries;
     const float *ts;
     const tgl_node *nodes;
+    const float *ts_index;
 } tgl_tcsr;
 
 /*
@@ -152,6 +160,8 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  *   ts_out     [device] float[M]              output, 16-byte aligned: the
  *                                             entries' timestamps again
  *   nodes_out  [device] tgl_node[num_nodes]   output, 16-byte aligned
+ *   ts_index_out [device] float[tgl_index_len(M)] output, 16-byte aligned, or
+ *                                             NULL (no search index)
  *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
  * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
  * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
@@ -162,20 +172,27 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          tgl_node *nodes_out, void *workspace, size_t workspace_bytes,
-                          void *stream);
+                          tgl_node *nodes_out, float *ts_index_out, void *workspace,
+                          size_t workspace_bytes, void *stream);
+
+/* Length of the search index of a T-CSR with num_entries entries:
+ * ceil(num_entries / TGL_INDEX_STRIDE), or -1 if num_entries is negative. */
+int64_t tgl_index_len(int64_t num_entries);
 
 /*
- * Writes the per-node summaries of a T-CSR given by its indptr and timestamp
- * arrays (for a T-CSR built elsewhere and uploaded).
+ * Writes the per-node summaries and, if ts_index is not NULL, the search index
+ * of a T-CSR given by its indptr and timestamp arrays (for a T-CSR built
+ * elsewhere and uploaded).
  *   indptr     [device] int64[num_nodes + 1]
  *   ts         [device] float[num_entries]
  *   num_nodes  in [1, 2^31 - 1];  num_entries in [0, 2^32 - 1]
  *   nodes      [device] tgl_node[num_nodes], 16-byte aligned, output
+ *   ts_index   [device] float[tgl_index_len(num_entries)], 16-byte aligned,
+ *              output, or NULL
  * indptr values are clamped into [0, num_entries].  Never synchronises.
  */
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
-                          int64_t num_entries, tgl_node *nodes, void *stream);
+                          int64_t num_entries, tgl_node *nodes, float *ts_index, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */

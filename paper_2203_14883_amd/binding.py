@@ -29,7 +29,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
-           "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample", "tgl_timer_enable",
+           "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
 
@@ -42,7 +42,7 @@ class TglError(RuntimeError):
 class c_tcsr(C.Structure):
     _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
                 ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p),
-                ("nodes", C.c_void_p)]
+                ("nodes", C.c_void_p), ("ts_index", C.c_void_p)]
 
 
 class c_hop_out(C.Structure):
@@ -70,9 +70,11 @@ def lib() -> C.CDLL:
     L.tgl_tcsr_build_workspace.restype = C.c_size_t
     L.tgl_tcsr_build_workspace.argtypes = [i64, i64, u32]
     L.tgl_tcsr_build.restype = i32
-    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, C.c_size_t, P]
+    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, P, C.c_size_t, P]
+    L.tgl_index_len.restype = i64
+    L.tgl_index_len.argtypes = [i64]
     L.tgl_tcsr_nodes.restype = i32
-    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P]
+    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -124,12 +126,15 @@ class TCSR:
     """Device T-CSR: indptr int64[N+1]; entries int64[M, 2] holding the 16-byte
     records (int32 nbr, float32 ts | int64 eid); ts float32[M], the entries'
     timestamps as the separate search array; nodes int32[N, 4], the per-node
-    run summaries (uint32 start, uint32 end, float32 first ts, float32 last ts)."""
+    run summaries (uint32 start, uint32 end, float32 first ts, float32 last ts);
+    ts_index float32[ceil(M / 32)], every 32nd timestamp (the search index), or
+    None."""
     indptr: torch.Tensor
     entries: torch.Tensor
     ts: torch.Tensor
     nodes: torch.Tensor
     num_nodes: int
+    ts_index: Optional[torch.Tensor] = None
 
     @property
     def num_entries(self) -> int:
@@ -151,7 +156,8 @@ class TCSR:
         m = self.num_entries
         return c_tcsr(self.num_nodes, m, self.indptr.data_ptr(),
                       self.entries.data_ptr() if m else None, self.ts.data_ptr() if m else None,
-                      self.nodes.data_ptr())
+                      self.nodes.data_ptr(),
+                      self.ts_index.data_ptr() if m and self.ts_index is not None else None)
 
 
 def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray:
@@ -164,8 +170,13 @@ def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray
     return rec.view(np.int64).reshape(m, 2)
 
 
-def tcsr_from_host(indptr, nbr, ts, eid, device="cuda") -> TCSR:
-    """Uploads a T-CSR given as host arrays (e.g. one built elsewhere)."""
+def index_len(num_entries: int) -> int:
+    return int(lib().tgl_index_len(int(num_entries)))
+
+
+def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True) -> TCSR:
+    """Uploads a T-CSR given as host arrays (e.g. one built elsewhere) and
+    computes its node summaries and, if `index`, its search index."""
     rec = pack_entries(nbr, ts, eid)
     ent = torch.from_numpy(rec).to(device)
     tsa = torch.from_numpy(np.ascontiguousarray(np.asarray(ts, np.float32))).to(device)
@@ -175,9 +186,11 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda") -> TCSR:
     n = len(indptr) - 1
     ip = torch.from_numpy(np.asarray(indptr, np.int64)).to(device)
     nodes = torch.empty((n, 4), dtype=torch.int32, device=device)
-    _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if tsa.numel() else None, n, int(ent.shape[0]),
-                                _p(nodes), _stream()), "tgl_tcsr_nodes")
-    return TCSR(ip, ent, tsa, nodes, n)
+    m = int(ent.shape[0])
+    tsx = torch.empty(index_len(m), dtype=torch.float32, device=device) if index else None
+    _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if m else None, n, m, _p(nodes),
+                                _p(tsx) if index and m else None, _stream()), "tgl_tcsr_nodes")
+    return TCSR(ip, ent, tsa, nodes, n, tsx)
 
 
 def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:
@@ -187,8 +200,9 @@ def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True
 
 def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
                eid: Optional[torch.Tensor], num_nodes: int, undirected: bool = True,
-               workspace: Optional[torch.Tensor] = None, stream=None) -> TCSR:
-    """Builds the T-CSR of a device COO (int32 src/dst, float32 ts, int64 eid or None)."""
+               workspace: Optional[torch.Tensor] = None, stream=None, index: bool = True) -> TCSR:
+    """Builds the T-CSR of a device COO (int32 src/dst, float32 ts, int64 eid or
+    None), with its search index if `index`."""
     L = lib()
     m0 = int(src.shape[0])
     flags = BUILD_UNDIRECTED if undirected else 0
@@ -203,6 +217,7 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     entries = torch.empty((M, 2), dtype=torch.int64, device=dev)
     tsa = torch.empty(M, dtype=torch.float32, device=dev)
     nodes = torch.empty((num_nodes, 4), dtype=torch.int32, device=dev)
+    tsx = torch.empty(index_len(M), dtype=torch.float32, device=dev) if index else None
     need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
     if need == 0:
         raise TglError(EINVAL, "tgl_tcsr_build_workspace")
@@ -211,11 +226,12 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     s = L.tgl_tcsr_build(_p(src), _p(dst), _p(ts), _p(eid), m0, num_nodes, flags, _p(indptr),
                          _p(entries) if M else None, _p(tsa) if M else None, _p(nodes),
-                         _p(workspace), workspace.numel(), _stream(stream))
+                         _p(tsx) if index and M else None, _p(workspace), workspace.numel(),
+                         _stream(stream))
     if own_ws:
         del workspace
     _check(s, "tgl_tcsr_build")
-    return TCSR(indptr, entries, tsa, nodes, num_nodes)
+    return TCSR(indptr, entries, tsa, nodes, num_nodes, tsx)
 
 
 # --------------------------------------------------------------------------

@@ -276,6 +276,14 @@ __global__ __launch_bounds__(kBlock) void nodes_kernel(const int64_t *__restrict
     }
 }
 
+// Search index: every TGL_INDEX_STRIDE-th timestamp.
+__global__ __launch_bounds__(kBlock) void index_kernel(const float *__restrict__ ts, int64_t L,
+                                                       float *__restrict__ idx) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < L; j += stride)
+        idx[j] = ts[j * TGL_INDEX_STRIDE];
+}
+
 __global__ __launch_bounds__(kBlock) void fill_indptr_kernel(int64_t *__restrict__ indptr, int64_t n,
                                                              int64_t value) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
@@ -339,12 +347,13 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          tgl_node *nodes_out, void *workspace, size_t workspace_bytes,
-                          void *stream) {
+                          tgl_node *nodes_out, float *ts_index_out, void *workspace,
+                          size_t workspace_bytes, void *stream) {
     if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
     if (num_edges > 0 && (!src || !dst || !ts || !entries || !ts_out)) return TGL_EINVAL;
     if (!indptr || !nodes_out) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(nodes_out) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(ts_index_out) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_out) & 15u) != 0) return TGL_EINVAL;
     const int64_t m0 = num_edges;
@@ -395,19 +404,33 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
                                                indptr, reinterpret_cast<int4 *>(entries), ts_out);
     nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
                                                          reinterpret_cast<int4 *>(nodes_out));
+    if (ts_index_out && M > 0) {
+        const int64_t L = tgl_index_len(M);
+        index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts_out, L, ts_index_out);
+    }
     return launch_status();
 }
 
+int64_t tgl_index_len(int64_t num_entries) {
+    if (num_entries < 0) return -1;
+    return num_entries / TGL_INDEX_STRIDE + (num_entries % TGL_INDEX_STRIDE != 0);
+}
+
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
-                          int64_t num_entries, tgl_node *nodes, void *stream) {
+                          int64_t num_entries, tgl_node *nodes, float *ts_index, void *stream) {
     if (num_nodes < 1 || num_nodes > INT32_MAX) return TGL_EINVAL;
     if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
     if (!indptr || !nodes || (num_entries > 0 && !ts)) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(nodes) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(ts_index) & 15u) != 0) return TGL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
                                                          reinterpret_cast<int4 *>(nodes));
+    if (ts_index && num_entries > 0) {
+        const int64_t L = tgl_index_len(num_entries);
+        index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts, L, ts_index);
+    }
     return launch_status();
 }
 

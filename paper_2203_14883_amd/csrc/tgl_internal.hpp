@@ -52,6 +52,12 @@ inline tgl_status launch_status() {
 
 __device__ __forceinline__ int lane_id() { return static_cast<int>(threadIdx.x & (kWave - 1)); }
 
+// Number of set bits of a wave-wide mask below the calling lane.
+__device__ __forceinline__ int rank_below(uint64_t mask) {
+    return static_cast<int>(__builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                      __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u)));
+}
+
 // Ballot restricted to the G-lane group of the calling lane (bit i = lane i
 // of the group).  Lanes of one group must be active together.
 template <int G>

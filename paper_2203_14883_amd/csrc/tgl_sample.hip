@@ -6,12 +6,16 @@
 // is its fallback for layers >= 2.  On the GPU every root is served by a group
 // of G lanes of one wavefront, with no shared mutable state:
 //
-//   1. window location: the root's run is [indptr[x], indptr[x+1]).  The
-//      search reads only the T-CSR's separate timestamp array.  A run of up to
-//      4G - 3 entries is loaded whole, four timestamps per lane (one 16-byte
-//      load each), and every window edge is a few ballots over it; a longer run
-//      is first narrowed G-ary (G probes per round, one ballot), about
-//      log_{G+1}(d / 4G) dependent loads, then finished the same way;
+//   1. window location: the root's run [start, end) and its first and last
+//      timestamps come from the node's 16-byte summary; a window edge those
+//      decide is not searched.  The search reads only the T-CSR's separate
+//      timestamp array.  A short run is loaded whole, 16-byte loads spread over
+//      the group's lanes, and every edge is a few ballots over it; a longer
+//      run is narrowed G-ary (G probes per round, one ballot), first on the
+//      search index (every 32nd timestamp, cache-resident) when the graph has
+//      one, so that only the last load of a search reads the run itself.  All
+//      edges of one root are searched together: their probes of a round are in
+//      flight at once;
 //   2. selection: lane j of the group takes slot j (most recent: the j-th
 //      newest candidate; uniform: a counter-hash draw keyed by the root's path);
 //   3. gather + emit: one aligned 16-byte load of the chosen T-CSR record per
@@ -45,6 +49,8 @@ struct HopArgs {
     const int64_t *indptr;
     const int4 *ent;            // tgl_entry viewed as 16-byte vectors
     const float *tsa;           // timestamps of the entries (search array)
+    const float *tsx;           // search index: every TGL_INDEX_STRIDE-th timestamp, or null
+    uint32_t nx;                // its length
     const int4 *nodes;          // tgl_node per node: run start, end, first ts, last ts
     int64_t num_nodes;
     int64_t num_entries;
@@ -129,58 +135,138 @@ __device__ __forceinline__ int group_sum(int c) {
     return c;
 }
 
-// lo + #{p in [lo, hi): (double)ts[p] < v} for [lo, hi) inside the held stretch.
+// lo + #{p in [lo, hi): ts[p] < v} for [lo, hi) inside the held stretch.
 template <int G>
-__device__ __forceinline__ uint32_t count_in(const HeldRun<G> &r, uint32_t lo, uint32_t hi, double v) {
+__device__ __forceinline__ uint32_t count_in(const HeldRun<G> &r, uint32_t lo, uint32_t hi, float v) {
     int c = 0;
 #pragma unroll
     for (int m = 0; m < HeldRun<G>::NV; m++) {
         const uint32_t p = r.p0 + 4 * m;
-        c += (p >= lo && p < hi && static_cast<double>(r.v[m].x) < v);
-        c += (p + 1 >= lo && p + 1 < hi && static_cast<double>(r.v[m].y) < v);
-        c += (p + 2 >= lo && p + 2 < hi && static_cast<double>(r.v[m].z) < v);
-        c += (p + 3 >= lo && p + 3 < hi && static_cast<double>(r.v[m].w) < v);
+        c += (p >= lo && p < hi && r.v[m].x < v);
+        c += (p + 1 >= lo && p + 1 < hi && r.v[m].y < v);
+        c += (p + 2 >= lo && p + 2 < hi && r.v[m].z < v);
+        c += (p + 3 >= lo && p + 3 < hi && r.v[m].w < v);
     }
     return lo + static_cast<uint32_t>(group_sum<G>(c));
 }
 
-// Number of entries p in [lo, hi) of a time-sorted run with (double)ts[p] < v,
-// found by the G lanes of one group together.  While the range is longer than
-// one held stretch, each round probes G evenly spaced positions; the probes
-// below v form a prefix, whose length narrows the range to one gap.  A NaN
-// bound compares false everywhere and gives lo.
-template <int G>
-__device__ __forceinline__ uint32_t count_below(const float *__restrict__ tsa, uint32_t lo, uint32_t hi,
-                                                uint32_t M, double v, int gl) {
-    while (hi - lo > HeldRun<G>::span) {
-        const uint64_t len = hi - lo;
-        const uint32_t pos = lo + static_cast<uint32_t>((static_cast<uint64_t>(gl + 1) * len) / (G + 1));
-        const bool below = static_cast<double>(tsa[pos]) < v;
-        const int c = __popcll(group_ballot<G>(below));
-        const uint32_t nlo = c > 0 ? lo + static_cast<uint32_t>((static_cast<uint64_t>(c) * len) / (G + 1)) + 1 : lo;
-        const uint32_t nhi = c < G ? lo + static_cast<uint32_t>((static_cast<uint64_t>(c + 1) * len) / (G + 1)) : hi;
-        lo = nlo;
-        hi = nhi;
+// For each i: lo[i] += #{p in [lo[i], hi[i]): arr[p] < v[i]}, over a sorted
+// stretch of arr (n_arr elements), found by the G lanes of one group together.
+// While a range is longer than one held stretch, each round probes G evenly
+// spaced positions of it; the probes below v[i] form a prefix, whose length
+// narrows the range to one gap; the last range is loaded whole and counted.
+// The NE searches advance together, so the probes of one round, and the final
+// loads, of all of them are in flight at the same time: the chain of dependent
+// loads is that of one search.
+template <int G, int NE>
+__device__ __forceinline__ void search_n(const float *__restrict__ arr, uint32_t n_arr, uint32_t (&lo)[NE],
+                                         uint32_t (&hi)[NE], const float (&v)[NE], int gl) {
+    for (;;) {
+        bool any = false;
+#pragma unroll
+        for (int i = 0; i < NE; i++) any |= hi[i] - lo[i] > HeldRun<G>::span;
+        if (!any) break;                            // group-uniform
+        // probes at lo + j * step, j = 1..G, step = len / (G + 1) >= 1: all
+        // inside (lo, hi), strictly increasing
+        float probe[NE];
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            probe[i] = 0.0f;
+            const uint32_t len = hi[i] - lo[i];
+            if (len > HeldRun<G>::span)
+                probe[i] = arr[lo[i] + static_cast<uint32_t>(gl + 1) * (len / (G + 1))];
+        }
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            const uint32_t len = hi[i] - lo[i];
+            if (len > HeldRun<G>::span) {           // group-uniform
+                const uint32_t step = len / (G + 1);
+                const uint32_t c = static_cast<uint32_t>(__popcll(group_ballot<G>(probe[i] < v[i])));
+                // probes 1..c are below v[i], probe c+1 (if any) is not
+                const uint32_t nlo = c > 0 ? lo[i] + c * step + 1 : lo[i];
+                if (c < G) hi[i] = lo[i] + (c + 1) * step;
+                lo[i] = nlo;
+            }
+        }
     }
-    return count_in<G>(load_run<G>(tsa, lo, hi, M, gl), lo, hi, v);
+    HeldRun<G> r[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) r[i] = load_run<G>(arr, lo[i], hi[i], n_arr, gl);
+#pragma unroll
+    for (int i = 0; i < NE; i++) lo[i] = count_in<G>(r[i], lo[i], hi[i], v[i]);
 }
 
-__device__ __forceinline__ double bound_value(float t, int32_t i, float delta) {
-    // upper edge of window i (= lower edge of window i - 1): t - i * delta
-    return i == 0 ? static_cast<double>(t)
-                  : static_cast<double>(t) - static_cast<double>(i) * static_cast<double>(delta);
+// Positions below NE thresholds in the time-sorted run [lo0, hi0) of the
+// timestamp array (M entries): out[i] = lo0 + #{p in [lo0, hi0): ts[p] < v[i]}
+// for each i with act[i] (out[i] = lo0 otherwise).  A run of at most one held
+// stretch is loaded once and serves every threshold.  A run long enough to
+// need more than one probe round is first narrowed on the search index tsx
+// (nx samples, tsx[j] = ts[j * TGL_INDEX_STRIDE]) when there is one: with r
+// the samples inside the run below v[i], the answer lies after sample r - 1
+// and at or before sample r, fewer than TGL_INDEX_STRIDE timestamps.
+template <int G, int NE>
+__device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uint32_t M,
+                                              const float *__restrict__ tsx, uint32_t nx, uint32_t lo0,
+                                              uint32_t hi0, const float (&v)[NE], const bool (&act)[NE],
+                                              uint32_t (&out)[NE], int gl) {
+    constexpr uint32_t X = TGL_INDEX_STRIDE;
+    if (hi0 - lo0 <= HeldRun<G>::span) {           // group-uniform: one load serves every bound
+        const HeldRun<G> r = load_run<G>(tsa, lo0, hi0, M, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++) out[i] = act[i] ? count_in<G>(r, lo0, hi0, v[i]) : lo0;
+        return;
+    }
+    uint32_t lo[NE], hi[NE];
+    if (tsx && hi0 - lo0 > HeldRun<G>::span * (G + 1)) {   // group-uniform
+        // samples j in [ja, jb) are the positions j * X inside [lo0, hi0)
+        const uint32_t ja = lo0 / X + (lo0 % X != 0);
+        const uint32_t jb = hi0 / X + (hi0 % X != 0);
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            lo[i] = ja;
+            hi[i] = act[i] ? jb : ja;
+        }
+        search_n<G, NE>(tsx, nx, lo, hi, v, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            const uint32_t r = lo[i];
+            lo[i] = r > ja ? (r - 1) * X + 1 : lo0;  // ts[(r-1) X] < v[i]
+            hi[i] = r < jb ? r * X : hi0;            // ts[r X] >= v[i]
+            if (!act[i]) hi[i] = lo[i];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            lo[i] = lo0;
+            hi[i] = act[i] ? hi0 : lo0;
+        }
+    }
+    search_n<G, NE>(tsa, M, lo, hi, v, gl);
+#pragma unroll
+    for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0;
+}
+
+// Upper edge of window i (= lower edge of window i - 1), t - i * delta, as a
+// float threshold.  Window membership compares a timestamp with the edge
+// computed in double; rounding the edge up to the nearest float f >= edge (+inf
+// above the float range, NaN for NaN) gives the same answer for every float
+// timestamp x: x < edge exactly when x < f, as no float lies in [edge, f).
+__device__ __forceinline__ float bound_value(float t, int32_t i, float delta) {
+    const double e = i == 0 ? static_cast<double>(t)
+                            : static_cast<double>(t) - static_cast<double>(i) * static_cast<double>(delta);
+    return __double2float_ru(e);
 }
 
 // a + #{p in [a, b): ts[p] < v} when the run's first and last timestamps
 // decide it alone (the run is sorted): a if first >= v (or v is NaN), b if
 // last < v.  Returns false when the edge falls inside the run.
-__device__ __forceinline__ bool edge_from_summary(uint32_t a, uint32_t b, float first, float last, double v,
+__device__ __forceinline__ bool edge_from_summary(uint32_t a, uint32_t b, float first, float last, float v,
                                                   uint32_t &c) {
-    if (!(static_cast<double>(first) < v)) {
+    if (!(first < v)) {
         c = a;
         return true;
     }
-    if (static_cast<double>(last) < v) {
+    if (last < v) {
         c = b;
         return true;
     }
@@ -241,70 +327,55 @@ __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// Window location, selection and emission for one root whose run is
-// [a, b), queried at time t (window s0 unless MULTI, path) and whose slots
-// start at q * windows * k.  All G lanes of the group call it together.
-template <int G, int MODE, bool MULTI, bool LAST>
-__device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32_t a, uint32_t b, float first,
-                                             float last, float t, int32_t s0, uint64_t hp, int gl,
-                                             uint32_t *my_edges) {
+// Window edges, selection and emission for one root of a first hop with S
+// windows: run [a, b) with first and last timestamps, query time t, hash key
+// hp; its slots start at q * S * k.  All G lanes of the group call it
+// together; my_edges is the group's row of LDS.
+template <int G, int MODE, bool LAST>
+__device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, uint32_t a, uint32_t b, float first,
+                                           float last, float t, uint64_t hp, int gl, uint32_t *my_edges) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
-    const int W = MULTI ? p.windows : 1;
+    const int W = p.windows;
     const int k = p.k;
-    // does any window edge fall inside the run? (group-uniform)
-    bool need = false;
-    {
-        uint32_t c;
-        if constexpr (MULTI) {
-            for (int i = 0; i <= W; i++) need |= !edge_from_summary(a, b, first, last, bound_value(t, i, p.delta), c);
-        } else {
-            need = !edge_from_summary(a, b, first, last, bound_value(t, s0, p.delta), c);
-            if (!p.delta_inf) need |= !edge_from_summary(a, b, first, last, bound_value(t, s0 + 1, p.delta), c);
+    // edges i = 0..W: window s spans [edge s+1, edge s).  Bounds fall with i,
+    // so edge i lies in [a, edge i-1]: edges are located four at a time, each
+    // batch inside what the previous one left.  An edge that the run's first
+    // and last timestamps decide is not searched.
+    constexpr int NE = 4;
+    uint32_t top = b;
+    for (int i0 = 0; i0 <= W; i0 += NE) {
+        float v[NE];
+        bool act[NE];
+        uint32_t c[NE];
+#pragma unroll
+        for (int u = 0; u < NE; u++) {
+            v[u] = bound_value(t, i0 + u, p.delta);
+            c[u] = a;
+            act[u] = i0 + u <= W && !edge_from_summary(a, b, first, last, v[u], c[u]);
+        }
+        uint32_t cs[NE];
+        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, a, top, v, act, cs, gl);
+#pragma unroll
+        for (int u = 0; u < NE; u++) {
+            if (i0 + u <= W) {
+                const uint32_t e = act[u] ? cs[u] : c[u];
+                if (gl == 0) my_edges[i0 + u] = e;
+                top = e < top ? e : top;
+            }
         }
     }
-    // a run short enough is loaded once and serves every window edge
-    const bool held = need && b - a <= HeldRun<G>::span;      // group-uniform
-    HeldRun<G> run;
-    if (held) run = load_run<G>(p.tsa, a, b, M, gl);
-    auto edge = [&](double v) -> uint32_t {
-        uint32_t c;
-        if (edge_from_summary(a, b, first, last, v, c)) return c;
-        return held ? count_in<G>(run, a, b, v) : count_below<G>(p.tsa, a, b, M, v, gl);
-    };
-
-    uint32_t lo = a, hi = a;
-    if constexpr (MULTI) {
-        // edges i = 0..W: window s spans [edge s+1, edge s)
-        for (int i = 0; i <= W; i++) {
-            const uint32_t c = edge(bound_value(t, i, p.delta));
-            if (gl == 0) my_edges[i] = c;
-        }
-        wave_sync_lds();
-    } else {
-        hi = edge(bound_value(t, s0, p.delta));
-        if (!p.delta_inf) lo = edge(bound_value(t, s0 + 1, p.delta));
-        if (lo > hi) lo = hi;
-    }
+    wave_sync_lds();
 
     const int nslots = W * k;
     const int64_t obase = q * static_cast<int64_t>(nslots);
     for (int base = 0; base < nslots; base += G) {   // group-uniform trip count
         const int e = base + gl;
-        int s, j;
-        uint32_t wlo, whi;
-        if constexpr (MULTI) {
-            const int ee = e < nslots ? e : nslots - 1;
-            s = ee / k;
-            j = ee - s * k;
-            whi = my_edges[s];
-            wlo = my_edges[s + 1];
-            if (wlo > whi) wlo = whi;
-        } else {
-            s = s0;
-            j = e;
-            whi = hi;
-            wlo = lo;
-        }
+        const int ee = e < nslots ? e : nslots - 1;
+        const int s = ee / k;
+        const int j = ee - s * k;
+        const uint32_t whi = my_edges[s];
+        uint32_t wlo = my_edges[s + 1];
+        if (wlo > whi) wlo = whi;
         const uint32_t n = whi - wlo;
         bool has = false;
         uint32_t pick = 0;
@@ -318,14 +389,14 @@ __device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32
             pick = wlo + static_cast<uint32_t>(__umul64hi(mix64(hp ^ key), static_cast<uint64_t>(n)));
         }
         const bool valid = e < nslots && has;
-        const int4 v = valid ? p.ent[pick] : make_int4(-1, -1, -1, -1);
-        if (e < nslots) emit_slot<LAST>(p, obase + e, valid, v, t);
+        const int4 rec = valid ? p.ent[pick] : make_int4(-1, -1, -1, -1);
+        if (e < nslots) emit_slot<LAST>(p, obase + e, valid, rec, t);
     }
 
     if (p.o_cnt) {
         for (int w = gl; w < W; w += G) {
-            uint32_t whi = MULTI ? my_edges[w] : hi;
-            uint32_t wlo = MULTI ? my_edges[w + 1] : lo;
+            const uint32_t whi = my_edges[w];
+            uint32_t wlo = my_edges[w + 1];
             if (wlo > whi) wlo = whi;
             const uint32_t n = whi - wlo;
             const int32_t c = MODE == TGL_MOST_RECENT ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
@@ -333,18 +404,16 @@ __device__ __forceinline__ void process_root(const HopArgs &p, int64_t q, uint32
             p.o_cnt[q * W + w] = c;
         }
     }
-    if constexpr (MULTI) wave_sync_lds();   // my_edges is rewritten by the next root
+    wave_sync_lds();   // my_edges is rewritten by the group's next root
 }
 
-// One hop.  Each wavefront takes chunks of 64 candidate roots:
-//   phase 1, one lane per candidate: hop 1 takes root v as given; later hops
-//     take slot v of the previous hop, valid when its nbr >= 0, as the root
-//     with index off[v / k_prev] + v % k_prev (and write its parent index).
-//     Every lane loads its root's time and run bounds; the valid roots are
-//     packed, in order, into LDS;
-//   phase 2, G lanes per root, 64 / G roots per round: search, select, emit.
-template <int G, int MODE, bool MULTI, bool LAST, bool FIRST>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) void hop_kernel(const HopArgs p) {
+// First hop with S > 1 windows.  Each wavefront takes chunks of 64 roots:
+//   phase 1, one lane per root: its time, path key and node summary are
+//     packed into LDS;
+//   phase 2, G lanes per root, 64 / G roots per round: the S + 1 window
+//     edges, then selection and emission of the root's S * k slots.
+template <int G, int MODE, bool LAST>
+__global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots served per wavefront round
     constexpr int GPB = kBlock / G;
     const int lane = lane_id();
@@ -355,88 +424,44 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(6))) voi
     __shared__ uint32_t r_b[kWavesPerBlock][kWave];
     __shared__ float r_f[kWavesPerBlock][kWave];
     __shared__ float r_l[kWavesPerBlock][kWave];
-    __shared__ int64_t r_q[kWavesPerBlock][kWave];
     __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
     __shared__ float r_t[kWavesPerBlock][kWave];
-    __shared__ int32_t r_s[kWavesPerBlock][kWave];
-    __shared__ uint32_t edges[MULTI ? GPB * (TGL_MAX_SNAPSHOTS + 1) : 1];
-    uint32_t *my_edges = edges + (MULTI ? (w * GPW + gw) * (TGL_MAX_SNAPSHOTS + 1) : 0);
+    __shared__ uint32_t edges[GPB * (TGL_MAX_SNAPSHOTS + 1)];
+    uint32_t *my_edges = edges + (w * GPW + gw) * (TGL_MAX_SNAPSHOTS + 1);
 
-    const int64_t pk = FIRST ? 1 : p.p_k;
-    int64_t nv;
-    if constexpr (FIRST) {
-        nv = p.num_roots;
-        if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = nv;
-    } else {
-        const int64_t groups = p.p_groups_dyn ? *p.p_groups_dyn : p.p_groups_static;
-        nv = groups * pk;
-    }
+    const int64_t nv = p.num_roots;
+    if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = nv;
     const int64_t nchunks = (nv + kWave - 1) / kWave;
-    const uint64_t S = static_cast<uint64_t>(p.S);
-    const uint64_t path1 = p.root_base * S * static_cast<uint64_t>(pk);   // hop-1 children: + v
-    const uint64_t lane_bit = 1ull << lane;
 
     for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w; c < nchunks;
          c += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
-        // ---- phase 1: one lane per candidate root ----
+        // ---- phase 1: one lane per root ----
         const int64_t v = c * kWave + lane;
-        bool valid;
+        const bool valid = v < nv;
         int32_t x = -1;
         float t = 0.0f;
-        int64_t q = 0;
-        int32_t s = 0;
-        uint64_t path = 0;
-        if constexpr (FIRST) {
-            valid = v < nv;
-            if (valid) {
-                x = p.rx[v];
-                t = p.rt[v];
-                q = v;
-                path = p.root_base + static_cast<uint64_t>(v);
-            }
-        } else {
-            x = v < nv ? p.p_nbr[v] : -1;
-            valid = x >= 0;
-            if (valid) {
-                t = p.p_ts[v];
-                const int64_t g = v / pk;
-                const int64_t j = v - g * pk;
-                q = p.p_off[g] + j;
-                if (p.p_s) {
-                    s = p.p_s[g];
-                    path = p.p_path[g] * static_cast<uint64_t>(pk) + static_cast<uint64_t>(j);
-                } else {
-                    s = static_cast<int32_t>(static_cast<uint64_t>(g) % S);
-                    path = path1 + static_cast<uint64_t>(v);
-                }
-                p.o_parent[q] = v;
-                if (p.o_s) {
-                    p.o_s[q] = s;
-                    p.o_path[q] = path;
-                }
-            }
+        if (valid) {
+            x = p.rx[v];
+            t = p.rt[v];
         }
         const NodeRun run = node_run(p, x, valid);
-        const uint64_t mask = __ballot(valid);
         if (valid) {
-            const int r = __popcll(mask & (lane_bit - 1));
-            r_a[w][r] = run.a;
-            r_b[w][r] = run.b;
-            r_f[w][r] = run.first;
-            r_l[w][r] = run.last;
-            r_q[w][r] = q;
-            r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
-            r_t[w][r] = t;
-            r_s[w][r] = s;
+            r_a[w][lane] = run.a;
+            r_b[w][lane] = run.b;
+            r_f[w][lane] = run.first;
+            r_l[w][lane] = run.last;
+            r_hp[w][lane] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ (p.root_base + static_cast<uint64_t>(v))) : 0;
+            r_t[w][lane] = t;
         }
         wave_sync_lds();
         // ---- phase 2: G lanes per root ----
-        const int nvalid = __popcll(mask);
+        const int64_t rem = nv - c * kWave;
+        const int nvalid = rem < kWave ? static_cast<int>(rem) : kWave;
         for (int base = 0; base < nvalid; base += GPW) {
             const int i = base + gw;
             if (i < nvalid) {                       // group-uniform
-                process_root<G, MODE, MULTI, LAST>(p, r_q[w][i], r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i],
-                                                   r_t[w][i], r_s[w][i], r_hp[w][i], gl, my_edges);
+                multi_root<G, MODE, LAST>(p, c * kWave + i, r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i], r_t[w][i],
+                                          r_hp[w][i], gl, my_edges);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows
@@ -450,19 +475,17 @@ template <int G>
 __device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint32_t b, float first, float last,
                                               float t, int32_t s0, int gl, uint32_t &lo, uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
-    const double vh = bound_value(t, s0, p.delta);
-    const double vl = p.delta_inf ? 0.0 : bound_value(t, s0 + 1, p.delta);
+    const float vh = bound_value(t, s0, p.delta);
+    const float vl = p.delta_inf ? 0.0f : bound_value(t, s0 + 1, p.delta);
     uint32_t ch = a, cl = a;
     const bool kh = edge_from_summary(a, b, first, last, vh, ch);
     const bool kl = p.delta_inf || edge_from_summary(a, b, first, last, vl, cl);
-    if (b - a <= HeldRun<G>::span) {                 // group-uniform
-        const HeldRun<G> run = load_run<G>(p.tsa, a, b, M, gl);
-        hi = kh ? ch : count_in<G>(run, a, b, vh);
-        lo = kl ? cl : count_in<G>(run, a, b, vl);
-    } else {
-        hi = kh ? ch : count_below<G>(p.tsa, a, b, M, vh, gl);
-        lo = kl ? cl : count_below<G>(p.tsa, a, b, M, vl, gl);
-    }
+    const float v[2] = {vh, vl};
+    const bool act[2] = {!kh, !kl};
+    uint32_t c[2];
+    count_below_n<G, 2>(p.tsa, M, p.tsx, p.nx, a, b, v, act, c, gl);
+    hi = kh ? ch : c[0];
+    lo = kl ? cl : c[1];
     if (lo > hi) lo = hi;
 }
 
@@ -507,7 +530,6 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
     const int64_t nchunks = (nv + kWave - 1) / kWave;
     const uint64_t S = static_cast<uint64_t>(p.S);
     const uint64_t path1 = p.root_base * S * static_cast<uint64_t>(pk);   // hop-1 children: + v
-    const uint64_t lane_bit = 1ull << lane;
     const int k = p.k;
     const uint64_t hop_key = static_cast<uint64_t>(p.hop) << 40;
 
@@ -564,7 +586,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
         const uint64_t mask = __ballot(valid);
         const uint64_t need_mask = __ballot(valid && need);
         if (valid) {
-            const int r = __popcll(mask & (lane_bit - 1));
+            const int r = rank_below(mask);
             r_lo[w][r] = need ? run.a : lo;
             r_n[w][r] = need ? run.b : hi - lo;
             r_f[w][r] = run.first;
@@ -573,7 +595,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
             r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
             r_t[w][r] = t;
             r_s[w][r] = s;
-            if (need) r_need[w][__popcll(need_mask & (lane_bit - 1))] = static_cast<uint8_t>(r);
+            if (need) r_need[w][rank_below(need_mask)] = static_cast<uint8_t>(r);
             if (!need && p.o_cnt) {
                 const uint32_t n = hi - lo;
                 p.o_cnt[q] = MODE == TGL_MOST_RECENT ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
@@ -644,15 +666,19 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
     }
 }
 
-template <int G, int MODE, bool MULTI, bool LAST>
-void launch_g(bool first, const HopArgs &a, int64_t work, hipStream_t st) {
+template <int MODE, bool LAST>
+void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t work, hipStream_t st) {
     // `work` candidate roots (hop 1: roots; later hops: previous slots), 64 per wavefront
     int64_t blocks = (work + kBlock - 1) / kBlock;
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxGrid) blocks = kMaxGrid;
     const unsigned nb = static_cast<unsigned>(blocks);
-    if constexpr (MULTI) {
-        if (first) hop_kernel<G, MODE, true, LAST, true><<<nb, kBlock, 0, st>>>(a);
+    if (multi) {                              // first hop only
+        switch (G) {
+            case 16: hop_multi_kernel<16, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_kernel<32, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_kernel<64, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
+        }
     } else {
         // the window search uses 8 lanes per root whatever the fanout
         if (first) hop_single_kernel<8, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a);
@@ -660,28 +686,15 @@ void launch_g(bool first, const HopArgs &a, int64_t work, hipStream_t st) {
     }
 }
 
-template <int MODE, bool MULTI, bool LAST>
-void launch_m(int G, bool first, const HopArgs &a, int64_t work, hipStream_t st) {
-    switch (G) {
-        case 16: launch_g<16, MODE, MULTI, LAST>(first, a, work, st); break;
-        case 32: launch_g<32, MODE, MULTI, LAST>(first, a, work, st); break;
-        default: launch_g<64, MODE, MULTI, LAST>(first, a, work, st); break;
-    }
-}
-
-template <int MODE>
-void launch_mode(int G, bool first, bool multi, bool last, const HopArgs &a, int64_t work, hipStream_t st) {
-    if (multi) {
-        last ? launch_m<MODE, true, true>(G, first, a, work, st) : launch_m<MODE, true, false>(G, first, a, work, st);
-    } else {
-        last ? launch_m<MODE, false, true>(G, first, a, work, st) : launch_m<MODE, false, false>(G, first, a, work, st);
-    }
-}
-
 void launch_hop(int G, int mode, bool first, bool multi, bool last, const HopArgs &a, int64_t work,
                 hipStream_t st) {
-    if (mode == TGL_MOST_RECENT) launch_mode<TGL_MOST_RECENT>(G, first, multi, last, a, work, st);
-    else launch_mode<TGL_UNIFORM>(G, first, multi, last, a, work, st);
+    if (mode == TGL_MOST_RECENT) {
+        last ? launch_mode_last<TGL_MOST_RECENT, true>(G, first, multi, a, work, st)
+             : launch_mode_last<TGL_MOST_RECENT, false>(G, first, multi, a, work, st);
+    } else {
+        last ? launch_mode_last<TGL_UNIFORM, true>(G, first, multi, a, work, st)
+             : launch_mode_last<TGL_UNIFORM, false>(G, first, multi, a, work, st);
+    }
 }
 
 // lanes per root for first hops with several windows: the slot count rounded
@@ -793,6 +806,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     if (!g->nodes || (reinterpret_cast<uintptr_t>(g->nodes) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->ts_index) & 15u) != 0) return TGL_EINVAL;
     if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
     int64_t cap[TGL_MAX_HOPS + 1];
     if (!capacities(num_roots, hops, fanouts, num_snapshots, cap)) return TGL_EINVAL;
@@ -812,6 +826,8 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     a.indptr = g->indptr;
     a.ent = reinterpret_cast<const int4 *>(g->entries);
     a.tsa = g->ts;
+    a.tsx = g->num_entries > 0 ? g->ts_index : nullptr;
+    a.nx = static_cast<uint32_t>(tgl_index_len(g->num_entries));
     a.nodes = reinterpret_cast<const int4 *>(g->nodes);
     a.num_nodes = g->num_nodes;
     a.num_entries = g->num_entries;

@@ -48,6 +48,9 @@ def tcsr_to_host(g):
     last = np.where(nonempty, ts[np.maximum(ip[1:] - 1, 0)] if len(ts) else -np.inf, -np.inf).astype(np.float32)
     assert np.array_equal(nodes[:, 2].view(np.float32).view(np.uint32), first.view(np.uint32)), "node summary first ts"
     assert np.array_equal(nodes[:, 3].view(np.float32).view(np.uint32), last.view(np.uint32)), "node summary last ts"
+    if g.ts_index is not None:
+        tsx = g.ts_index.cpu().numpy()
+        assert np.array_equal(tsx.view(np.uint32), ts[::32].view(np.uint32)), "search index"
     return oracle.TCSR(g.indptr.cpu().numpy(), w[:, 0].copy(), ent[:, 1].copy(),
                        w[:, 1].copy().view(np.float32))
 

@@ -94,6 +94,7 @@ def _sample_call(**kw):
     dict(g=B.c_tcsr(10, 100, FAKE, None, FAKE, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE + 8, FAKE, FAKE)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, None, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE + 4, FAKE)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, None)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE + 8)),
+    dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE, FAKE + 4)),
     dict(g=B.c_tcsr(10, 2**32, FAKE, FAKE, FAKE, FAKE)),
     dict(g=B.c_tcsr(2**31, 100, FAKE, FAKE, FAKE, FAKE)), dict(g=None), dict(counts=None),
 ])
@@ -118,10 +119,11 @@ def test_sample_workspace_too_small():
 def _build_call(**kw):
     L = P.lib()
     a = dict(src=FAKE, dst=FAKE, ts=FAKE, eid=None, m=10, n=5, flags=1, indptr=FAKE,
-             ent=FAKE, ts_out=FAKE, nodes=FAKE, ws=FAKE, ws_bytes=1 << 30)
+             ent=FAKE, ts_out=FAKE, nodes=FAKE, tsx=None, ws=FAKE, ws_bytes=1 << 30)
     a.update(kw)
     return L.tgl_tcsr_build(a["src"], a["dst"], a["ts"], a["eid"], a["m"], a["n"], a["flags"],
-                            a["indptr"], a["ent"], a["ts_out"], a["nodes"], a["ws"], a["ws_bytes"], None)
+                            a["indptr"], a["ent"], a["ts_out"], a["nodes"], a["tsx"], a["ws"], a["ws_bytes"],
+                            None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -130,7 +132,7 @@ def _build_call(**kw):
     (dict(ts=None), B.EINVAL), (dict(ent=None), B.EINVAL), (dict(indptr=None), B.EINVAL),
     (dict(ent=FAKE + 4), B.EINVAL), (dict(m=2**31), B.EINVAL),
     (dict(ts_out=None), B.EINVAL), (dict(ts_out=FAKE + 8), B.EINVAL),
-    (dict(nodes=None), B.EINVAL), (dict(nodes=FAKE + 4), B.EINVAL),
+    (dict(nodes=None), B.EINVAL), (dict(nodes=FAKE + 4), B.EINVAL), (dict(tsx=FAKE + 8), B.EINVAL),
     (dict(ws_bytes=8), B.ENOSPACE), (dict(ws=None), B.ENOSPACE),
 ])
 def test_build_rejects_invalid_arguments(kw, want):
@@ -142,7 +144,14 @@ def test_nodes_rejects_invalid_arguments():
     for args in [(FAKE, FAKE, 0, 10, FAKE), (FAKE, FAKE, 2**31, 10, FAKE), (FAKE, FAKE, 5, -1, FAKE),
                  (FAKE, FAKE, 5, 2**32, FAKE), (None, FAKE, 5, 10, FAKE), (FAKE, None, 5, 10, FAKE),
                  (FAKE, FAKE, 5, 10, None), (FAKE, FAKE, 5, 10, FAKE + 4)]:
-        assert L.tgl_tcsr_nodes(*args, None) == B.EINVAL, args
+        assert L.tgl_tcsr_nodes(*args, None, None) == B.EINVAL, args
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, FAKE + 4, None) == B.EINVAL
+
+
+def test_index_len():
+    L = P.lib()
+    for m, want in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (64, 2), (65, 3), (2**32 - 1, 2**27), (-1, -1)]:
+        assert L.tgl_index_len(m) == want, m
 
 
 def test_timer_argument_checks():

@@ -4,6 +4,7 @@ Every comparison is on the same seeded inputs: the T-CSR built on the GPU
 must equal the oracle's T-CSR, and sampling on the GPU must equal the
 oracle's sampling (nbr, eid, float32 ts and dt bit patterns, parent indices,
 per-hop root counts)."""
+import dataclasses
 import math
 
 import numpy as np
@@ -186,3 +187,35 @@ def test_degenerate_cases(torch):
     announce("self loop")
     out = gpu_sample(g, np.array([0, 0], np.int32), np.array([6, 5], np.float32), [3], "recent", 1, math.inf, 1, 0)
     assert out[0]["nbr"].tolist() == [0, 0, -1, -1, -1, -1]
+
+
+def test_long_runs_and_off_grid_window_edges(torch):
+    """Runs whose lengths straddle the held-stretch sizes of the 8-, 16-, 32- and
+    64-lane searches (61/62, 125/126, 253/254) plus long runs, timestamps on a
+    1/16 grid near 1e6 with ties, and window lengths (0.1, 0.37) whose edges
+    t - i*delta fall between adjacent float32 values; 1..64 snapshots, so the
+    edges of a root are located in batches with ragged last batches."""
+    rng = np.random.default_rng(77)
+    lens = [200_000, 61, 62, 125, 126, 253, 254, 5_000, 1]
+    N = len(lens) + 1                     # the last node has no entries
+    src = np.concatenate([np.full(L, x, np.int32) for x, L in enumerate(lens)])
+    dst = rng.integers(0, N, len(src)).astype(np.int32)
+    ts = np.concatenate([np.float32(1e6) + np.float32(0.0625) * rng.integers(0, max(2, L // 3), L).astype(np.float32)
+                         for L in lens]).astype(np.float32)
+    want_g = oracle.build_tcsr(src, dst, ts, None, N, False)
+    g = gpu_build(src, dst, ts, None, N, False)
+    assert_tcsr_equal(tcsr_to_host(g), want_g, "long runs")
+    assert g.ts_index is not None
+    g_plain = dataclasses.replace(g, ts_index=None)
+    for S, D, R in [(1, math.inf, 3000), (1, 0.1, 3000), (3, 0.37, 3000), (7, 0.1, 1500), (8, 0.37, 1500),
+                    (9, 0.1, 1000), (64, 0.1, 300)]:
+        roots = rng.integers(0, N, R).astype(np.int32)
+        span = np.float32(0.0625) * np.float32(70_000)
+        rts = (np.float32(1e6) + rng.random(R, dtype=np.float32) * span).astype(np.float32)
+        rts[: R // 3] = ts[rng.integers(0, len(ts), R // 3)]          # query times equal to timestamps
+        for mode in ("recent", "uniform"):
+            announce("long runs S=%d D=%s R=%d mode=%s" % (S, D, R, mode))
+            want = oracle.sample(want_g, roots, rts, [10, 5], mode, S, D, 11, 3)
+            for gg, what in ((g, "indexed"), (g_plain, "no index")):
+                got = gpu_sample(gg, roots, rts, [10, 5], mode, S, D, 11, 3)
+                assert_hops_equal(got, want, "S=%d D=%s %s %s" % (S, D, mode, what))
