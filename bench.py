@@ -293,7 +293,7 @@ def main():
                                    "compaction": comp_ms / args.steps},
         },
         "roofline": {
-            "kernel": "hop_kernel (hops >= 2)",
+            "kernel": "hop_single_kernel (hops >= 2)",
             "bound": "hbm",
             "achieved": achieved,
             "peak": PEAK_HBM_GBS,

@@ -62,19 +62,24 @@ typedef struct tgl_entry {
 } tgl_entry;
 
 /*
- * Summary of one node's run, one 16-byte record per node: the run occupies
- * entries [start, end); first_ts and last_ts are the timestamps of its first
- * and last entry (+inf and -inf for an empty run).  The sampler reads it in
- * place of the indptr pair.  A window edge at or below first_ts, or above
- * last_ts, is then resolved without reading the run -- the O(1) candidate
- * location that Section 3.1 obtains from per-node pointer arrays, kept here
- * as stateless per-node data.
+ * Summary of one node's run, one 128-byte record (one cache line) per node:
+ * the run occupies entries [start, end); first_ts and last_ts are the
+ * timestamps of its first and last entry (+inf and -inf for an empty run);
+ * ts[i] is the timestamp of entry start + i for i < min(end - start,
+ * TGL_NODE_INLINE), +inf beyond.  The sampler reads it in place of the indptr
+ * pair.  A window edge at or below first_ts, or above last_ts, is then
+ * resolved without reading the run -- the O(1) candidate location that
+ * Section 3.1 obtains from per-node pointer arrays, kept here as stateless
+ * per-node data -- and a run of at most TGL_NODE_INLINE entries is searched
+ * inside the same line.
  */
+#define TGL_NODE_INLINE 28
 typedef struct tgl_node {
     uint32_t start;
     uint32_t end;
     float first_ts;
     float last_ts;
+    float ts[TGL_NODE_INLINE];
 } tgl_node;
 
 /*
@@ -87,7 +92,7 @@ typedef struct tgl_node {
  *   ts       [device] float[num_entries], 16-byte aligned: ts[p] equals
  *                     entries[p].ts.  The window search reads only this array
  *                     (4 bytes per entry), the gather only `entries`.
- *   nodes    [device] tgl_node[num_nodes], 16-byte aligned: the summary of
+ *   nodes    [device] tgl_node[num_nodes], 128-byte aligned: the summary of
  *                     each run (start = indptr[x], end = indptr[x+1]); see
  *                     tgl_tcsr_nodes for a T-CSR built elsewhere.
  *   ts_index [device] float[tgl_index_len(num_entries)], 16-byte aligned, or
@@ -159,7 +164,7 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  *   entries    [device] tgl_entry[M]          output, 16-byte aligned
  *   ts_out     [device] float[M]              output, 16-byte aligned: the
  *                                             entries' timestamps again
- *   nodes_out  [device] tgl_node[num_nodes]   output, 16-byte aligned
+ *   nodes_out  [device] tgl_node[num_nodes]   output, 128-byte aligned
  *   ts_index_out [device] float[tgl_index_len(M)] output, 16-byte aligned, or
  *                                             NULL (no search index)
  *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
@@ -186,7 +191,7 @@ int64_t tgl_index_len(int64_t num_entries);
  *   indptr     [device] int64[num_nodes + 1]
  *   ts         [device] float[num_entries]
  *   num_nodes  in [1, 2^31 - 1];  num_entries in [0, 2^32 - 1]
- *   nodes      [device] tgl_node[num_nodes], 16-byte aligned, output
+ *   nodes      [device] tgl_node[num_nodes], 128-byte aligned, output
  *   ts_index   [device] float[tgl_index_len(num_entries)], 16-byte aligned,
  *              output, or NULL
  * indptr values are clamped into [0, num_entries].  Never synchronises.

@@ -24,6 +24,10 @@ BUILD_UNDIRECTED = 1
 MAX_HOPS, MAX_FANOUT, MAX_SNAPSHOTS = 8, 1024, 64
 TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD = 0, 1, 2, 3
 
+NODE_WORDS = 32     # int32 words of one node record (128 bytes)
+NODE_INLINE = 28    # timestamps held inline in a node record
+INDEX_STRIDE = 32   # entries per sample of the search index
+
 MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
          MOST_RECENT: MOST_RECENT, UNIFORM: UNIFORM}
 
@@ -125,8 +129,9 @@ def _i32_array(v: Sequence[int]):
 class TCSR:
     """Device T-CSR: indptr int64[N+1]; entries int64[M, 2] holding the 16-byte
     records (int32 nbr, float32 ts | int64 eid); ts float32[M], the entries'
-    timestamps as the separate search array; nodes int32[N, 4], the per-node
-    run summaries (uint32 start, uint32 end, float32 first ts, float32 last ts);
+    timestamps as the separate search array; nodes int32[N, 32], the per-node
+    128-byte records (uint32 start, uint32 end, float32 first ts, float32 last
+    ts, then float32 ts of the run's first 28 entries, +inf beyond);
     ts_index float32[ceil(M / 32)], every 32nd timestamp (the search index), or
     None."""
     indptr: torch.Tensor
@@ -185,7 +190,7 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True) -> T
         tsa = torch.empty(0, dtype=torch.float32, device=device)
     n = len(indptr) - 1
     ip = torch.from_numpy(np.asarray(indptr, np.int64)).to(device)
-    nodes = torch.empty((n, 4), dtype=torch.int32, device=device)
+    nodes = torch.empty((n, NODE_WORDS), dtype=torch.int32, device=device)
     m = int(ent.shape[0])
     tsx = torch.empty(index_len(m), dtype=torch.float32, device=device) if index else None
     _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if m else None, n, m, _p(nodes),
@@ -216,7 +221,7 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     indptr = torch.empty(num_nodes + 1, dtype=torch.int64, device=dev)
     entries = torch.empty((M, 2), dtype=torch.int64, device=dev)
     tsa = torch.empty(M, dtype=torch.float32, device=dev)
-    nodes = torch.empty((num_nodes, 4), dtype=torch.int32, device=dev)
+    nodes = torch.empty((num_nodes, NODE_WORDS), dtype=torch.int32, device=dev)
     tsx = torch.empty(index_len(M), dtype=torch.float32, device=dev) if index else None
     need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
     if need == 0:

@@ -259,20 +259,35 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
     }
 }
 
-// Per-node run summaries {start, end, first ts, last ts}.
+// Per-node records {start, end, first ts, last ts, ts[0..27]}: eight lanes per
+// node, lane i writing the i-th 16 bytes of the node's 128-byte record.
 __global__ __launch_bounds__(kBlock) void nodes_kernel(const int64_t *__restrict__ indptr,
                                                        const float *__restrict__ ts, int64_t N, int64_t M,
                                                        int4 *__restrict__ nodes) {
+    constexpr int kParts = static_cast<int>(sizeof(tgl_node) / 16);
+    static_assert(sizeof(tgl_node) == 128 && TGL_NODE_INLINE == 4 * (kParts - 1), "node record layout");
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t x = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; x < N; x += stride) {
+    const int64_t total = N * kParts;
+    for (int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; g < total; g += stride) {
+        const int64_t x = g / kParts;
+        const int part = static_cast<int>(g - x * kParts);
         int64_t a = indptr[x];
         int64_t b = indptr[x + 1];
         a = a < 0 ? 0 : (a > M ? M : a);
         b = b < a ? a : (b > M ? M : b);
-        const float first = b > a ? ts[a] : __builtin_inff();
-        const float last = b > a ? ts[b - 1] : -__builtin_inff();
-        nodes[x] = make_int4(static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>(static_cast<uint32_t>(b)),
-                             __float_as_int(first), __float_as_int(last));
+        int4 v;
+        if (part == 0) {
+            const float first = b > a ? ts[a] : __builtin_inff();
+            const float last = b > a ? ts[b - 1] : -__builtin_inff();
+            v = make_int4(static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>(static_cast<uint32_t>(b)),
+                          __float_as_int(first), __float_as_int(last));
+        } else {
+            const int64_t p = a + 4 * (part - 1);
+            const float inf = __builtin_inff();
+            v = make_int4(__float_as_int(p < b ? ts[p] : inf), __float_as_int(p + 1 < b ? ts[p + 1] : inf),
+                          __float_as_int(p + 2 < b ? ts[p + 2] : inf), __float_as_int(p + 3 < b ? ts[p + 3] : inf));
+        }
+        nodes[g] = v;
     }
 }
 
@@ -352,7 +367,7 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
     if (num_edges > 0 && (!src || !dst || !ts || !entries || !ts_out)) return TGL_EINVAL;
     if (!indptr || !nodes_out) return TGL_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(nodes_out) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(nodes_out) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_index_out) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_out) & 15u) != 0) return TGL_EINVAL;
@@ -367,8 +382,8 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
 
     if (M == 0) {
         fill_indptr_kernel<<<grid_for(num_nodes + 1), kBlock, 0, st>>>(indptr, num_nodes + 1, 0);
-        nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts_out, num_nodes, 0,
-                                                             reinterpret_cast<int4 *>(nodes_out));
+        nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, 0,
+                                                                 reinterpret_cast<int4 *>(nodes_out));
         return launch_status();
     }
 
@@ -402,8 +417,8 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     }
     emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes,
                                                indptr, reinterpret_cast<int4 *>(entries), ts_out);
-    nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
-                                                         reinterpret_cast<int4 *>(nodes_out));
+    nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
+                                                             reinterpret_cast<int4 *>(nodes_out));
     if (ts_index_out && M > 0) {
         const int64_t L = tgl_index_len(M);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts_out, L, ts_index_out);
@@ -421,12 +436,12 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
     if (num_nodes < 1 || num_nodes > INT32_MAX) return TGL_EINVAL;
     if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
     if (!indptr || !nodes || (num_entries > 0 && !ts)) return TGL_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(nodes) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(nodes) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_index) & 15u) != 0) return TGL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
-    nodes_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
-                                                         reinterpret_cast<int4 *>(nodes));
+    nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
+                                                             reinterpret_cast<int4 *>(nodes));
     if (ts_index && num_entries > 0) {
         const int64_t L = tgl_index_len(num_entries);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts, L, ts_index);

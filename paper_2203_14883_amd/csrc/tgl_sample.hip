@@ -51,7 +51,8 @@ struct HopArgs {
     const float *tsa;           // timestamps of the entries (search array)
     const float *tsx;           // search index: every TGL_INDEX_STRIDE-th timestamp, or null
     uint32_t nx;                // its length
-    const int4 *nodes;          // tgl_node per node: run start, end, first ts, last ts
+    const int4 *nodes;          // tgl_node per node (8 x 16 bytes): run start, end, first ts,
+                                // last ts, then the run's first timestamps
     int64_t num_nodes;
     int64_t num_entries;
     // hop 1: dense roots
@@ -127,6 +128,29 @@ __device__ __forceinline__ HeldRun<G> load_run(const float *__restrict__ tsa, ui
     return r;
 }
 
+// The run [a, b), b - a <= TGL_NODE_INLINE, held from the inline timestamps
+// of its node record rec (16-byte words 1..7): position a + i is inline
+// timestamp i, so the stretch starts at a and count_in applies unchanged.
+template <int G>
+__device__ __forceinline__ HeldRun<G> load_inline(const int4 *__restrict__ rec, uint32_t a, int gl) {
+    constexpr int kWords = TGL_NODE_INLINE / 4;
+    static_assert(HeldRun<G>::H * G >= TGL_NODE_INLINE, "held stretch covers the inline timestamps");
+    HeldRun<G> r;
+    r.p0 = a + HeldRun<G>::H * static_cast<uint32_t>(gl);
+    const float inf = __builtin_inff();
+#pragma unroll
+    for (int m = 0; m < HeldRun<G>::NV; m++) {
+        const int q = HeldRun<G>::NV * gl + m;
+        if (q < kWords) {
+            const int4 w = rec[1 + q];
+            r.v[m] = make_float4(__int_as_float(w.x), __int_as_float(w.y), __int_as_float(w.z), __int_as_float(w.w));
+        } else {
+            r.v[m] = make_float4(inf, inf, inf, inf);
+        }
+    }
+    return r;
+}
+
 // Sum over the G lanes of the calling lane's group.
 template <int G>
 __device__ __forceinline__ int group_sum(int c) {
@@ -198,20 +222,23 @@ __device__ __forceinline__ void search_n(const float *__restrict__ arr, uint32_t
 
 // Positions below NE thresholds in the time-sorted run [lo0, hi0) of the
 // timestamp array (M entries): out[i] = lo0 + #{p in [lo0, hi0): ts[p] < v[i]}
-// for each i with act[i] (out[i] = lo0 otherwise).  A run of at most one held
-// stretch is loaded once and serves every threshold.  A run long enough to
+// for each i with act[i] (out[i] = lo0 otherwise).  rec, when not null, is the
+// record of a node whose whole run (lo0 onwards) is inline in it: the run is
+// then read from there.  A run of at most one held stretch is loaded once and
+// serves every threshold.  A run long enough to
 // need more than one probe round is first narrowed on the search index tsx
 // (nx samples, tsx[j] = ts[j * TGL_INDEX_STRIDE]) when there is one: with r
 // the samples inside the run below v[i], the answer lies after sample r - 1
 // and at or before sample r, fewer than TGL_INDEX_STRIDE timestamps.
 template <int G, int NE>
 __device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uint32_t M,
-                                              const float *__restrict__ tsx, uint32_t nx, uint32_t lo0,
-                                              uint32_t hi0, const float (&v)[NE], const bool (&act)[NE],
-                                              uint32_t (&out)[NE], int gl) {
+                                              const float *__restrict__ tsx, uint32_t nx,
+                                              const int4 *__restrict__ rec, uint32_t lo0, uint32_t hi0,
+                                              const float (&v)[NE], const bool (&act)[NE], uint32_t (&out)[NE],
+                                              int gl) {
     constexpr uint32_t X = TGL_INDEX_STRIDE;
-    if (hi0 - lo0 <= HeldRun<G>::span) {           // group-uniform: one load serves every bound
-        const HeldRun<G> r = load_run<G>(tsa, lo0, hi0, M, gl);
+    if (rec || hi0 - lo0 <= HeldRun<G>::span) {    // group-uniform: one load serves every bound
+        const HeldRun<G> r = rec ? load_inline<G>(rec, lo0, gl) : load_run<G>(tsa, lo0, hi0, M, gl);
 #pragma unroll
         for (int i = 0; i < NE; i++) out[i] = act[i] ? count_in<G>(r, lo0, hi0, v[i]) : lo0;
         return;
@@ -283,7 +310,7 @@ struct NodeRun {
 __device__ __forceinline__ NodeRun node_run(const HopArgs &p, int32_t x, bool valid) {
     NodeRun r{0u, 0u, __builtin_inff(), -__builtin_inff()};
     if (valid && x >= 0 && x < p.num_nodes) {
-        const int4 nd = p.nodes[x];
+        const int4 nd = p.nodes[static_cast<int64_t>(x) * 8];
         const uint32_t M = static_cast<uint32_t>(p.num_entries);
         uint32_t a = static_cast<uint32_t>(nd.x);
         uint32_t b = static_cast<uint32_t>(nd.y);
@@ -354,7 +381,7 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, uint32_t
             act[u] = i0 + u <= W && !edge_from_summary(a, b, first, last, v[u], c[u]);
         }
         uint32_t cs[NE];
-        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, a, top, v, act, cs, gl);
+        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, nullptr, a, top, v, act, cs, gl);
 #pragma unroll
         for (int u = 0; u < NE; u++) {
             if (i0 + u <= W) {
@@ -470,22 +497,27 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
 
 // Window [lo, hi) of a root with run [a, b) at time t in window s0 (one
 // window per root), by the G lanes of its group.  An edge that the run's
-// first and last timestamps decide is not searched.
-template <int G>
-__device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint32_t b, float first, float last,
-                                              float t, int32_t s0, int gl, uint32_t &lo, uint32_t &hi) {
+// first and last timestamps decide is not searched.  NB is the number of
+// window edges: 1 when windows are unbounded below (lo = a), else 2.
+template <int G, int NB>
+__device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint32_t a, uint32_t b, float first,
+                                              float last, float t, int32_t s0, int gl, uint32_t &lo, uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
-    const float vh = bound_value(t, s0, p.delta);
-    const float vl = p.delta_inf ? 0.0f : bound_value(t, s0 + 1, p.delta);
-    uint32_t ch = a, cl = a;
-    const bool kh = edge_from_summary(a, b, first, last, vh, ch);
-    const bool kl = p.delta_inf || edge_from_summary(a, b, first, last, vl, cl);
-    const float v[2] = {vh, vl};
-    const bool act[2] = {!kh, !kl};
-    uint32_t c[2];
-    count_below_n<G, 2>(p.tsa, M, p.tsx, p.nx, a, b, v, act, c, gl);
-    hi = kh ? ch : c[0];
-    lo = kl ? cl : c[1];
+    // a non-empty run belongs to a node inside the graph
+    const int4 *rec = b > a && b - a <= TGL_NODE_INLINE ? p.nodes + static_cast<int64_t>(x) * 8 : nullptr;
+    float v[NB];
+    bool act[NB];
+    uint32_t c[NB];
+#pragma unroll
+    for (int i = 0; i < NB; i++) {
+        v[i] = bound_value(t, s0 + i, p.delta);
+        c[i] = a;
+        act[i] = !edge_from_summary(a, b, first, last, v[i], c[i]);
+    }
+    uint32_t cs[NB];
+    count_below_n<G, NB>(p.tsa, M, p.tsx, p.nx, rec, a, b, v, act, cs, gl);
+    hi = act[0] ? cs[0] : c[0];
+    lo = NB == 1 ? a : (act[NB - 1] ? cs[NB - 1] : c[NB - 1]);
     if (lo > hi) lo = hi;
 }
 
@@ -500,8 +532,8 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, uint32_t a, uint
 //   phase 3, one lane per slot: selection, gather and emit.  The packed roots
 //     have consecutive indices, so the slots of a chunk are one contiguous
 //     range of the output and the stores coalesce.
-template <int G, int MODE, bool LAST, bool FIRST>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) void hop_single_kernel(const HopArgs p) {
+template <int G, int MODE, bool LAST, bool FIRST, int NB>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 7 : 6))) void hop_single_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots located per wavefront round
     constexpr int U = 4;                      // slots per lane whose loads are in flight together
     const int lane = lane_id();
@@ -516,6 +548,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
     __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
     __shared__ float r_t[kWavesPerBlock][kWave];
     __shared__ int32_t r_s[kWavesPerBlock][kWave];
+    __shared__ int32_t r_x[kWavesPerBlock][kWave];     // node of each packed root
     __shared__ uint8_t r_need[kWavesPerBlock][kWave];  // packed roots whose window needs a search
 
     const int64_t pk = FIRST ? 1 : p.p_k;
@@ -579,7 +612,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
         bool need = false;
         if (valid) {
             need = !edge_from_summary(run.a, run.b, run.first, run.last, bound_value(t, s, p.delta), hi);
-            if (!p.delta_inf)
+            if constexpr (NB == 2)
                 need |= !edge_from_summary(run.a, run.b, run.first, run.last, bound_value(t, s + 1, p.delta), lo);
             if (lo > hi) lo = hi;
         }
@@ -595,6 +628,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
             r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
             r_t[w][r] = t;
             r_s[w][r] = s;
+            r_x[w][r] = x;
             if (need) r_need[w][rank_below(need_mask)] = static_cast<uint8_t>(r);
             if (!need && p.o_cnt) {
                 const uint32_t n = hi - lo;
@@ -611,8 +645,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(7))) voi
             if (base + gw < nneed) {                // group-uniform
                 const int i = r_need[w][base + gw];
                 uint32_t wlo, whi;
-                locate_window<G>(p, r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_t[w][i], r_s[w][i], gl,
-                                 wlo, whi);
+                locate_window<G, NB>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_t[w][i], r_s[w][i],
+                                 gl, wlo, whi);
                 if (gl == 0) {
                     r_lo[w][i] = wlo;
                     r_n[w][i] = whi - wlo;
@@ -680,9 +714,15 @@ void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t w
             default: hop_multi_kernel<64, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
         }
     } else {
-        // the window search uses 8 lanes per root whatever the fanout
-        if (first) hop_single_kernel<8, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a);
-        else hop_single_kernel<8, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a);
+        // the window search uses 8 lanes per root whatever the fanout; one
+        // window edge when windows are unbounded below, else two
+        if (a.delta_inf) {
+            if (first) hop_single_kernel<8, MODE, LAST, true, 1><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 1><<<nb, kBlock, 0, st>>>(a);
+        } else {
+            if (first) hop_single_kernel<8, MODE, LAST, true, 2><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 2><<<nb, kBlock, 0, st>>>(a);
+        }
     }
 }
 
@@ -803,7 +843,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     if (g->num_entries < 0 || g->num_entries > static_cast<int64_t>(UINT32_MAX)) return TGL_EINVAL;
     if (!g->indptr || (g->num_entries > 0 && !g->entries)) return TGL_EINVAL;
     if (g->num_entries > 0 && !g->ts) return TGL_EINVAL;
-    if (!g->nodes || (reinterpret_cast<uintptr_t>(g->nodes) & 15u) != 0) return TGL_EINVAL;
+    if (!g->nodes || (reinterpret_cast<uintptr_t>(g->nodes) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts_index) & 15u) != 0) return TGL_EINVAL;

@@ -48,6 +48,12 @@ def tcsr_to_host(g):
     last = np.where(nonempty, ts[np.maximum(ip[1:] - 1, 0)] if len(ts) else -np.inf, -np.inf).astype(np.float32)
     assert np.array_equal(nodes[:, 2].view(np.float32).view(np.uint32), first.view(np.uint32)), "node summary first ts"
     assert np.array_equal(nodes[:, 3].view(np.float32).view(np.uint32), last.view(np.uint32)), "node summary last ts"
+    assert nodes.shape[1] == 32
+    for i in range(28):                     # inline timestamps of each run's first 28 entries
+        has = ip[:-1] + i < ip[1:]
+        want = np.full(len(has), np.inf, np.float32)
+        want[has] = ts[ip[:-1][has] + i]
+        assert np.array_equal(nodes[:, 4 + i].view(np.uint32), want.view(np.uint32)), "inline ts %d" % i
     if g.ts_index is not None:
         tsx = g.ts_index.cpu().numpy()
         assert np.array_equal(tsx.view(np.uint32), ts[::32].view(np.uint32)), "search index"

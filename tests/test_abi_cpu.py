@@ -94,6 +94,7 @@ def _sample_call(**kw):
     dict(g=B.c_tcsr(10, 100, FAKE, None, FAKE, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE + 8, FAKE, FAKE)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, None, FAKE)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE + 4, FAKE)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, None)), dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE + 8)),
+    dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE + 64)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE, FAKE + 4)),
     dict(g=B.c_tcsr(10, 2**32, FAKE, FAKE, FAKE, FAKE)),
     dict(g=B.c_tcsr(2**31, 100, FAKE, FAKE, FAKE, FAKE)), dict(g=None), dict(counts=None),
@@ -132,7 +133,7 @@ def _build_call(**kw):
     (dict(ts=None), B.EINVAL), (dict(ent=None), B.EINVAL), (dict(indptr=None), B.EINVAL),
     (dict(ent=FAKE + 4), B.EINVAL), (dict(m=2**31), B.EINVAL),
     (dict(ts_out=None), B.EINVAL), (dict(ts_out=FAKE + 8), B.EINVAL),
-    (dict(nodes=None), B.EINVAL), (dict(nodes=FAKE + 4), B.EINVAL), (dict(tsx=FAKE + 8), B.EINVAL),
+    (dict(nodes=None), B.EINVAL), (dict(nodes=FAKE + 4), B.EINVAL), (dict(nodes=FAKE + 64), B.EINVAL), (dict(tsx=FAKE + 8), B.EINVAL),
     (dict(ws_bytes=8), B.ENOSPACE), (dict(ws=None), B.ENOSPACE),
 ])
 def test_build_rejects_invalid_arguments(kw, want):
@@ -143,7 +144,7 @@ def test_nodes_rejects_invalid_arguments():
     L = P.lib()
     for args in [(FAKE, FAKE, 0, 10, FAKE), (FAKE, FAKE, 2**31, 10, FAKE), (FAKE, FAKE, 5, -1, FAKE),
                  (FAKE, FAKE, 5, 2**32, FAKE), (None, FAKE, 5, 10, FAKE), (FAKE, None, 5, 10, FAKE),
-                 (FAKE, FAKE, 5, 10, None), (FAKE, FAKE, 5, 10, FAKE + 4)]:
+                 (FAKE, FAKE, 5, 10, None), (FAKE, FAKE, 5, 10, FAKE + 4), (FAKE, FAKE, 5, 10, FAKE + 64)]:
         assert L.tgl_tcsr_nodes(*args, None, None) == B.EINVAL, args
     assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, FAKE + 4, None) == B.EINVAL
 

@@ -58,6 +58,11 @@ def build_on_gpu(torch, w):
     return g
 
 
+def torch_mod():
+    import torch
+    return torch
+
+
 def check_runs(g, og, nodes):
     """GPU runs of ``nodes`` equal the oracle's runs bit for bit."""
     ip = g.indptr.cpu().numpy()
@@ -70,6 +75,20 @@ def check_runs(g, og, nodes):
         assert np.array_equal(w4[:, 0], og.nbr[c:d]), "nbr of node %d" % x
         assert np.array_equal(ent[:, 1], og.eid[c:d]), "eid of node %d" % x
         assert same_bits(w4[:, 1].copy().view(np.float32), og.ts[c:d]), "ts of node %d" % x
+        rec = g.nodes[x].cpu().numpy()
+        bounds = rec[:2].view(np.uint32)
+        assert bounds[0] == a and bounds[1] == b, "node record bounds of node %d" % x
+        inl = np.full(28, np.inf, np.float32)
+        inl[:min(28, d - c)] = og.ts[c:c + min(28, d - c)]
+        first = og.ts[c] if d > c else np.float32(np.inf)
+        last = og.ts[d - 1] if d > c else np.float32(-np.inf)
+        assert same_bits(rec[2:4].copy().view(np.float32), np.array([first, last], np.float32)), \
+            "node record first/last of node %d" % x
+        assert same_bits(rec[4:].copy().view(np.float32), inl), "node record inline ts of node %d" % x
+    if g.ts_index is not None and g.num_entries:
+        j = np.unique(np.random.default_rng(5).integers(0, g.ts_index.numel(), 4096))
+        jt = torch_mod().from_numpy(j).to(g.ts.device)
+        assert same_bits(g.ts_index[jt].cpu().numpy(), g.ts[jt * 32].cpu().numpy()), "search index"
 
 
 def gpu_step(torch, g, w, b0, B):

@@ -190,13 +190,14 @@ def test_degenerate_cases(torch):
 
 
 def test_long_runs_and_off_grid_window_edges(torch):
-    """Runs whose lengths straddle the held-stretch sizes of the 8-, 16-, 32- and
-    64-lane searches (61/62, 125/126, 253/254) plus long runs, timestamps on a
+    """Runs whose lengths straddle the inline timestamps of a node record (27-29)
+    and the held-stretch sizes of the 8-, 16-, 32- and 64-lane searches (61/62,
+    125/126, 253/254) plus long runs, timestamps on a
     1/16 grid near 1e6 with ties, and window lengths (0.1, 0.37) whose edges
     t - i*delta fall between adjacent float32 values; 1..64 snapshots, so the
     edges of a root are located in batches with ragged last batches."""
     rng = np.random.default_rng(77)
-    lens = [200_000, 61, 62, 125, 126, 253, 254, 5_000, 1]
+    lens = [200_000, 61, 62, 125, 126, 253, 254, 5_000, 1, 27, 28, 29, 4]
     N = len(lens) + 1                     # the last node has no entries
     src = np.concatenate([np.full(L, x, np.int32) for x, L in enumerate(lens)])
     dst = rng.integers(0, N, len(src)).astype(np.int32)
