@@ -260,6 +260,54 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
                       void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Feature / state gather for sampled slots (Figure 2, steps 2 and 3)       */
+/* ------------------------------------------------------------------------ */
+
+#define TGL_KEY_NODE   0   /* rows indexed by the slot's neighbour id (nbr)   */
+#define TGL_KEY_EDGE   1   /* rows indexed by the slot's edge id (eid)        */
+#define TGL_MAX_TABLES 8
+#define TGL_MAX_ROW_BYTES 65536
+
+/*
+ * One table of fixed-size rows (node features, node memory, mailbox, edge
+ * features, ...) and the output it is gathered into.
+ *   rows       [device] num_rows x row_bytes, 16-byte aligned
+ *   out        [device] n x row_bytes (n of tgl_gather), 16-byte aligned
+ *   num_rows   >= 0
+ *   row_bytes  multiple of 16 in [16, TGL_MAX_ROW_BYTES]; any element type
+ *   key        TGL_KEY_NODE or TGL_KEY_EDGE
+ */
+typedef struct tgl_table {
+    const void *rows;
+    void *out;
+    int64_t num_rows;
+    int32_t row_bytes;
+    int32_t key;
+} tgl_table;
+
+/*
+ * For every slot i < n and every table T: T.out[i] = T.rows[key_i], where
+ * key_i is nbr[i] (TGL_KEY_NODE) or eid[i] (TGL_KEY_EDGE); a key outside
+ * [0, T.num_rows) -- PAD slots carry -1 -- gives a row of zero bytes.  This
+ * is the lookup of node features, memory, mailbox and edge features for the
+ * nodes and edges of a sampled mini-batch (Figure 2, steps 2-3; Section 3).
+ * All tables are served by one launch.
+ *   nbr        [device] int32[n], or NULL if no table is keyed by node
+ *   eid        [device] int64[n], or NULL if no table is keyed by edge
+ *   n          slots, >= 0
+ *   count      [device] int64 or NULL: when given, only slots
+ *              i < min(n, count[0] * per_count) are gathered and the rest of
+ *              every output is left untouched (the valid prefix of a hop's
+ *              output, whose root count tgl_sample leaves on the device)
+ *   per_count  >= 1, slots per counted root
+ *   tables     [host] tgl_table[num_tables], num_tables in [1, TGL_MAX_TABLES]
+ * Outputs must not overlap the inputs.  Never synchronises.  Errors:
+ * TGL_EINVAL for a bad argument, TGL_EDEVICE if the launch fails.
+ */
+tgl_status tgl_gather(const int32_t *nbr, const int64_t *eid, int64_t n, const int64_t *count,
+                      int64_t per_count, const tgl_table *tables, int32_t num_tables, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timers (instrumentation for benchmarks)                           */
 /* ------------------------------------------------------------------------ */
 
@@ -267,7 +315,8 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
 #define TGL_TIMER_HOPN    1  /* sampling kernel of hops >= 2                  */
 #define TGL_TIMER_COMPACT 2  /* next-hop root compaction (scan + emit)         */
 #define TGL_TIMER_BUILD   3  /* whole tgl_tcsr_build                          */
-#define TGL_TIMER_KINDS   4
+#define TGL_TIMER_GATHER  4  /* tgl_gather                                    */
+#define TGL_TIMER_KINDS   5
 
 /*
  * Starts recording HIP events around every kernel of the kinds above, on the

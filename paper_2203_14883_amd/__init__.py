@@ -1,8 +1,9 @@
 """MI355X-native hot path of TGL (Zhou et al., VLDB 2022): T-CSR build and
-multi-hop temporal neighbour sampling as hand-written HIP kernels behind the C
+multi-hop temporal neighbour sampling, and the feature / state lookup of the
+sampled slots, as hand-written HIP kernels behind the C
 ABI of include/tgl.h.  ``binding`` marshals torch tensors into that ABI;
 ``workloads`` draws the seeded synthetic graphs and root streams."""
 from .binding import (TCSR, Hop, Sampler, TglError, lib, sample, sample_capacity,  # noqa: F401
                       status_str, tcsr_build, tcsr_build_workspace, tcsr_from_host,
                       pack_entries, timer_enable, timer_disable, timer_read, timer_reset,
-                      EXPORTS, LIB_PATH, MOST_RECENT, UNIFORM)
+                      gather, EXPORTS, LIB_PATH, MOST_RECENT, UNIFORM, KEY_NODE, KEY_EDGE)

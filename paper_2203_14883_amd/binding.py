@@ -22,7 +22,9 @@ OK, EINVAL, ERANGE, ENOSPACE, EDEVICE = 0, -1, -2, -3, -4
 MOST_RECENT, UNIFORM = 0, 1
 BUILD_UNDIRECTED = 1
 MAX_HOPS, MAX_FANOUT, MAX_SNAPSHOTS = 8, 1024, 64
-TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD = 0, 1, 2, 3
+TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD, TIMER_GATHER = 0, 1, 2, 3, 4
+KEY_NODE, KEY_EDGE = 0, 1
+MAX_TABLES = 8
 
 NODE_WORDS = 32     # int32 words of one node record (128 bytes)
 NODE_INLINE = 28    # timestamps held inline in a node record
@@ -33,7 +35,8 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
-           "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample", "tgl_timer_enable",
+           "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
+           "tgl_gather", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
 
@@ -47,6 +50,11 @@ class c_tcsr(C.Structure):
     _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
                 ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p),
                 ("nodes", C.c_void_p), ("ts_index", C.c_void_p)]
+
+
+class c_table(C.Structure):
+    _fields_ = [("rows", C.c_void_p), ("out", C.c_void_p), ("num_rows", C.c_int64),
+                ("row_bytes", C.c_int32), ("key", C.c_int32)]
 
 
 class c_hop_out(C.Structure):
@@ -86,6 +94,8 @@ def lib() -> C.CDLL:
     L.tgl_sample.restype = i32
     L.tgl_sample.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
                              C.POINTER(c_hop_out), P, P, C.c_size_t, P]
+    L.tgl_gather.restype = i32
+    L.tgl_gather.argtypes = [P, P, i64, P, i64, C.POINTER(c_table), i32, P]
     L.tgl_timer_enable.restype = i32
     L.tgl_timer_enable.argtypes = [i32]
     L.tgl_timer_disable.restype = i32
@@ -330,6 +340,55 @@ def sample(g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, fanouts: Sequenc
     smp = Sampler(max(int(roots.shape[0]), 0), fanouts, snapshots, device=roots.device)
     smp.run(g, roots, root_ts, mode, snapshot_len, seed, root_base, stream)
     return smp.hops()
+
+
+# --------------------------------------------------------------------------
+# feature / state gather
+# --------------------------------------------------------------------------
+
+KEYS = {"node": KEY_NODE, "edge": KEY_EDGE, KEY_NODE: KEY_NODE, KEY_EDGE: KEY_EDGE}
+
+
+def _row_bytes(t: torch.Tensor) -> int:
+    if t.dim() < 1 or not t.is_contiguous():
+        raise ValueError("a table must be a contiguous tensor of rows")
+    return int(t[0].numel() * t.element_size()) if t.shape[0] else int(
+        math.prod(t.shape[1:]) * t.element_size())
+
+
+def gather(nbr: Optional[torch.Tensor], eid: Optional[torch.Tensor], tables, n: Optional[int] = None,
+           count: Optional[torch.Tensor] = None, per_count: int = 1, outs=None, stream=None):
+    """Looks up one row per slot in each table (Fig. 2, steps 2-3).
+
+    ``tables`` is a list of ``(rows, key)`` with ``rows`` a contiguous
+    ``[num_rows, ...]`` tensor (row size a multiple of 16 bytes) and ``key``
+    ``"node"`` (rows indexed by ``nbr``) or ``"edge"`` (by ``eid``).  Slot i of
+    the output of a table is ``rows[key_i]``, or zeros when the key is outside
+    ``[0, num_rows)`` (PAD slots carry -1).  With ``count`` (a device int64
+    tensor) only slots ``i < min(n, count[0] * per_count)`` are written.
+    Returns the outputs (allocated here unless ``outs`` is given)."""
+    if n is None:
+        ref = nbr if nbr is not None else eid
+        n = int(ref.shape[0])
+    if nbr is not None and (nbr.dtype != torch.int32 or not nbr.is_contiguous()):
+        raise ValueError("nbr must be a contiguous int32 tensor")
+    if eid is not None and (eid.dtype != torch.int64 or not eid.is_contiguous()):
+        raise ValueError("eid must be a contiguous int64 tensor")
+    if count is not None and (count.dtype != torch.int64 or count.device.type != "cuda"):
+        raise ValueError("count must be a device int64 tensor")
+    tabs = (c_table * max(len(tables), 1))()
+    result = []
+    for i, (rows, key) in enumerate(tables):
+        rb = _row_bytes(rows)
+        out = outs[i] if outs is not None else torch.empty((n,) + tuple(rows.shape[1:]), dtype=rows.dtype,
+                                                            device=rows.device)
+        tabs[i] = c_table(rows.data_ptr() if rows.numel() else None, out.data_ptr() if n else None,
+                          int(rows.shape[0]), rb, KEYS[key])
+        result.append(out)
+    s = lib().tgl_gather(_p(nbr), _p(eid), int(n), _p(count), int(per_count), tabs, len(tables),
+                         _stream(stream))
+    _check(s, "tgl_gather")
+    return result
 
 
 # --------------------------------------------------------------------------

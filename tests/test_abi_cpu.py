@@ -158,8 +158,34 @@ def test_index_len():
 def test_timer_argument_checks():
     L = P.lib()
     ms, n = C.c_double(), C.c_int64()
-    assert L.tgl_timer_read(4, C.byref(ms), C.byref(n)) == B.EINVAL
+    assert L.tgl_timer_read(5, C.byref(ms), C.byref(n)) == B.EINVAL
     assert L.tgl_timer_read(-1, C.byref(ms), C.byref(n)) == B.EINVAL
     assert L.tgl_timer_read(0, None, C.byref(n)) == B.EINVAL
     assert L.tgl_timer_enable(0) == B.EINVAL
     assert L.tgl_timer_read(0, C.byref(ms), C.byref(n)) == 0 and n.value == 0
+
+
+def _gather_call(n=10, per=1, nt=1, nbr=FAKE, eid=FAKE, count=None, **tab):
+    L = P.lib()
+    t = dict(rows=FAKE, out=FAKE, num_rows=100, row_bytes=64, key=B.KEY_NODE)
+    t.update(tab)
+    tabs = (B.c_table * max(nt, 1))(*[B.c_table(t["rows"], t["out"], t["num_rows"], t["row_bytes"], t["key"])
+                                      for _ in range(max(nt, 1))])
+    return L.tgl_gather(nbr, eid, n, count, per, tabs, nt, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(n=-1), dict(per=0), dict(nt=0), dict(nt=9), dict(row_bytes=8), dict(row_bytes=24),
+    dict(row_bytes=65552), dict(row_bytes=0), dict(key=2), dict(num_rows=-1), dict(out=None),
+    dict(rows=None), dict(rows=FAKE + 8), dict(out=FAKE + 4), dict(nbr=None), dict(key=B.KEY_EDGE, eid=None),
+    dict(num_rows=2**62, row_bytes=64),
+])
+def test_gather_rejects_invalid_arguments(kw):
+    assert _gather_call(**kw) == B.EINVAL
+
+
+def test_gather_empty_is_a_no_op():
+    # nothing to gather: valid arguments return OK without touching the device
+    assert _gather_call(n=0, out=None) == B.OK
+    assert _gather_call(n=0, nbr=None, out=None) == B.OK
+    assert _gather_call(n=5, rows=None, num_rows=0, nt=0) == B.EINVAL
