@@ -54,23 +54,27 @@ def parse():
                     help="first run a plain 4 GiB device copy (for scaling byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--small", action="store_true", help="reduced graph size (development only)")
+    ap.add_argument("--row", default="sample", choices=["sample", "f1"],
+                    help="sample: the sampler step (default); f1: node-feature lookup of the sampled slots")
+    ap.add_argument("--gather-steps", type=int, default=8,
+                    help="f1: sampler steps whose slots are looked up in the timed region")
     return ap.parse_args()
 
 
-def kernel_source_hash():
-    """Hash of the sources that define the sampling kernels."""
+def kernel_source_hash(files=("tgl_internal.hpp", "tgl_sample.hip")):
+    """Hash of the sources that define the measured kernels."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2203_14883_amd", "csrc")
-    for f in ("tgl_internal.hpp", "tgl_sample.hip"):
+    for f in files:
         with open(os.path.join(csrc, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel_hash, workload):
+def read_traffic(kernel_hash, workload, prefix="hop_kernel"):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "hop_kernel_%s_pmc.md" % workload)
+    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (prefix, workload))
     if not os.path.exists(path):
         return None
     vals = {}
@@ -126,6 +130,153 @@ def cpu_baseline(w, nbatches):
                 sample="%d roots (%d consecutive batches from batch %d) of %s, %d hops, %d neighbours, "
                        "%.2f s single-threaded (sampling call only; T-CSR of the reached sub-graph built beforehand)"
                        % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, dt))
+
+
+GATHER_DIM = 768             # MAG node features (Table 3), bfloat16
+GATHER_CHUNK = 1 << 20       # slots per tgl_gather launch
+GATHER_METRIC = "looked-up node-feature rows/sec (768-dim bf16) for the sampled slots + achieved HBM GB/s vs peak"
+
+
+def gather_cpu_baseline(table, keys, nslots):
+    """The lookup oracle, single-threaded, on a bounded sample: ``nslots``
+    slots drawn at random from one step, over a host copy of exactly the table
+    rows they reference (a full host copy of the table would not fit).  Only
+    the oracle's lookup is timed."""
+    import torch
+    from oracle import features as F
+    pick = np.sort(np.random.default_rng(2).choice(keys.numel(), min(nslots, keys.numel()), replace=False))
+    k = keys[torch.from_numpy(pick).to(keys.device)].cpu().numpy().astype(np.int64)
+    valid = (k >= 0) & (k < table.shape[0])
+    uniq, inv = np.unique(k[valid], return_inverse=True)
+    rows = table[torch.from_numpy(uniq).to(table.device)].view(torch.int16).cpu().numpy().view(np.uint16)
+    kc = np.full(len(k), -1, np.int64)
+    kc[valid] = inv
+    t = time.perf_counter()
+    (out,) = F.gather(kc.astype(np.int32), None, [(rows, F.NODE)])
+    dt = time.perf_counter() - t
+    return dict(value=len(k) / dt, unit="rows/s", cores=1, kind="oracle",
+                sample="%d random slots of one c4 step (%d distinct nodes, %d PAD), %d-dim bf16 rows, %.2f s "
+                       "single-threaded (lookup only; host copy of the referenced rows made beforehand)"
+                       % (len(k), len(uniq), int((~valid).sum()), table.shape[1], dt))
+
+
+def measure_gather(args, w, g, smp, run, timed_pos, B, dev):
+    """Row f1: node-feature lookup (Fig. 2, steps 2-3) of every hop-1 and hop-2
+    slot of sampler steps, GATHER_CHUNK slots per tgl_gather launch, against
+    a table of GATHER_DIM-dim bf16 rows for every node of the graph."""
+    import torch
+    import paper_2203_14883_amd as P
+    from oracle import features as F
+
+    rows = w.num_nodes
+    need = rows * GATHER_DIM * 2
+    free, _ = torch.cuda.mem_get_info(dev)
+    if need + (8 << 30) > free:
+        raise SystemExit("f1: a %.1f GB feature table does not fit (%.1f GB free)" % (need / 1e9, free / 1e9))
+    table = torch.empty((rows, GATHER_DIM), dtype=torch.bfloat16, device=dev)
+    iv = table.view(torch.int16)
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(12345)
+    for i in range(0, rows, 1 << 22):
+        iv[i:i + (1 << 22)].random_(-32768, 32767, generator=gen)   # random bits; values do not matter
+    out = torch.empty((GATHER_CHUNK, GATHER_DIM), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log("f1: node-feature table %d x %d bf16 (%.1f GB)" % (rows, GATHER_DIM, need / 1e9))
+
+    steps = timed_pos[:max(args.gather_steps, 1)]
+    slot_lists = []                     # per step: the slots' neighbour ids of every hop, concatenated
+    for b in steps:
+        run(b)
+        hs = smp.hops()
+        slot_lists.append(torch.cat([h.nbr for h in hs]))
+    torch.cuda.synchronize()
+
+    def gather_all(keys):
+        for c0 in range(0, keys.numel(), GATHER_CHUNK):
+            kc = keys[c0:c0 + GATHER_CHUNK]
+            P.gather(kc, None, [(table, "node")], outs=[out[:kc.numel()]])
+
+    gather_all(slot_lists[0])           # warm-up
+    torch.cuda.synchronize()
+    P.timer_reset()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for keys in slot_lists:
+        gather_all(keys)
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    k_ms, k_n = P.timer_read(P.binding.TIMER_GATHER)
+    nslots = sum(int(k.numel()) for k in slot_lists)
+    nvalid = sum(int(((k >= 0) & (k < rows)).sum()) for k in slot_lists)
+    rb = GATHER_DIM * 2
+    alg_bytes = nslots * (4 + rb) + nvalid * rb        # key read + row written per slot; row read when valid
+    achieved = alg_bytes / k_n / (k_ms / k_n * 1e-3) / 1e9
+    value = nslots / (total_ms * 1e-3)
+    log("f1: %d launches, %d slots (%d valid): %.2f ms total, kernel %.2f ms; %.3g rows/s; %.1f GB/s algorithmic"
+        % (k_n, nslots, nvalid, total_ms, k_ms, value, achieved))
+
+    # parity spot check of the last launch against the oracle (sampled rows)
+    last = slot_lists[-1]
+    c0 = ((last.numel() - 1) // GATHER_CHUNK) * GATHER_CHUNK
+    kc = last[c0:]
+    pick = torch.from_numpy(np.random.default_rng(1).choice(kc.numel(), min(4096, kc.numel()), replace=False)).to(dev)
+    keys = kc[pick].cpu().numpy()
+    ok = (keys >= 0) & (keys < rows)
+    uniq, inv = np.unique(keys[ok], return_inverse=True)
+    host_rows = table[torch.from_numpy(uniq.astype(np.int64)).to(dev)].view(torch.int16).cpu().numpy().view(np.uint16)
+    kk = np.full(len(keys), -1, np.int32)
+    kk[ok] = inv
+    (want,) = F.gather(kk, None, [(host_rows, F.NODE)])
+    got = out[pick].view(torch.int16).cpu().numpy().view(np.uint16)
+    if got.tobytes() != want.tobytes():
+        raise SystemExit("f1: looked-up rows differ from the oracle")
+    log("f1: %d sampled rows of the last launch equal the oracle's" % len(keys))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        del out
+        torch.cuda.empty_cache()
+        cpu = gather_cpu_baseline(table, slot_lists[len(slot_lists) // 2], 2 << 20)
+        log("f1 CPU oracle: %.3g rows/s (%s)" % (cpu["value"], cpu["sample"]))
+    khash = kernel_source_hash(("tgl_internal.hpp", "tgl_gather.hip"))
+    line = {
+        "metric": GATHER_METRIC,
+        "value": value,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": len(slot_lists),
+        "warmup": 1,
+        "ms_per_step": total_ms / len(slot_lists),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: node-feature lookup (%d-dim bf16 rows, %d nodes) of every hop-1 and hop-2 slot of %d "
+                        "sampler steps (%d-hop %s %s, %d batches of %d edges x 3 roots per step), %d slots per launch"
+                        % (w.name, GATHER_DIM, rows, len(slot_lists), len(w.fanouts), w.mode,
+                           "x".join(map(str, w.fanouts)), B, w.batch_edges, GATHER_CHUNK),
+            "slots_per_step": nslots / len(slot_lists),
+            "valid_fraction": nvalid / max(nslots, 1),
+        },
+        "roofline": {
+            "kernel": "gather_kernel",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": read_traffic(khash, w.name, "gather_kernel"),
+            "algorithmic_bytes_per_launch": alg_bytes / k_n,
+            "avg_launch_ms": k_ms / k_n,
+            "kernel_source_hash": khash,
+        },
+        "cpu_baseline": cpu,
+    }
+    P.timer_disable()
+    print(json.dumps(line), flush=True)
 
 
 def copy_calibration(dev, gib=4, reps=3):
@@ -210,6 +361,10 @@ def main():
     def run(b):
         r, t_, base, n = inputs[b]
         smp.run(g, r, t_, w.mode, w.snapshot_len, w.sample_seed, base, num_roots=n)
+
+    if args.row == "f1":
+        measure_gather(args, w, g, smp, run, timed_pos, B, dev)
+        return
 
     for b in warm_pos:
         run(b)
