@@ -308,6 +308,39 @@ tgl_status tgl_gather(const int32_t *nbr, const int64_t *eid, int64_t n, const i
                       int64_t per_count, const tgl_table *tables, int32_t num_tables, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Time encoding of sampled slots (Equation 3)                              */
+/* ------------------------------------------------------------------------ */
+
+#define TGL_OUT_F32  0     /* float32 output rows                              */
+#define TGL_OUT_BF16 1     /* bfloat16 output rows (round to nearest even)    */
+#define TGL_MAX_TIME_DIM 4096
+
+/*
+ * Time encoding of the slots' time differences (Equation 3, the time encoder
+ * of Section 2): out[i][j] = cos(omega[j] * dt[i] + phi[j]) for every slot
+ * i < n with dt[i] >= 0; a slot with dt[i] < 0 (PAD slots carry -1) gets a
+ * row of zeros.  The argument is formed in double precision (the float
+ * product omega * dt is exact there) and reduced modulo 2 pi before a float
+ * cosine, so the result is within 1e-6 of the exact value whatever the size
+ * of omega * dt (before the bfloat16 rounding, for TGL_OUT_BF16).
+ *   dt         [device] float[n] (a hop's dt output)
+ *   n          slots, >= 0
+ *   count      [device] int64 or NULL: when given, only slots
+ *              i < min(n, count[0] * per_count) are encoded and the rest of
+ *              `out` is left untouched
+ *   per_count  >= 1, slots per counted root
+ *   omega, phi [device] float[dim]
+ *   dim        in [1, TGL_MAX_TIME_DIM]
+ *   out_type   TGL_OUT_F32 or TGL_OUT_BF16
+ *   out        [device] n x dim elements of out_type, row-major, 4-byte aligned
+ * Never synchronises.  Errors: TGL_EINVAL for a bad argument, TGL_EDEVICE if
+ * the launch fails.
+ */
+tgl_status tgl_time_encode(const float *dt, int64_t n, const int64_t *count, int64_t per_count,
+                           const float *omega, const float *phi, int32_t dim, int32_t out_type,
+                           void *out, void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel timers (instrumentation for benchmarks)                           */
 /* ------------------------------------------------------------------------ */
 
@@ -316,7 +349,8 @@ tgl_status tgl_gather(const int32_t *nbr, const int64_t *eid, int64_t n, const i
 #define TGL_TIMER_COMPACT 2  /* next-hop root compaction (scan + emit)         */
 #define TGL_TIMER_BUILD   3  /* whole tgl_tcsr_build                          */
 #define TGL_TIMER_GATHER  4  /* tgl_gather                                    */
-#define TGL_TIMER_KINDS   5
+#define TGL_TIMER_TIMEENC 5  /* tgl_time_encode                               */
+#define TGL_TIMER_KINDS   6
 
 /*
  * Starts recording HIP events around every kernel of the kinds above, on the

@@ -1,4 +1,5 @@
-"""Oracle for the lookup of per-node and per-edge rows of sampled slots.
+"""Oracle for what the sampled slots feed: the lookup of per-node and
+per-edge rows, and the time encoding of the slots' time differences.
 
 TEST INFRASTRUCTURE ONLY: tests, the smoke check and the benchmark's CPU
 baseline leg may use this module; the product library never does.  It shares
@@ -11,6 +12,9 @@ lookup has a plain definition: output row i of a table is the table's row
 ``key_i``, where ``key_i`` is the slot's neighbour id or edge id.  A padded
 slot (key -1) has no node or edge; it gets a row of zeros, as does any key
 outside the table.
+
+Equation 3 (the time encoder of Section 2) maps a time difference dt to
+cos(omega * dt + phi); ``time_encode`` evaluates it per slot in float64.
 """
 from __future__ import annotations
 
@@ -50,3 +54,19 @@ def gather_loop(nbr, eid, tables, limit=None):
             out.append(rows[k].copy() if 0 <= k < rows.shape[0] else np.zeros(rows.shape[1:], rows.dtype))
         outs.append(np.array(out, dtype=rows.dtype).reshape((n,) + rows.shape[1:]))
     return outs
+
+
+def time_encode(dt: np.ndarray, omega: np.ndarray, phi: np.ndarray, limit: Optional[int] = None) -> np.ndarray:
+    """Equation 3 (the time encoder of Section 2): row i is
+    cos(omega * dt[i] + phi) for a slot with dt[i] >= 0 and zeros for a padded
+    slot (dt = -1), for i < limit (default: every slot).  Evaluated in float64
+    from the float32 inputs: the product of two float32 values is exact in
+    float64, so the only roundings are the sum's and the cosine's."""
+    dt = np.asarray(dt, np.float32)
+    n = len(dt) if limit is None else max(0, min(int(limit), len(dt)))
+    d = dt[:n].astype(np.float64)[:, None]
+    w = np.asarray(omega, np.float32).astype(np.float64)[None, :]
+    p = np.asarray(phi, np.float32).astype(np.float64)[None, :]
+    out = np.cos(d * w + p)
+    out[~(d[:, 0] >= 0.0)] = 0.0
+    return out

@@ -22,7 +22,8 @@ OK, EINVAL, ERANGE, ENOSPACE, EDEVICE = 0, -1, -2, -3, -4
 MOST_RECENT, UNIFORM = 0, 1
 BUILD_UNDIRECTED = 1
 MAX_HOPS, MAX_FANOUT, MAX_SNAPSHOTS = 8, 1024, 64
-TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD, TIMER_GATHER = 0, 1, 2, 3, 4
+TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD, TIMER_GATHER, TIMER_TIMEENC = 0, 1, 2, 3, 4, 5
+OUT_F32, OUT_BF16 = 0, 1
 KEY_NODE, KEY_EDGE = 0, 1
 MAX_TABLES = 8
 
@@ -36,7 +37,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
            "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
-           "tgl_gather", "tgl_timer_enable",
+           "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
 
@@ -96,6 +97,8 @@ def lib() -> C.CDLL:
                              C.POINTER(c_hop_out), P, P, C.c_size_t, P]
     L.tgl_gather.restype = i32
     L.tgl_gather.argtypes = [P, P, i64, P, i64, C.POINTER(c_table), i32, P]
+    L.tgl_time_encode.restype = i32
+    L.tgl_time_encode.argtypes = [P, i64, P, i64, P, P, i32, i32, P, P]
     L.tgl_timer_enable.restype = i32
     L.tgl_timer_enable.argtypes = [i32]
     L.tgl_timer_disable.restype = i32
@@ -389,6 +392,38 @@ def gather(nbr: Optional[torch.Tensor], eid: Optional[torch.Tensor], tables, n: 
                          _stream(stream))
     _check(s, "tgl_gather")
     return result
+
+
+# --------------------------------------------------------------------------
+# time encoding (Eq. 3)
+# --------------------------------------------------------------------------
+
+def time_encode(dt: torch.Tensor, omega: torch.Tensor, phi: torch.Tensor, out_dtype=torch.float32,
+                n: Optional[int] = None, count: Optional[torch.Tensor] = None, per_count: int = 1,
+                out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Row i = cos(omega * dt[i] + phi) for dt[i] >= 0, zeros for PAD slots
+    (dt = -1); ``[n, dim]`` float32 or bfloat16.  With ``count`` (a device
+    int64 tensor) only rows ``i < min(n, count[0] * per_count)`` are written."""
+    if dt.dtype != torch.float32 or not dt.is_contiguous():
+        raise ValueError("dt must be a contiguous float32 tensor")
+    for t in (omega, phi):
+        if t.dtype != torch.float32 or not t.is_contiguous() or t.dim() != 1:
+            raise ValueError("omega and phi must be contiguous float32 vectors")
+    if omega.numel() != phi.numel():
+        raise ValueError("omega and phi must have the same length")
+    if out_dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("out_dtype must be float32 or bfloat16")
+    if count is not None and (count.dtype != torch.int64 or count.device.type != "cuda"):
+        raise ValueError("count must be a device int64 tensor")
+    n = int(dt.shape[0]) if n is None else int(n)
+    dim = int(omega.numel())
+    if out is None:
+        out = torch.empty((n, dim), dtype=out_dtype, device=dt.device)
+    s = lib().tgl_time_encode(_p(dt), n, _p(count), int(per_count), _p(omega), _p(phi), dim,
+                              OUT_F32 if out_dtype == torch.float32 else OUT_BF16,
+                              out.data_ptr() if n else None, _stream(stream))
+    _check(s, "tgl_time_encode")
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -158,7 +158,7 @@ def test_index_len():
 def test_timer_argument_checks():
     L = P.lib()
     ms, n = C.c_double(), C.c_int64()
-    assert L.tgl_timer_read(5, C.byref(ms), C.byref(n)) == B.EINVAL
+    assert L.tgl_timer_read(6, C.byref(ms), C.byref(n)) == B.EINVAL
     assert L.tgl_timer_read(-1, C.byref(ms), C.byref(n)) == B.EINVAL
     assert L.tgl_timer_read(0, None, C.byref(n)) == B.EINVAL
     assert L.tgl_timer_enable(0) == B.EINVAL
@@ -189,3 +189,19 @@ def test_gather_empty_is_a_no_op():
     assert _gather_call(n=0, out=None) == B.OK
     assert _gather_call(n=0, nbr=None, out=None) == B.OK
     assert _gather_call(n=5, rows=None, num_rows=0, nt=0) == B.EINVAL
+
+
+def _te_call(dt=FAKE, n=10, count=None, per=1, omega=FAKE, phi=FAKE, dim=100, out_type=B.OUT_F32, out=FAKE):
+    return P.lib().tgl_time_encode(dt, n, count, per, omega, phi, dim, out_type, out, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(n=-1), dict(per=0), dict(dim=0), dict(dim=4097), dict(out_type=2), dict(omega=None), dict(phi=None),
+    dict(dt=None), dict(out=None), dict(out=FAKE + 2), dict(n=2**62, dim=4096),
+])
+def test_time_encode_rejects_invalid_arguments(kw):
+    assert _te_call(**kw) == B.EINVAL
+
+
+def test_time_encode_empty_is_a_no_op():
+    assert _te_call(n=0, dt=None, out=None) == B.OK

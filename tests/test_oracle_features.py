@@ -9,6 +9,11 @@ things other than itself:
   output for a seeded graph;
 * plausible mistakes (clamping keys, no zero rows, off-by-one bound, wrong key
   array, ignoring the limit) each fail one of these checks.
+
+and of the time encoding (Eq. 3) against closed forms (omega = 0, dt = 0,
+omega * dt a multiple of pi) and a 50-digit mpmath evaluation at Wikipedia-
+sized time differences, with its own mutants (sin for cos, phi dropped, a
+float32 argument, PAD rows encoded).
 """
 import numpy as np
 import pytest
@@ -117,3 +122,78 @@ def test_gathered_rows_of_sampled_slots():
         assert np.array_equal(ef[:, 0], np.where(pad, 0, h.eid))
         assert np.array_equal(nf[:, 3], np.where(pad, 0, h.nbr))
         assert pad.any() and (~pad).any()
+
+
+# ---------------------------------------------------------------------------
+# time encoding (Eq. 3)
+# ---------------------------------------------------------------------------
+
+def _te_pin_checks(enc):
+    """Pins of the time encoding against closed forms and an independent
+    50-digit evaluation (mpmath)."""
+    import mpmath
+    f32 = np.float32
+    # closed forms: omega = 0 gives cos(phi); dt = 0 likewise; phi = 0 and
+    # omega * dt = 0 gives 1; PAD rows are zero
+    phi = np.array([0.0, np.pi / 3, np.pi / 2, np.pi, -np.pi / 3], f32)
+    want_phi = np.array([1.0, 0.5, 0.0, -1.0, 0.5])
+    out = enc(np.array([0.0, 5.0, -1.0], f32), np.array([0.0, 0.0, 0.0, 0.0, 0.0], f32), phi)
+    if out.shape != (3, 5) or np.abs(out[0] - want_phi).max() > 1e-7 or np.abs(out[1] - want_phi).max() > 1e-7:
+        return False
+    if np.any(out[2] != 0.0):
+        return False
+    # omega = 1/1024 and dt a multiple of 1024 * pi in float: omega * dt = k * pi
+    # up to dt's float rounding, so the value is +-1 to first order
+    out = enc(np.array([f32(1024 * np.pi * 3)], f32), np.array([1.0 / 1024], f32), np.array([0.0], f32))
+    if abs(out[0, 0] + 1.0) > 1e-6:
+        return False
+    # large arguments (Wikipedia-sized dt): against mpmath at 50 digits
+    rng = np.random.default_rng(4)
+    dt = (rng.random(64) * 2.7e6).astype(f32)
+    omega = (1.0 / 10 ** np.linspace(0, 9, 16)).astype(f32)   # the TGAT-style frequency ladder
+    phi = (rng.random(16) * 6.0 - 3.0).astype(f32)
+    out = enc(dt, omega, phi)
+    mpmath.mp.dps = 50
+    for i in range(0, 64, 7):
+        for j in range(16):
+            exact = float(mpmath.cos(mpmath.mpf(float(omega[j])) * mpmath.mpf(float(dt[i])) + mpmath.mpf(float(phi[j]))))
+            if abs(out[i, j] - exact) > 1e-9:
+                return False
+    # limit
+    if enc(dt, omega, phi, 5).shape != (5, 16) or enc(dt, omega, phi, 0).shape != (0, 16):
+        return False
+    return True
+
+
+def test_time_encode_pins():
+    assert _te_pin_checks(F.time_encode)
+
+
+def _te_sin(dt, omega, phi, limit=None):
+    out = F.time_encode(dt, omega, phi, limit)
+    d = np.asarray(dt, np.float32)[:out.shape[0]].astype(np.float64)[:, None]
+    s = np.sin(d * np.asarray(omega, np.float64)[None, :] + np.asarray(phi, np.float64)[None, :])
+    return np.where(out == 0.0, 0.0, s)
+
+
+def _te_no_phi(dt, omega, phi, limit=None):
+    return F.time_encode(dt, omega, np.zeros_like(np.asarray(phi)), limit)
+
+
+def _te_float32_argument(dt, omega, phi, limit=None):
+    dt = np.asarray(dt, np.float32)
+    n = len(dt) if limit is None else max(0, min(int(limit), len(dt)))
+    a = (dt[:n, None] * np.asarray(omega, np.float32)[None, :] + np.asarray(phi, np.float32)[None, :]).astype(np.float32)
+    out = np.cos(a.astype(np.float64))
+    out[~(dt[:n] >= 0)] = 0.0
+    return out
+
+
+def _te_pad_not_zero(dt, omega, phi, limit=None):
+    dt = np.abs(np.asarray(dt, np.float32))
+    return F.time_encode(dt, omega, phi, limit)
+
+
+@pytest.mark.parametrize("mutant", [_te_sin, _te_no_phi, _te_float32_argument, _te_pad_not_zero])
+def test_time_encode_pins_catch_mutants(mutant):
+    assert not _te_pin_checks(mutant)
