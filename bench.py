@@ -54,10 +54,13 @@ def parse():
                     help="first run a plain 4 GiB device copy (for scaling byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--small", action="store_true", help="reduced graph size (development only)")
-    ap.add_argument("--row", default="sample", choices=["sample", "f1"],
-                    help="sample: the sampler step (default); f1: node-feature lookup of the sampled slots")
+    ap.add_argument("--row", default="sample", choices=["sample", "f1", "f2"],
+                    help="sample: the sampler step (default); f1: node-feature lookup of the sampled slots; "
+                         "f2: time encoding of the sampled slots")
     ap.add_argument("--gather-steps", type=int, default=8,
-                    help="f1: sampler steps whose slots are looked up in the timed region")
+                    help="f1, f2: sampler steps whose slots are processed in the timed region")
+    ap.add_argument("--chunk", type=int, default=None,
+                    help="f1, f2: slots per launch (default 2^20 for f1, 2^23 for f2)")
     return ap.parse_args()
 
 
@@ -133,7 +136,7 @@ def cpu_baseline(w, nbatches):
 
 
 GATHER_DIM = 768             # MAG node features (Table 3), bfloat16
-GATHER_CHUNK = 1 << 20       # slots per tgl_gather launch
+GATHER_CHUNK = 1 << 22       # slots per tgl_gather launch (6.4 GB of rows)
 GATHER_METRIC = "looked-up node-feature rows/sec (768-dim bf16) for the sampled slots + achieved HBM GB/s vs peak"
 
 
@@ -179,7 +182,8 @@ def measure_gather(args, w, g, smp, run, timed_pos, B, dev):
     gen.manual_seed(12345)
     for i in range(0, rows, 1 << 22):
         iv[i:i + (1 << 22)].random_(-32768, 32767, generator=gen)   # random bits; values do not matter
-    out = torch.empty((GATHER_CHUNK, GATHER_DIM), dtype=torch.bfloat16, device=dev)
+    chunk = args.chunk or GATHER_CHUNK
+    out = torch.empty((chunk, GATHER_DIM), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
     log("f1: node-feature table %d x %d bf16 (%.1f GB)" % (rows, GATHER_DIM, need / 1e9))
 
@@ -192,8 +196,8 @@ def measure_gather(args, w, g, smp, run, timed_pos, B, dev):
     torch.cuda.synchronize()
 
     def gather_all(keys):
-        for c0 in range(0, keys.numel(), GATHER_CHUNK):
-            kc = keys[c0:c0 + GATHER_CHUNK]
+        for c0 in range(0, keys.numel(), chunk):
+            kc = keys[c0:c0 + chunk]
             P.gather(kc, None, [(table, "node")], outs=[out[:kc.numel()]])
 
     gather_all(slot_lists[0])           # warm-up
@@ -218,7 +222,7 @@ def measure_gather(args, w, g, smp, run, timed_pos, B, dev):
 
     # parity spot check of the last launch against the oracle (sampled rows)
     last = slot_lists[-1]
-    c0 = ((last.numel() - 1) // GATHER_CHUNK) * GATHER_CHUNK
+    c0 = ((last.numel() - 1) // chunk) * chunk
     kc = last[c0:]
     pick = torch.from_numpy(np.random.default_rng(1).choice(kc.numel(), min(4096, kc.numel()), replace=False)).to(dev)
     keys = kc[pick].cpu().numpy()
@@ -257,7 +261,7 @@ def measure_gather(args, w, g, smp, run, timed_pos, B, dev):
             "workload": "%s: node-feature lookup (%d-dim bf16 rows, %d nodes) of every hop-1 and hop-2 slot of %d "
                         "sampler steps (%d-hop %s %s, %d batches of %d edges x 3 roots per step), %d slots per launch"
                         % (w.name, GATHER_DIM, rows, len(slot_lists), len(w.fanouts), w.mode,
-                           "x".join(map(str, w.fanouts)), B, w.batch_edges, GATHER_CHUNK),
+                           "x".join(map(str, w.fanouts)), B, w.batch_edges, chunk),
             "slots_per_step": nslots / len(slot_lists),
             "valid_fraction": nvalid / max(nslots, 1),
         },
@@ -269,6 +273,120 @@ def measure_gather(args, w, g, smp, run, timed_pos, B, dev):
             "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBS,
             "traffic": read_traffic(khash, w.name, "gather_kernel"),
+            "algorithmic_bytes_per_launch": alg_bytes / k_n,
+            "avg_launch_ms": k_ms / k_n,
+            "kernel_source_hash": khash,
+        },
+        "cpu_baseline": cpu,
+    }
+    P.timer_disable()
+    print(json.dumps(line), flush=True)
+
+
+TIME_DIM = 100               # time-encoding width (TGL's default)
+TIME_CHUNK = 1 << 23          # slots per tgl_time_encode launch (3.2 GB of float32 rows)
+TIME_METRIC = "time-encoded slots/sec (100-dim float32, Eq. 3) for the sampled slots + achieved HBM GB/s vs peak"
+
+
+def measure_timeenc(args, w, smp, run, timed_pos, B, dev):
+    """Row f2: time encoding (Eq. 3) of the dt of every hop-1 and hop-2 slot
+    of sampler steps, TIME_CHUNK slots per tgl_time_encode launch, float32
+    rows of TIME_DIM elements, TGAT-style frequencies omega_j = 10^(-9j/(d-1))."""
+    import torch
+    import paper_2203_14883_amd as P
+    from oracle import features as F
+
+    omega_h = (1.0 / 10 ** np.linspace(0, 9, TIME_DIM)).astype(np.float32)
+    phi_h = (np.random.default_rng(7).random(TIME_DIM) * 6.0 - 3.0).astype(np.float32)
+    omega, phi = torch.from_numpy(omega_h).to(dev), torch.from_numpy(phi_h).to(dev)
+    chunk = args.chunk or TIME_CHUNK
+    out = torch.empty((chunk, TIME_DIM), dtype=torch.float32, device=dev)
+    steps = timed_pos[:max(args.gather_steps, 1)]
+    dts = []
+    for b in steps:
+        run(b)
+        dts.append(torch.cat([h.dt for h in smp.hops()]))
+    torch.cuda.synchronize()
+
+    def encode_all(d):
+        for c0 in range(0, d.numel(), chunk):
+            dc = d[c0:c0 + chunk]
+            P.time_encode(dc, omega, phi, out=out[:dc.numel()])
+
+    encode_all(dts[0])                  # warm-up
+    torch.cuda.synchronize()
+    P.timer_reset()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for d in dts:
+        encode_all(d)
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    k_ms, k_n = P.timer_read(P.binding.TIMER_TIMEENC)
+    nslots = sum(int(d.numel()) for d in dts)
+    nvalid = sum(int((d >= 0).sum()) for d in dts)
+    alg_bytes = nslots * (4 + TIME_DIM * 4)          # dt read, row written
+    achieved = alg_bytes / k_n / (k_ms / k_n * 1e-3) / 1e9
+    value = nslots / (total_ms * 1e-3)
+    log("f2: %d launches, %d slots (%d valid): %.2f ms total, kernel %.2f ms; %.3g slots/s; %.1f GB/s algorithmic"
+        % (k_n, nslots, nvalid, total_ms, k_ms, value, achieved))
+
+    # spot check of the last launch against the oracle (sampled rows, derived tolerance)
+    last = dts[-1]
+    c0 = ((last.numel() - 1) // chunk) * chunk
+    dc = last[c0:]
+    pick = np.random.default_rng(1).choice(dc.numel(), min(4096, dc.numel()), replace=False)
+    pk = torch.from_numpy(pick).to(dev)
+    want = F.time_encode(dc[pk].cpu().numpy(), omega_h, phi_h)
+    got = out[pk].cpu().numpy().astype(np.float64)
+    err = float(np.abs(got - want).max()) if want.size else 0.0
+    if not err <= 1e-6:
+        raise SystemExit("f2: encodings differ from the oracle by %.3g" % err)
+    log("f2: %d sampled rows of the last launch within %.2g of the oracle" % (len(pick), err))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        d = dts[len(dts) // 2]
+        pick = np.sort(np.random.default_rng(2).choice(d.numel(), min(1 << 20, d.numel()), replace=False))
+        dh = d[torch.from_numpy(pick).to(dev)].cpu().numpy()
+        t = time.perf_counter()
+        F.time_encode(dh, omega_h, phi_h)
+        dt_ = time.perf_counter() - t
+        cpu = dict(value=len(dh) / dt_, unit="slots/s", cores=1, kind="oracle",
+                   sample="%d random slots of one c4 step, %d-dim rows, %.2f s single-threaded (numpy float64)"
+                          % (len(dh), TIME_DIM, dt_))
+        log("f2 CPU oracle: %.3g slots/s (%s)" % (cpu["value"], cpu["sample"]))
+    khash = kernel_source_hash(("tgl_internal.hpp", "tgl_timeenc.hip"))
+    line = {
+        "metric": TIME_METRIC,
+        "value": value,
+        "unit": "slots/s",
+        "n_gpus": 1,
+        "steps": len(dts),
+        "warmup": 1,
+        "ms_per_step": total_ms / len(dts),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: time encoding (%d-dim float32 rows) of every hop-1 and hop-2 slot of %d sampler steps "
+                        "(%d-hop %s %s, %d batches of %d edges x 3 roots per step), %d slots per launch"
+                        % (w.name, TIME_DIM, len(dts), len(w.fanouts), w.mode, "x".join(map(str, w.fanouts)),
+                           B, w.batch_edges, chunk),
+            "slots_per_step": nslots / len(dts),
+            "valid_fraction": nvalid / max(nslots, 1),
+        },
+        "roofline": {
+            "kernel": "timeenc_vec_kernel",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": read_traffic(khash, w.name, "timeenc_kernel"),
             "algorithmic_bytes_per_launch": alg_bytes / k_n,
             "avg_launch_ms": k_ms / k_n,
             "kernel_source_hash": khash,
@@ -364,6 +482,9 @@ def main():
 
     if args.row == "f1":
         measure_gather(args, w, g, smp, run, timed_pos, B, dev)
+        return
+    if args.row == "f2":
+        measure_timeenc(args, w, smp, run, timed_pos, B, dev)
         return
 
     for b in warm_pos:
