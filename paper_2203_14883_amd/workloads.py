@@ -37,6 +37,8 @@ __all__ = ["Workload", "make", "PRESETS", "make_c1", "make_c2", "make_c3",
 
 _CHUNK = 1 << 24          # elements per independently seeded chunk
 _NEG_TAG = 0x6E6567       # stream tag for negative destinations ("neg")
+_CHUNK_TAG = 0x63686B     # stream tag for random chunk scheduling offsets ("chk")
+_CNEG_TAG = 0x636E67      # stream tag for negatives of chunk-scheduled batches ("cng")
 
 
 def _threads() -> int:
@@ -157,6 +159,47 @@ class Workload:
         roots = np.concatenate(parts).astype(np.int32, copy=False)
         root_ts = np.concatenate([t] * len(parts)).astype(np.float32, copy=False)
         return roots, root_ts, self.root_base(b)
+
+    def chunk_schedule(self, epoch: int, chunk_edges: int, batch_edges: Optional[int] = None):
+        """Random chunk scheduling (Alg. 2): the training edges are cut into
+        chunks of ``chunk_edges``; each epoch starts its batches of
+        ``batch_edges`` (default: the preset's) at a randomly chosen chunk
+        boundary inside the first batch, and keeps only whole batches, so that
+        neighbouring chunks fall into different mini-batches from one epoch to
+        the next.  Returns the epoch's batches as edge ranges ``(e_s, e_e)``.
+
+        The printed start offset is rand(0, bs/cs) * bs, a whole number of
+        batches, which would not move any chunk relative to the batch grid;
+        following the text (one chunk picked as the starting point) the
+        offset is read as rand(0, bs/cs) * cs."""
+        bs = int(batch_edges or self.batch_edges)
+        cs = int(chunk_edges)
+        if cs < 1 or bs % cs != 0:
+            raise ValueError("the chunk size must divide the batch size")
+        e_s = int(_rng(self.gen_seed, _CHUNK_TAG, int(epoch)).integers(0, bs // cs)) * cs
+        out = []
+        while e_s + bs <= self.num_edges:
+            out.append((e_s, e_s + bs))
+            e_s += bs
+        return out
+
+    def edge_batch(self, e0: int, e1: int, epoch: int = 0):
+        """Roots of the edges [e0, e1) -- sources, destinations and (if the
+        preset has them) one uniform negative destination per edge, drawn from
+        a stream keyed by (epoch, e0) -- with root_base = roots_per_edge * e0,
+        so that the batches of one epoch have disjoint root indices whatever
+        their offsets."""
+        if not 0 <= e0 <= e1 <= self.num_edges:
+            raise IndexError((e0, e1))
+        parts = [self.src[e0:e1], self.dst[e0:e1]]
+        if self.negatives:
+            lo, hi = self.neg_range
+            parts.append(_rng(self.gen_seed, _CNEG_TAG, int(epoch), int(e0)).integers(lo, hi, size=e1 - e0)
+                         .astype(np.int32))
+        t = self.ts[e0:e1]
+        roots = np.concatenate(parts).astype(np.int32, copy=False)
+        root_ts = np.concatenate([t] * len(parts)).astype(np.float32, copy=False)
+        return roots, root_ts, self.roots_per_edge * e0
 
     def batches(self, b0: int, b1: int):
         """Concatenated roots of batches [b0, b1): consecutive root_base ranges."""

@@ -220,3 +220,22 @@ def test_long_runs_and_off_grid_window_edges(torch):
             for gg, what in ((g, "indexed"), (g_plain, "no index")):
                 got = gpu_sample(gg, roots, rts, [10, 5], mode, S, D, 11, 3)
                 assert_hops_equal(got, want, "S=%d D=%s %s %s" % (S, D, mode, what))
+
+
+def test_chunk_scheduled_batches(torch):
+    """Batches of random chunk scheduling (Alg. 2) -- edge ranges that start at
+    chunk offsets, not at the batch grid -- fused into one GPU call, against the
+    oracle on the same roots and root_base."""
+    w = W.make_c2(n_users=3000, n_items=400, num_edges=60_000, seed=8)
+    og = oracle.build_tcsr(w.src, w.dst, w.ts, None, w.num_nodes, True)
+    g = gpu_build(w.src, w.dst, w.ts, None, w.num_nodes, True)
+    for epoch in (0, 3):
+        sch = w.chunk_schedule(epoch, 150)
+        parts = [w.edge_batch(a, b, epoch) for a, b in sch[10:16]]
+        roots = np.concatenate([p[0] for p in parts])
+        rts = np.concatenate([p[1] for p in parts])
+        base = parts[0][2]
+        announce("chunk-scheduled batches epoch %d start %d" % (epoch, sch[0][0]))
+        want = oracle.sample(og, roots, rts, (10, 10), "uniform", 1, math.inf, epoch, base)
+        got = gpu_sample(g, roots, rts, (10, 10), "uniform", 1, math.inf, epoch, base)
+        assert_hops_equal(got, want, "epoch %d" % epoch)

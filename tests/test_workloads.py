@@ -68,3 +68,56 @@ def test_c5_build_order_is_a_permutation():
     assert np.array_equal(src, w.src[eid]) and np.array_equal(ts, w.ts[eid])
     assert not np.all(np.diff(ts) >= 0)
     assert w.snapshots == 3 and w.snapshot_len == 1e6 and not math.isinf(w.snapshot_len)
+
+
+def test_chunk_schedule_alg2():
+    """Random chunk scheduling (Alg. 2): each epoch's batches start at a chunk
+    boundary inside the first batch, are contiguous, all full, and stop before
+    running past the last edge; the start moves from epoch to epoch."""
+    w = W.make_c2(n_users=500, n_items=60, num_edges=10_000, seed=3)
+    bs, cs = w.batch_edges, 50
+    starts = set()
+    for epoch in range(20):
+        sch = w.chunk_schedule(epoch, cs)
+        e_s = sch[0][0]
+        assert 0 <= e_s < bs and e_s % cs == 0
+        starts.add(e_s)
+        for (a, b), (c, d) in zip(sch, sch[1:]):
+            assert b == c
+        assert all(b - a == bs for a, b in sch)
+        assert sch[-1][1] <= w.num_edges < sch[-1][1] + bs
+        assert w.chunk_schedule(epoch, cs) == sch          # deterministic per epoch
+    assert len(starts) > 3
+    # one chunk per batch: the schedule is the aligned batch grid (whole batches only)
+    assert w.chunk_schedule(7, bs) == [(b * bs, (b + 1) * bs) for b in range(w.num_edges // bs)]
+    with pytest.raises(ValueError):
+        w.chunk_schedule(0, 7)
+
+
+def test_edge_batch_matches_aligned_batches():
+    w = W.make_c2(n_users=500, n_items=60, num_edges=10_000, seed=3)
+    bs = w.batch_edges
+    for b in (0, 3, 9):
+        r, t, base = w.batch(b)
+        r2, t2, base2 = w.edge_batch(b * bs, (b + 1) * bs, epoch=1)
+        assert base2 == base
+        assert np.array_equal(r2[:2 * bs], r[:2 * bs]) and np.array_equal(t2, t)
+        assert r2[2 * bs:].min() >= w.neg_range[0] and r2[2 * bs:].max() < w.neg_range[1]
+
+
+def test_chunk_batches_fuse_like_aligned_batches():
+    """Consecutive chunk-scheduled batches sampled in one call (root_base of
+    the first) give the same slots as sampled one by one: their root indices
+    are disjoint and contiguous."""
+    import oracle
+    w = W.make_c2(n_users=500, n_items=60, num_edges=10_000, seed=3)
+    g = oracle.build_tcsr(w.src, w.dst, w.ts, None, w.num_nodes, True)
+    sch = w.chunk_schedule(4, 100)[5:8]
+    parts = [w.edge_batch(a, b, epoch=4) for a, b in sch]
+    roots = np.concatenate([p[0] for p in parts])
+    rts = np.concatenate([p[1] for p in parts])
+    whole = oracle.sample(g, roots, rts, (10, 10), "uniform", 1, math.inf, 11, parts[0][2])
+    one = [oracle.sample(g, r, t, (10, 10), "uniform", 1, math.inf, 11, base) for r, t, base in parts]
+    for h in range(2):
+        assert np.array_equal(whole[h].nbr, np.concatenate([o[h].nbr for o in one]))
+        assert np.array_equal(whole[h].eid, np.concatenate([o[h].eid for o in one]))
