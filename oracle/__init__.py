@@ -66,6 +66,9 @@ def load(path: Optional[str] = None) -> C.CDLL:
     lib.oracle_sample.restype = C.c_int
     lib.oracle_sample.argtypes = [i64, P, P, P, P, i64, P, P, i32, P, i32, i32, f32,
                                   u64, u64, P, P, P, P, P, P]
+    lib.oracle_sample_anchored.restype = C.c_int
+    lib.oracle_sample_anchored.argtypes = [i64, P, P, P, P, i64, P, P, i32, P, i32, i32, f32,
+                                           u64, u64, i32, P, P, P, P, P, P]
     _lib_cache[path] = lib
     return lib
 
@@ -153,10 +156,15 @@ def capacities(num_roots: int, fanouts: Sequence[int], snapshots: int) -> List[i
     return caps
 
 
+ANCHORS = {"own": 0, "root": 1, 0: 0, 1: 1}
+
+
 def sample(g: TCSR, roots, root_ts, fanouts: Sequence[int], mode: str = "uniform",
            snapshots: int = 1, snapshot_len: float = math.inf, seed: int = 0,
-           root_base: int = 0, lib: Optional[C.CDLL] = None) -> List[Hop]:
-    """Run Algorithm 1 serially; returns one ``Hop`` per layer, sliced to its size."""
+           root_base: int = 0, lib: Optional[C.CDLL] = None, anchor="own") -> List[Hop]:
+    """Run Algorithm 1 serially; returns one ``Hop`` per layer, sliced to its size.
+    ``anchor`` places the snapshot windows of hops >= 2: "own" (the root's own
+    time) or "root" (the hop-1 root's time, below the root's own time)."""
     lib = lib or load()
     roots = np.ascontiguousarray(roots, dtype=np.int32)
     root_ts = np.ascontiguousarray(root_ts, dtype=np.float32)
@@ -170,10 +178,10 @@ def sample(g: TCSR, roots, root_ts, fanouts: Sequence[int], mode: str = "uniform
     parents = [None] + [np.empty(max(c, 1), np.int64) for c in caps[:-1]]
     PA = C.c_void_p * hops
     counts = np.zeros(hops, dtype=np.int64)
-    r = lib.oracle_sample(g.num_nodes, _ptr(g.indptr), _ptr(g.nbr), _ptr(g.eid), _ptr(g.ts),
+    r = lib.oracle_sample_anchored(g.num_nodes, _ptr(g.indptr), _ptr(g.nbr), _ptr(g.eid), _ptr(g.ts),
                           R, _ptr(roots), _ptr(root_ts), hops, _ptr(fan), MODES[mode],
                           snapshots, C.c_float(snapshot_len), seed & (2**64 - 1),
-                          root_base & (2**64 - 1),
+                          root_base & (2**64 - 1), ANCHORS[anchor],
                           PA(*[_ptr(o["nbr"]) for o in outs]), PA(*[_ptr(o["eid"]) for o in outs]),
                           PA(*[_ptr(o["ts"]) for o in outs]), PA(*[_ptr(o["dt"]) for o in outs]),
                           PA(*[_ptr(p) for p in parents]), _ptr(counts))

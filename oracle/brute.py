@@ -64,25 +64,31 @@ def _f32(x: float) -> np.float32:
 
 def sample(src, dst, ts, eid, num_nodes: int, undirected: bool, roots, root_ts,
            fanouts: Sequence[int], mode: str, snapshots: int = 1,
-           snapshot_len: float = math.inf, seed: int = 0, root_base: int = 0):
-    """Returns a list of dicts per hop: nbr, eid, ts, dt (numpy) and parent."""
+           snapshot_len: float = math.inf, seed: int = 0, root_base: int = 0, anchor: str = "own"):
+    """Returns a list of dicts per hop: nbr, eid, ts, dt (numpy) and parent.
+    With anchor "root", a root of hop >= 2 takes the window s of its hop-1
+    ancestor's time t0, cut below its own time t: t0 - (s+1)D <= ts < min(t0 - sD, t)."""
     ents = _entries(src, dst, ts, eid, undirected)
     by_owner = {}
     for en in ents:
         by_owner.setdefault(en[0], []).append(en)
     S = snapshots
     delta = float(np.float32(snapshot_len))
-    # current roots: (node, time as float of f32, window, path)
-    cur = [(int(x), float(np.float32(t)), 0, (root_base + r) & M64)
+    # current roots: (node, time as float of f32, window, path, hop-1 ancestor time)
+    cur = [(int(x), float(np.float32(t)), 0, (root_base + r) & M64, float(np.float32(t)))
            for r, (x, t) in enumerate(zip(roots, root_ts))]
     result = []
     for h, k in enumerate(fanouts, start=1):
         wins = S if h == 1 else 1
         nbr, eo, tso, dto, nxt, parent = [], [], [], [], [], []
-        for q, (x, t, s_in, path) in enumerate(cur):
+        for q, (x, t, s_in, path, t0) in enumerate(cur):
             for w in range(wins):
                 s = w if h == 1 else s_in
-                lo, hi = _window(t, s, delta)
+                if h >= 2 and anchor == "root":
+                    lo, hi = _window(t0, s, delta)
+                    hi = min(hi, t)
+                else:
+                    lo, hi = _window(t, s, delta)
                 cands = []
                 if 0 <= x < num_nodes:
                     cands = [en for en in by_owner.get(x, [])
@@ -106,7 +112,7 @@ def sample(src, dst, ts, eid, num_nodes: int, undirected: bool, roots, root_ts,
                     dto.append(float(_f32(t) - _f32(te)))    # float32 subtraction
                     if h < len(fanouts):
                         cpath = ((path * S * k + s * k + j) if h == 1 else (path * k + j)) & M64
-                        nxt.append((v, te, s, cpath))
+                        nxt.append((v, te, s, cpath, t0))
                         parent.append(slot)
         result.append(dict(nbr=np.array(nbr, np.int32), eid=np.array(eo, np.int64),
                            ts=np.array(tso, np.float32), dt=np.array(dto, np.float32),

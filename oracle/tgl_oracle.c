@@ -181,19 +181,26 @@ static double window_lo(float t, int32_t s, float delta)
     return (double)t - (double)(s + 1) * (double)delta;
 }
 
-/* Candidate window [*lo, *hi) of root (x, t) in snapshot s.  A node outside
- * [0, num_nodes) has an empty window at position 0. */
+/* Candidate window [*lo, *hi) of node x between the bounds v_lo <= ts < v_hi.
+ * A node outside [0, num_nodes) has an empty window at position 0. */
+static void locate_bounds(int64_t num_nodes, const int64_t *indptr, const float *ts,
+                          int32_t x, double v_lo, double v_hi, int64_t *lo, int64_t *hi)
+{
+    if (x < 0 || x >= num_nodes) { *lo = 0; *hi = 0; return; }
+    int64_t a = indptr[x], b = indptr[x + 1];
+    int64_t h = first_not_below(ts, a, b, v_hi);
+    int64_t l = first_not_below(ts, a, b, v_lo);
+    if (l > h) l = h;            /* keeps n = hi - lo >= 0 for any bound pair */
+    *lo = l;
+    *hi = h;
+}
+
+/* Candidate window [*lo, *hi) of root (x, t) in snapshot s. */
 void oracle_locate(int64_t num_nodes, const int64_t *indptr, const float *ts,
                    int32_t x, float t, int32_t s, float delta,
                    int64_t *lo, int64_t *hi)
 {
-    if (x < 0 || x >= num_nodes) { *lo = 0; *hi = 0; return; }
-    int64_t a = indptr[x], b = indptr[x + 1];
-    int64_t h = first_not_below(ts, a, b, window_hi(t, s, delta));
-    int64_t l = first_not_below(ts, a, b, window_lo(t, s, delta));
-    if (l > h) l = h;            /* keeps n = hi - lo >= 0 for any bound pair */
-    *lo = l;
-    *hi = h;
+    locate_bounds(num_nodes, indptr, ts, x, window_lo(t, s, delta), window_hi(t, s, delta), lo, hi);
 }
 
 /* Batch form for tests: windows of n roots in snapshots s[i]. */
@@ -247,16 +254,27 @@ static int64_t scale_draw(uint64_t h, int64_t n)
  * Hop 1 slot (r, s, j) is at (r*S + s)*k1 + j; hop h >= 2 slot (q, j) at
  * q*k_h + j.
  */
-int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
-                  const int64_t *eid, const float *ts,
-                  int64_t num_roots, const int32_t *roots, const float *root_ts,
-                  int32_t hops, const int32_t *fanouts, int32_t mode,
-                  int32_t num_snapshots, float delta, uint64_t seed,
-                  uint64_t root_base,
-                  int32_t *const *o_nbr, int64_t *const *o_eid,
-                  float *const *o_ts, float *const *o_dt,
-                  int64_t *const *o_parent, int64_t *counts)
+/*
+ * anchor selects the snapshot windows of a root of hop h >= 2 (the paper
+ * creates snapshots from the target nodes' timestamps, Section 3, and
+ * searches them at later layers, Algorithm 1):
+ *   0 -- relative to the root's own time t (its parent slot's timestamp):
+ *        [t - (s+1)D, t - sD);
+ *   1 -- relative to the time t0 of the hop-1 root it descends from, and
+ *        before its own time: [t0 - (s+1)D, min(t0 - sD, t)).
+ * Hop 1 is the same under both (t0 = t).
+ */
+int oracle_sample_anchored(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
+                           const int64_t *eid, const float *ts,
+                           int64_t num_roots, const int32_t *roots, const float *root_ts,
+                           int32_t hops, const int32_t *fanouts, int32_t mode,
+                           int32_t num_snapshots, float delta, uint64_t seed,
+                           uint64_t root_base, int32_t anchor,
+                           int32_t *const *o_nbr, int64_t *const *o_eid,
+                           float *const *o_ts, float *const *o_dt,
+                           int64_t *const *o_parent, int64_t *counts)
 {
+    if (anchor != 0 && anchor != 1) return ORACLE_EINVAL;
     if (num_nodes < 1 || num_roots < 0 || hops < 1 || hops > 8) return ORACLE_EINVAL;
     if (mode != ORACLE_MOST_RECENT && mode != ORACLE_UNIFORM) return ORACLE_EINVAL;
     if (num_snapshots < 1 || isnan(delta) || !(delta > 0.0f)) return ORACLE_EINVAL;
@@ -272,12 +290,14 @@ int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
     float *ct = (float *)malloc((size_t)(n_cur > 0 ? n_cur : 1) * sizeof(float));
     int32_t *cs = (int32_t *)malloc((size_t)(n_cur > 0 ? n_cur : 1) * sizeof(int32_t));
     uint64_t *cp = (uint64_t *)malloc((size_t)(n_cur > 0 ? n_cur : 1) * sizeof(uint64_t));
-    if (!cx || !ct || !cs || !cp) return ORACLE_ENOMEM;
+    float *ca = (float *)malloc((size_t)(n_cur > 0 ? n_cur : 1) * sizeof(float));   /* hop-1 ancestor time */
+    if (!cx || !ct || !cs || !cp || !ca) return ORACLE_ENOMEM;
     for (int64_t r = 0; r < num_roots; r++) {
         cx[r] = roots[r];
         ct[r] = root_ts[r];
         cs[r] = 0;
         cp[r] = root_base + (uint64_t)r;
+        ca[r] = root_ts[r];
     }
 
     for (int32_t h = 1; h <= hops; h++) {
@@ -286,7 +306,7 @@ int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
         counts[h - 1] = n_cur;
 
         int64_t n_slots = n_cur * wins * k;
-        int32_t *nx = NULL; float *nt = NULL; int32_t *ns = NULL; uint64_t *np_ = NULL;
+        int32_t *nx = NULL; float *nt = NULL; int32_t *ns = NULL; uint64_t *np_ = NULL; float *na = NULL;
         int64_t n_next = 0;
         if (h < hops) {
             size_t cap = (size_t)(n_slots > 0 ? n_slots : 1);
@@ -294,14 +314,21 @@ int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
             nt = (float *)malloc(cap * sizeof(float));
             ns = (int32_t *)malloc(cap * sizeof(int32_t));
             np_ = (uint64_t *)malloc(cap * sizeof(uint64_t));
-            if (!nx || !nt || !ns || !np_) return ORACLE_ENOMEM;
+            na = (float *)malloc(cap * sizeof(float));
+            if (!nx || !nt || !ns || !np_ || !na) return ORACLE_ENOMEM;
         }
 
         for (int64_t q = 0; q < n_cur; q++) {
             for (int32_t w = 0; w < wins; w++) {
                 int32_t s = (h == 1) ? w : cs[q];
                 int64_t lo, hi;
-                oracle_locate(num_nodes, indptr, ts, cx[q], ct[q], s, delta, &lo, &hi);
+                if (h >= 2 && anchor == 1) {
+                    double v_hi = window_hi(ca[q], s, delta);
+                    if ((double)ct[q] < v_hi) v_hi = (double)ct[q];
+                    locate_bounds(num_nodes, indptr, ts, cx[q], window_lo(ca[q], s, delta), v_hi, &lo, &hi);
+                } else {
+                    oracle_locate(num_nodes, indptr, ts, cx[q], ct[q], s, delta, &lo, &hi);
+                }
                 int64_t n = hi - lo;
                 for (int32_t j = 0; j < k; j++) {
                     int64_t slot = (q * wins + w) * (int64_t)k + j;
@@ -326,6 +353,7 @@ int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
                         nx[n_next] = nbr[p];
                         nt[n_next] = ts[p];
                         ns[n_next] = s;
+                        na[n_next] = ca[q];
                         np_[n_next] = (h == 1)
                             ? cp[q] * (uint64_t)S * (uint64_t)k + (uint64_t)s * (uint64_t)k + (uint64_t)j
                             : cp[q] * (uint64_t)k + (uint64_t)j;
@@ -336,12 +364,28 @@ int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
             }
         }
 
-        free(cx); free(ct); free(cs); free(cp);
+        free(cx); free(ct); free(cs); free(cp); free(ca);
         if (h == hops) { cx = NULL; break; }
-        cx = nx; ct = nt; cs = ns; cp = np_;
+        cx = nx; ct = nt; cs = ns; cp = np_; ca = na;
         n_cur = n_next;
     }
     return ORACLE_OK;
+}
+
+/* Algorithm 1 with every window relative to its root's own time. */
+int oracle_sample(int64_t num_nodes, const int64_t *indptr, const int32_t *nbr,
+                  const int64_t *eid, const float *ts,
+                  int64_t num_roots, const int32_t *roots, const float *root_ts,
+                  int32_t hops, const int32_t *fanouts, int32_t mode,
+                  int32_t num_snapshots, float delta, uint64_t seed,
+                  uint64_t root_base,
+                  int32_t *const *o_nbr, int64_t *const *o_eid,
+                  float *const *o_ts, float *const *o_dt,
+                  int64_t *const *o_parent, int64_t *counts)
+{
+    return oracle_sample_anchored(num_nodes, indptr, nbr, eid, ts, num_roots, roots, root_ts, hops,
+                                  fanouts, mode, num_snapshots, delta, seed, root_base, 0,
+                                  o_nbr, o_eid, o_ts, o_dt, o_parent, counts);
 }
 
 int oracle_version(void) { return 1; }

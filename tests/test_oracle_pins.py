@@ -280,3 +280,48 @@ def test_reached_subgraph_equals_full_graph(name, kw):
         a, b = full.indptr[x], full.indptr[x + 1]
         c, d = g.indptr[x], g.indptr[x + 1]
         assert np.array_equal(full.eid[a:b], g.eid[c:d]) and np.array_equal(full.ts[a:b], g.ts[c:d])
+
+
+def test_anchor_root_matches_brute_force():
+    """Snapshot anchor A (windows of hops >= 2 at the hop-1 root's time, cut
+    below the root's own time) against the brute-force scan."""
+    rng = np.random.default_rng(12)
+    trials = 0
+    while trials < 150:
+        N, src, dst, ts, eid, und, roots, rts, fan, mode, S, delta, seed, base = _random_case(rng)
+        if len(fan) < 2:
+            continue
+        trials += 1
+        g = oracle.build_tcsr(src, dst, ts, eid, N, und)
+        got = oracle.sample(g, roots, rts, fan, mode, S, delta, seed, base, anchor="root")
+        want = brute.sample(src, dst, ts, eid, N, und, roots, rts, fan, mode, S, delta, seed, base,
+                            anchor="root")
+        assert_hops_equal(got, want, "anchor trial %d" % trials)
+
+
+def test_anchor_root_invariants_and_special_case():
+    """Under anchor A every slot of hop >= 2 lies in its ancestor's window s
+    and before its parent's time; with one unbounded window (S = 1, D = inf)
+    the two anchors coincide, since a parent's time is below its root's."""
+    w = W.make_c2(n_users=400, n_items=50, num_edges=8000, seed=31)
+    g = oracle.build_tcsr(w.src, w.dst, w.ts, None, w.num_nodes, True)
+    roots, rts, base = w.batches(2, 6)
+    a = oracle.sample(g, roots, rts, (10, 10), "uniform", 1, math.inf, 5, base, anchor="root")
+    b = oracle.sample(g, roots, rts, (10, 10), "uniform", 1, math.inf, 5, base, anchor="own")
+    assert_hops_equal(a, b, "S=1 anchors")
+    S, D = 3, 2.0e4
+    for mode in ("uniform", "recent"):
+        hops = oracle.sample(g, roots, rts, (5, 5, 3), mode, S, D, 5, base, anchor="root")
+        t0 = np.repeat(rts.astype(np.float64), S * 5)            # hop-1 slot -> its root's time
+        s1 = np.tile(np.repeat(np.arange(S), 5), len(roots))     # hop-1 slot -> its window
+        par_t = hops[0].ts.astype(np.float64)
+        for h in (1, 2):
+            hop = hops[h]
+            k = 5 if h == 1 else 3
+            par = np.repeat(hop.parent, k)
+            t0, s1, par_t = t0[par], s1[par], par_t[par]
+            ok = hop.nbr >= 0
+            tsv = hop.ts.astype(np.float64)
+            assert np.all(tsv[ok] >= t0[ok] - (s1[ok] + 1) * D)
+            assert np.all(tsv[ok] < np.minimum(t0[ok] - s1[ok] * D, par_t[ok]))
+            par_t = tsv
