@@ -259,6 +259,33 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
                       uint64_t root_base, const tgl_hop_out *outs, int64_t *counts,
                       void *workspace, size_t workspace_bytes, void *stream);
 
+/* Options of tgl_sample_ex (zero-initialise; NULL means all defaults). */
+#define TGL_ANCHOR_OWN  0  /* windows of a hop >= 2 root at its own time t:
+                              [t - (s+1) D, t - s D) (the default)              */
+#define TGL_ANCHOR_ROOT 1  /* at the time t0 of its hop-1 ancestor, cut below
+                              its own time: [t0 - (s+1) D, min(t0 - s D, t))    */
+typedef struct tgl_sample_opts {
+    int32_t anchor;        /* TGL_ANCHOR_OWN or TGL_ANCHOR_ROOT                   */
+    int32_t reserved;      /* 0                                                  */
+} tgl_sample_opts;
+
+/*
+ * tgl_sample with options.  The snapshot anchor chooses where the windows of
+ * the roots of hops >= 2 sit.  The paper creates snapshots from the target
+ * nodes' timestamps (Section 3) and searches "the snapshot S_s" at later
+ * layers (Algorithm 1); TGL_ANCHOR_OWN reads the target of a later layer as
+ * that layer's root (its own time, the neighbour's edge time), and
+ * TGL_ANCHOR_ROOT as the mini-batch's root, keeping strict ts < t below the
+ * parent.  Hop 1 is the same under both, and so is every hop when S = 1 and
+ * D = +inf.  Other arguments, errors and outputs as tgl_sample; opts may be
+ * NULL; an unknown anchor is TGL_EINVAL.
+ */
+tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
+                         int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
+                         int32_t num_snapshots, float snapshot_len, uint64_t seed,
+                         uint64_t root_base, const tgl_sample_opts *opts, const tgl_hop_out *outs,
+                         int64_t *counts, void *workspace, size_t workspace_bytes, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Feature / state gather for sampled slots (Figure 2, steps 2 and 3)       */
 /* ------------------------------------------------------------------------ */

@@ -37,6 +37,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
            "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
+           "tgl_sample_ex",
            "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
@@ -56,6 +57,13 @@ class c_tcsr(C.Structure):
 class c_table(C.Structure):
     _fields_ = [("rows", C.c_void_p), ("out", C.c_void_p), ("num_rows", C.c_int64),
                 ("row_bytes", C.c_int32), ("key", C.c_int32)]
+
+
+class c_sample_opts(C.Structure):
+    _fields_ = [("anchor", C.c_int32), ("reserved", C.c_int32)]
+
+
+ANCHORS = {"own": 0, "root": 1, 0: 0, 1: 1}
 
 
 class c_hop_out(C.Structure):
@@ -95,6 +103,9 @@ def lib() -> C.CDLL:
     L.tgl_sample.restype = i32
     L.tgl_sample.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
                              C.POINTER(c_hop_out), P, P, C.c_size_t, P]
+    L.tgl_sample_ex.restype = i32
+    L.tgl_sample_ex.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
+                                C.POINTER(c_sample_opts), C.POINTER(c_hop_out), P, P, C.c_size_t, P]
     L.tgl_gather.restype = i32
     L.tgl_gather.argtypes = [P, P, i64, P, i64, C.POINTER(c_table), i32, P]
     L.tgl_time_encode.restype = i32
@@ -308,7 +319,10 @@ class Sampler:
 
     def run(self, g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, mode="uniform",
             snapshot_len: float = math.inf, seed: int = 0, root_base: int = 0, stream=None,
-            num_roots: Optional[int] = None):
+            num_roots: Optional[int] = None, anchor="own"):
+        """Enqueues one sampling call.  ``anchor`` places the snapshot windows
+        of hops >= 2 at the root's own time ("own") or at its hop-1 ancestor's
+        time, cut below its own ("root")."""
         n = int(roots.shape[0]) if num_roots is None else int(num_roots)
         if n > self.max_roots:
             raise ValueError("more roots than the sampler was sized for")
@@ -317,12 +331,13 @@ class Sampler:
         if not roots.is_contiguous() or not root_ts.is_contiguous():
             raise ValueError("roots and root_ts must be contiguous")
         view = g.c_view()
-        s = lib().tgl_sample(C.byref(view), _p(roots), _p(root_ts), n, len(self.fanouts), self._fp,
-                             MODES[mode], self.snapshots, C.c_float(snapshot_len),
-                             C.c_uint64(seed & (2**64 - 1)), C.c_uint64(root_base & (2**64 - 1)),
-                             self._outs, _p(self.counts), _p(self.workspace),
-                             self.workspace.numel(), _stream(stream))
-        _check(s, "tgl_sample")
+        opts = c_sample_opts(ANCHORS[anchor], 0)
+        s = lib().tgl_sample_ex(C.byref(view), _p(roots), _p(root_ts), n, len(self.fanouts), self._fp,
+                                MODES[mode], self.snapshots, C.c_float(snapshot_len),
+                                C.c_uint64(seed & (2**64 - 1)), C.c_uint64(root_base & (2**64 - 1)),
+                                C.byref(opts), self._outs, _p(self.counts), _p(self.workspace),
+                                self.workspace.numel(), _stream(stream))
+        _check(s, "tgl_sample_ex")
 
     def hops(self) -> List[Hop]:
         """Slices the outputs of the last call by the per-hop root counts (syncs)."""
@@ -338,10 +353,10 @@ class Sampler:
 
 def sample(g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, fanouts: Sequence[int],
            mode="uniform", snapshots: int = 1, snapshot_len: float = math.inf, seed: int = 0,
-           root_base: int = 0, stream=None) -> List[Hop]:
+           root_base: int = 0, stream=None, anchor="own") -> List[Hop]:
     """One-shot sampling call; returns per-hop outputs sliced to their sizes."""
     smp = Sampler(max(int(roots.shape[0]), 0), fanouts, snapshots, device=roots.device)
-    smp.run(g, roots, root_ts, mode, snapshot_len, seed, root_base, stream)
+    smp.run(g, roots, root_ts, mode, snapshot_len, seed, root_base, stream, anchor=anchor)
     return smp.hops()
 
 

@@ -64,6 +64,7 @@ struct HopArgs {
     const float *p_ts;
     const int64_t *p_off;       // exclusive offsets of the previous hop's groups
     const int32_t *p_s;         // window of each previous-hop group (null: hop 1 groups)
+    const float *p_t0;          // hop-1 ancestor time of each previous-hop group (anchor A, hops >= 3)
     const uint64_t *p_path;     // path of each previous-hop group (null: hop 1 groups)
     int32_t p_k;                // fanout of the previous hop
     int64_t p_groups_static;    // previous hop's groups (hop 1 groups: R*S) ...
@@ -76,6 +77,7 @@ struct HopArgs {
     int32_t windows;            // windows per root: S on hop 1, 1 afterwards
     float delta;
     int32_t delta_inf;
+    int32_t anchor;             // TGL_ANCHOR_OWN / TGL_ANCHOR_ROOT (windows of hops >= 2)
     uint64_t seedmix;           // mix64(seed ^ golden)
     // outputs
     int32_t *o_nbr;
@@ -85,6 +87,7 @@ struct HopArgs {
     int64_t *o_parent;          // hops >= 2
     int32_t *o_cnt;             // valid slots per (root, window) group, or null (last hop)
     int32_t *o_s;               // window of each root, for a later hop (or null)
+    float *o_t0;                // hop-1 ancestor time of each root, for a later hop (anchor A, or null)
     uint64_t *o_path;           // path of each root, for a later hop (or null)
     int64_t *count0_out;        // hop 1 stores its root count here
 };
@@ -495,13 +498,14 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     }
 }
 
-// Window [lo, hi) of a root with run [a, b) at time t in window s0 (one
-// window per root), by the G lanes of its group.  An edge that the run's
-// first and last timestamps decide is not searched.  NB is the number of
-// window edges: 1 when windows are unbounded below (lo = a), else 2.
+// Window [lo, hi) of a root with run [a, b) between the float thresholds
+// vl <= ts < vh (one window per root), by the G lanes of its group.  An edge
+// that the run's first and last timestamps decide is not searched.  NB is
+// the number of window edges: 1 when windows are unbounded below (lo = a),
+// else 2.
 template <int G, int NB>
 __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint32_t a, uint32_t b, float first,
-                                              float last, float t, int32_t s0, int gl, uint32_t &lo, uint32_t &hi) {
+                                              float last, float vh, float vl, int gl, uint32_t &lo, uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     // a non-empty run belongs to a node inside the graph
     const int4 *rec = b > a && b - a <= TGL_NODE_INLINE ? p.nodes + static_cast<int64_t>(x) * 8 : nullptr;
@@ -510,7 +514,7 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
     uint32_t c[NB];
 #pragma unroll
     for (int i = 0; i < NB; i++) {
-        v[i] = bound_value(t, s0 + i, p.delta);
+        v[i] = i == 0 ? vh : vl;
         c[i] = a;
         act[i] = !edge_from_summary(a, b, first, last, v[i], c[i]);
     }
@@ -549,6 +553,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
     __shared__ float r_t[kWavesPerBlock][kWave];
     __shared__ int32_t r_s[kWavesPerBlock][kWave];
     __shared__ int32_t r_x[kWavesPerBlock][kWave];     // node of each packed root
+    __shared__ float r_vh[kWavesPerBlock][kWave];      // window thresholds: vl <= ts < vh
+    __shared__ float r_vl[kWavesPerBlock][NB == 2 ? kWave : 1];
     __shared__ uint8_t r_need[kWavesPerBlock][kWave];  // packed roots whose window needs a search
 
     const int64_t pk = FIRST ? 1 : p.p_k;
@@ -576,11 +582,13 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
         int64_t q = 0;
         int32_t s = 0;
         uint64_t path = 0;
+        float ta = 0.0f;                        // the time the windows are placed at
         if constexpr (FIRST) {
             valid = v < nv;
             if (valid) {
                 x = p.rx[v];
                 t = p.rt[v];
+                ta = t;
                 q = v;
                 path = p.root_base + static_cast<uint64_t>(v);
             }
@@ -589,6 +597,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
             valid = x >= 0;
             if (valid) {
                 t = p.p_ts[v];
+                ta = t;
                 const int64_t g = v / pk;
                 const int64_t j = v - g * pk;
                 q = p.p_off[g] + j;
@@ -599,6 +608,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                     s = static_cast<int32_t>(static_cast<uint64_t>(g) % S);
                     path = path1 + static_cast<uint64_t>(v);
                 }
+                if (p.anchor == TGL_ANCHOR_ROOT) {
+                    // hop-1 ancestor: hop-2 roots come from hop-1 group (r, s) = g
+                    ta = p.p_t0 ? p.p_t0[g] : p.rt[static_cast<uint64_t>(g) / S];
+                    if (p.o_t0) p.o_t0[q] = ta;
+                }
                 p.o_parent[q] = v;
                 if (p.o_s) {
                     p.o_s[q] = s;
@@ -607,13 +621,16 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
             }
         }
         const NodeRun run = node_run(p, x, valid);
+        // window thresholds; with the root anchor the window also ends below t
+        float vh = bound_value(ta, s, p.delta);
+        if (p.anchor == TGL_ANCHOR_ROOT && t < vh) vh = t;
+        const float vl = NB == 2 ? bound_value(ta, s + 1, p.delta) : 0.0f;
         // window edges the run's first and last timestamps decide
         uint32_t lo = run.a, hi = run.a;
         bool need = false;
         if (valid) {
-            need = !edge_from_summary(run.a, run.b, run.first, run.last, bound_value(t, s, p.delta), hi);
-            if constexpr (NB == 2)
-                need |= !edge_from_summary(run.a, run.b, run.first, run.last, bound_value(t, s + 1, p.delta), lo);
+            need = !edge_from_summary(run.a, run.b, run.first, run.last, vh, hi);
+            if constexpr (NB == 2) need |= !edge_from_summary(run.a, run.b, run.first, run.last, vl, lo);
             if (lo > hi) lo = hi;
         }
         const uint64_t mask = __ballot(valid);
@@ -629,6 +646,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
             r_t[w][r] = t;
             r_s[w][r] = s;
             r_x[w][r] = x;
+            r_vh[w][r] = vh;
+            if constexpr (NB == 2) r_vl[w][r] = vl;
             if (need) r_need[w][rank_below(need_mask)] = static_cast<uint8_t>(r);
             if (!need && p.o_cnt) {
                 const uint32_t n = hi - lo;
@@ -645,8 +664,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
             if (base + gw < nneed) {                // group-uniform
                 const int i = r_need[w][base + gw];
                 uint32_t wlo, whi;
-                locate_window<G, NB>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_t[w][i], r_s[w][i],
-                                 gl, wlo, whi);
+                locate_window<G, NB>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_vh[w][i],
+                                     NB == 2 ? r_vl[w][i] : 0.0f, gl, wlo, whi);
                 if (gl == 0) {
                     r_lo[w][i] = wlo;
                     r_n[w][i] = whi - wlo;
@@ -775,11 +794,13 @@ struct SampleWs {
     int64_t *partials = nullptr;
     int32_t *s[2] = {nullptr, nullptr};       // window per root (hops 2..L-1)
     uint64_t *path[2] = {nullptr, nullptr};   // path per root (hops 2..L-1)
+    float *t0[2] = {nullptr, nullptr};        // hop-1 ancestor time per root (hops 2..L-1, root anchor)
     size_t bytes = 0;
 };
 
 // Workspace: per-group counts, offsets and scan partials for the largest hop
-// h < L; window and path of the roots of hops 2..L-1 (two alternating buffers).
+// h < L; window, path and hop-1 ancestor time of the roots of hops 2..L-1
+// (two alternating buffers).
 SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S) {
     SampleWs w;
     Carver cv(base);
@@ -796,6 +817,7 @@ SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S
             for (int i = 0; i < nbuf; i++) {
                 w.s[i] = cv.take<int32_t>(static_cast<size_t>(max_mid));
                 w.path[i] = cv.take<uint64_t>(static_cast<size_t>(max_mid));
+                w.t0[i] = cv.take<float>(static_cast<size_t>(max_mid));
             }
         }
     }
@@ -827,13 +849,15 @@ size_t tgl_sample_workspace(int64_t num_roots, int32_t hops, const int32_t *fano
     return carve_sample_ws(nullptr, hops, cap, num_snapshots).bytes;
 }
 
-tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
-                      int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
-                      int32_t num_snapshots, float snapshot_len, uint64_t seed,
-                      uint64_t root_base, const tgl_hop_out *outs, int64_t *counts,
-                      void *workspace, size_t workspace_bytes, void *stream) {
+tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
+                         int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
+                         int32_t num_snapshots, float snapshot_len, uint64_t seed,
+                         uint64_t root_base, const tgl_sample_opts *opts, const tgl_hop_out *outs,
+                         int64_t *counts, void *workspace, size_t workspace_bytes, void *stream) {
     // ---- host-side argument checks (nothing is enqueued on failure) ----
     if (!g || !outs || !counts) return TGL_EINVAL;
+    const int32_t anchor = opts ? opts->anchor : TGL_ANCHOR_OWN;
+    if (anchor != TGL_ANCHOR_OWN && anchor != TGL_ANCHOR_ROOT) return TGL_EINVAL;
     if (!sample_args_ok(num_roots, hops, fanouts, num_snapshots)) return TGL_EINVAL;
     if (mode != TGL_MOST_RECENT && mode != TGL_UNIFORM) return TGL_EINVAL;
     if (snapshot_len != snapshot_len || !(snapshot_len > 0.0f)) return TGL_EINVAL;
@@ -878,6 +902,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
     a.S = num_snapshots;
     a.delta = snapshot_len;
     a.delta_inf = dinf ? 1 : 0;
+    a.anchor = anchor;
     a.seedmix = mix64(seed ^ kGolden);
 
     const int32_t S = num_snapshots;
@@ -899,6 +924,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
         const bool keep = h >= 2 && h < hops;
         a.o_s = keep ? ws.s[h & 1] : nullptr;
         a.o_path = keep ? ws.path[h & 1] : nullptr;
+        a.o_t0 = keep && anchor == TGL_ANCHOR_ROOT ? ws.t0[h & 1] : nullptr;
         a.count0_out = h == 1 ? counts : nullptr;
         if (h >= 2) {
             const tgl_hop_out &po = outs[h - 2];
@@ -908,6 +934,7 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
             a.p_k = fanouts[h - 2];
             a.p_s = h >= 3 ? ws.s[(h - 1) & 1] : nullptr;
             a.p_path = h >= 3 ? ws.path[(h - 1) & 1] : nullptr;
+            a.p_t0 = h >= 3 && anchor == TGL_ANCHOR_ROOT ? ws.t0[(h - 1) & 1] : nullptr;
             a.p_groups_static = h == 2 ? num_roots * S : 0;
             a.p_groups_dyn = h == 2 ? nullptr : counts + (h - 2);
         }
@@ -934,6 +961,15 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
     }
     return TGL_OK;
+}
+
+tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
+                      int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
+                      int32_t num_snapshots, float snapshot_len, uint64_t seed,
+                      uint64_t root_base, const tgl_hop_out *outs, int64_t *counts,
+                      void *workspace, size_t workspace_bytes, void *stream) {
+    return tgl_sample_ex(g, roots, root_ts, num_roots, hops, fanouts, mode, num_snapshots, snapshot_len, seed,
+                         root_base, nullptr, outs, counts, workspace, workspace_bytes, stream);
 }
 
 }  // extern "C"

@@ -205,3 +205,14 @@ def test_time_encode_rejects_invalid_arguments(kw):
 
 def test_time_encode_empty_is_a_no_op():
     assert _te_call(n=0, dt=None, out=None) == B.OK
+
+
+def test_sample_ex_rejects_unknown_anchor():
+    L = P.lib()
+    fa, fp = _fan([10, 10])
+    outs = (B.c_hop_out * 2)(*[B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE) for _ in range(2)])
+    g = B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE)
+    for anchor in (2, -1):
+        opts = B.c_sample_opts(anchor, 0)
+        assert L.tgl_sample_ex(C.byref(g), FAKE, FAKE, 5, 2, fp, 1, 1, C.c_float(math.inf), C.c_uint64(1),
+                               C.c_uint64(0), C.byref(opts), outs, FAKE, FAKE, 1 << 30, None) == B.EINVAL

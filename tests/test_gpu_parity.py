@@ -36,8 +36,9 @@ def gpu_build(src, dst, ts, eid, n, undirected):
                         None if eid is None else upload(eid, np.int64), n, undirected)
 
 
-def gpu_sample(g, roots, rts, fan, mode, S, D, seed, base):
-    out = P.sample(g, upload(roots, np.int32), upload(rts, np.float32), fan, mode, S, D, seed, base)
+def gpu_sample(g, roots, rts, fan, mode, S, D, seed, base, anchor="own"):
+    out = P.sample(g, upload(roots, np.int32), upload(rts, np.float32), fan, mode, S, D, seed, base,
+                   anchor=anchor)
     return hops_to_numpy(out)
 
 
@@ -239,3 +240,37 @@ def test_chunk_scheduled_batches(torch):
         want = oracle.sample(og, roots, rts, (10, 10), "uniform", 1, math.inf, epoch, base)
         got = gpu_sample(g, roots, rts, (10, 10), "uniform", 1, math.inf, epoch, base)
         assert_hops_equal(got, want, "epoch %d" % epoch)
+
+
+def test_snapshot_anchor_root(torch):
+    """Snapshot anchor A (windows of hops >= 2 at the hop-1 root's time, cut
+    below the root's own time) on random graphs with 2-4 hops, several
+    snapshots and finite window lengths, and on a reduced c5 (3 snapshots of
+    1e6, 2-hop uniform)."""
+    rng = np.random.default_rng(99)
+    trial = 0
+    while trial < 60:
+        N, src, dst, ts, eid, und, roots, rts, fan, mode, S, D, seed, base = _rand_case(rng)
+        if len(fan) < 2:
+            continue
+        if math.isinf(D):
+            S, D = int(rng.integers(2, 5)), float(rng.choice([2.5, 9.0]))
+        trial += 1
+        announce("anchor trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s" % (trial, N, len(src), len(roots), fan,
+                                                                              mode, S, D))
+        want_g = oracle.build_tcsr(src, dst, ts, eid, N, und)
+        g = gpu_build(src, dst, ts, eid, N, und)
+        want = oracle.sample(want_g, roots, rts, fan, mode, S, D, seed, base, anchor="root")
+        got = gpu_sample(g, roots, rts, fan, mode, S, D, seed, base, anchor="root")
+        assert_hops_equal(got, want, "anchor trial %d" % trial)
+    w = W.make_c5(num_nodes=1_000_000, num_edges=10_000_000, batch_edges=60_000)
+    og = oracle.build_tcsr(w.src, w.dst, w.ts, None, w.num_nodes, True)
+    g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid)
+    roots, rts, base = w.batches(80, 81)
+    for anchor in ("root", "own"):
+        announce("anchor %s on reduced c5" % anchor)
+        want = oracle.sample(og, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base,
+                             anchor=anchor)
+        got = gpu_sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base,
+                         anchor=anchor)
+        assert_hops_equal(got, want, "c5 anchor %s" % anchor)
