@@ -267,6 +267,8 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
 typedef struct tgl_sample_opts {
     int32_t anchor;        /* TGL_ANCHOR_OWN or TGL_ANCHOR_ROOT                   */
     int32_t reserved;      /* 0                                                  */
+    uint32_t *pointers;    /* [device] (S + 1) x num_nodes saved window edges, or
+                              NULL: see tgl_pointers_reset                       */
 } tgl_sample_opts;
 
 /*
@@ -285,6 +287,26 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
                          int32_t num_snapshots, float snapshot_len, uint64_t seed,
                          uint64_t root_base, const tgl_sample_opts *opts, const tgl_hop_out *outs,
                          int64_t *counts, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Per-node pointer arrays of Section 3.1 / Algorithm 1 for hop 1: entry
+ * i * num_nodes + x is a saved position in node x's run for window edge i
+ * (edge i at t - i * D, i = 0..S), which the sampler advances as roots come
+ * in chronologically instead of searching the run from scratch.  On the GPU
+ * they are an acceleration structure with no effect on results: hop 1 of a
+ * tgl_sample_ex call with opts->pointers reads a node's saved position for
+ * each edge it must locate in a run longer than 61 entries (the shorter ones
+ * are one load anyway), loads the timestamps around it, falls back to a
+ * search of the rest of the run if the edge is not among them, and raises
+ * the saved position to the edge found (atomic maximum, so duplicate roots
+ * in a batch need no locks).  Roots in chronological order per node make the
+ * first load the answer, as in the paper; any order gives the same samples.
+ *   pointers   [device] uint32[(num_snapshots + 1) * num_nodes], caller-owned,
+ *              kept across calls for one T-CSR and one num_snapshots
+ * tgl_pointers_reset sets every saved position to the start of its run (the
+ * start of an epoch).  Never synchronises.
+ */
+tgl_status tgl_pointers_reset(const tgl_tcsr *g, int32_t num_snapshots, uint32_t *pointers, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Feature / state gather for sampled slots (Figure 2, steps 2 and 3)       */

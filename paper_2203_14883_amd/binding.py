@@ -37,7 +37,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
            "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
-           "tgl_sample_ex",
+           "tgl_sample_ex", "tgl_pointers_reset",
            "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
@@ -60,7 +60,7 @@ class c_table(C.Structure):
 
 
 class c_sample_opts(C.Structure):
-    _fields_ = [("anchor", C.c_int32), ("reserved", C.c_int32)]
+    _fields_ = [("anchor", C.c_int32), ("reserved", C.c_int32), ("pointers", C.c_void_p)]
 
 
 ANCHORS = {"own": 0, "root": 1, 0: 0, 1: 1}
@@ -106,6 +106,8 @@ def lib() -> C.CDLL:
     L.tgl_sample_ex.restype = i32
     L.tgl_sample_ex.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
                                 C.POINTER(c_sample_opts), C.POINTER(c_hop_out), P, P, C.c_size_t, P]
+    L.tgl_pointers_reset.restype = i32
+    L.tgl_pointers_reset.argtypes = [C.POINTER(c_tcsr), i32, P, P]
     L.tgl_gather.restype = i32
     L.tgl_gather.argtypes = [P, P, i64, P, i64, C.POINTER(c_table), i32, P]
     L.tgl_time_encode.restype = i32
@@ -319,10 +321,12 @@ class Sampler:
 
     def run(self, g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, mode="uniform",
             snapshot_len: float = math.inf, seed: int = 0, root_base: int = 0, stream=None,
-            num_roots: Optional[int] = None, anchor="own"):
+            num_roots: Optional[int] = None, anchor="own", pointers: Optional[torch.Tensor] = None):
         """Enqueues one sampling call.  ``anchor`` places the snapshot windows
         of hops >= 2 at the root's own time ("own") or at its hop-1 ancestor's
-        time, cut below its own ("root")."""
+        time, cut below its own ("root").  ``pointers`` (from
+        ``pointers_reset``) makes hop 1 start from, and advance, saved window
+        edges (Sec. 3.1); the samples are the same."""
         n = int(roots.shape[0]) if num_roots is None else int(num_roots)
         if n > self.max_roots:
             raise ValueError("more roots than the sampler was sized for")
@@ -331,7 +335,10 @@ class Sampler:
         if not roots.is_contiguous() or not root_ts.is_contiguous():
             raise ValueError("roots and root_ts must be contiguous")
         view = g.c_view()
-        opts = c_sample_opts(ANCHORS[anchor], 0)
+        if pointers is not None and (pointers.dtype != torch.int32 or not pointers.is_contiguous()
+                                     or pointers.numel() != (self.snapshots + 1) * g.num_nodes):
+            raise ValueError("pointers must be a contiguous int32 tensor of (snapshots + 1) * num_nodes")
+        opts = c_sample_opts(ANCHORS[anchor], 0, None if pointers is None else pointers.data_ptr())
         s = lib().tgl_sample_ex(C.byref(view), _p(roots), _p(root_ts), n, len(self.fanouts), self._fp,
                                 MODES[mode], self.snapshots, C.c_float(snapshot_len),
                                 C.c_uint64(seed & (2**64 - 1)), C.c_uint64(root_base & (2**64 - 1)),
@@ -349,6 +356,20 @@ class Sampler:
             out.append(Hop(self.nbr[h][:n], self.eid[h][:n], self.ts[h][:n], self.dt[h][:n],
                            None if h == 0 else self.parent[h][:nr], nr))
         return out
+
+
+def pointers_reset(g: TCSR, snapshots: int = 1, pointers: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """Saved window edges of hop 1 (Sec. 3.1's per-node pointers), one per node
+    and window edge, set to the start of every run; allocated here unless
+    given.  Stored as int32 (the library reads them as uint32 positions)."""
+    n = (int(snapshots) + 1) * g.num_nodes
+    if pointers is None:
+        pointers = torch.empty(n, dtype=torch.int32, device=g.indptr.device)
+    view = g.c_view()
+    _check(lib().tgl_pointers_reset(C.byref(view), int(snapshots), pointers.data_ptr(), _stream(stream)),
+           "tgl_pointers_reset")
+    return pointers
 
 
 def sample(g: TCSR, roots: torch.Tensor, root_ts: torch.Tensor, fanouts: Sequence[int],

@@ -78,6 +78,7 @@ struct HopArgs {
     float delta;
     int32_t delta_inf;
     int32_t anchor;             // TGL_ANCHOR_OWN / TGL_ANCHOR_ROOT (windows of hops >= 2)
+    uint32_t *ptr;              // hop 1: saved window edges, (S + 1) x num_nodes, or null
     uint64_t seedmix;           // mix64(seed ^ golden)
     // outputs
     int32_t *o_nbr;
@@ -276,6 +277,59 @@ __device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uin
     for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0;
 }
 
+// Window edges of a long run [a, b) found from saved positions -- the
+// per-node pointers of Section 3.1, kept for hop 1 -- by the G lanes of one
+// group: edge i (threshold v[i]) is first looked for in the held stretch that
+// starts one entry before its saved position ptr[ei[i] * N + x].  If the whole
+// stretch lies at or above v[i] the edge is before it, if the whole stretch
+// lies below v[i] the edge is after it: only then is the rest of the run
+// searched.  The saved position is raised to the edge found.  Any saved
+// position in [a, b] gives the same result; a chronological root stream
+// makes the first load the answer.
+template <int G, int NE>
+__device__ __forceinline__ void from_pointers(const HopArgs &p, int32_t x, uint32_t a, uint32_t b,
+                                              const int (&ei)[NE], const float (&v)[NE], const bool (&act)[NE],
+                                              uint32_t (&out)[NE], int gl) {
+    const uint32_t M = static_cast<uint32_t>(p.num_entries);
+    constexpr uint32_t span = HeldRun<G>::span;
+    uint32_t lo[NE], hi[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        uint32_t p0 = a;
+        if (act[i]) {
+            p0 = p.ptr[static_cast<int64_t>(ei[i]) * p.num_nodes + x];
+            p0 = p0 < a ? a : (p0 > b ? b : p0);
+        }
+        lo[i] = p0 > a ? p0 - 1 : a;
+        hi[i] = act[i] ? (b - lo[i] > span ? lo[i] + span : b) : lo[i];
+    }
+    HeldRun<G> r[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) r[i] = load_run<G>(p.tsa, lo[i], hi[i], M, gl);
+    uint32_t flo[NE], fhi[NE];
+    bool fb[NE];
+    bool any = false;
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        out[i] = count_in<G>(r[i], lo[i], hi[i], v[i]);
+        fb[i] = act[i] && ((out[i] == lo[i] && lo[i] > a) || (out[i] == hi[i] && hi[i] < b));
+        flo[i] = fb[i] ? (out[i] == lo[i] && lo[i] > a ? a : hi[i]) : a;
+        fhi[i] = fb[i] ? (out[i] == lo[i] && lo[i] > a ? lo[i] : b) : a;
+        any |= fb[i];
+    }
+    if (any) {                                      // group-uniform
+        search_n<G, NE>(p.tsa, M, flo, fhi, v, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++)
+            if (fb[i]) out[i] = flo[i];
+    }
+    if (gl == 0) {
+#pragma unroll
+        for (int i = 0; i < NE; i++)
+            if (act[i]) atomicMax(p.ptr + static_cast<int64_t>(ei[i]) * p.num_nodes + x, out[i]);
+    }
+}
+
 // Upper edge of window i (= lower edge of window i - 1), t - i * delta, as a
 // float threshold.  Window membership compares a timestamp with the edge
 // computed in double; rounding the edge up to the nearest float f >= edge (+inf
@@ -361,9 +415,10 @@ __device__ __forceinline__ void wave_sync_lds() {
 // windows: run [a, b) with first and last timestamps, query time t, hash key
 // hp; its slots start at q * S * k.  All G lanes of the group call it
 // together; my_edges is the group's row of LDS.
-template <int G, int MODE, bool LAST>
-__device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, uint32_t a, uint32_t b, float first,
-                                           float last, float t, uint64_t hp, int gl, uint32_t *my_edges) {
+template <int G, int MODE, bool LAST, bool PTR>
+__device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, int32_t x, uint32_t a, uint32_t b,
+                                           float first, float last, float t, uint64_t hp, int gl,
+                                           uint32_t *my_edges) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     const int W = p.windows;
     const int k = p.k;
@@ -384,7 +439,14 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, uint32_t
             act[u] = i0 + u <= W && !edge_from_summary(a, b, first, last, v[u], c[u]);
         }
         uint32_t cs[NE];
-        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, nullptr, a, top, v, act, cs, gl);
+        if (PTR && b - a > HeldRun<G>::span) {      // group-uniform: long run, saved positions kept
+            int ei[NE];
+#pragma unroll
+            for (int u = 0; u < NE; u++) ei[u] = i0 + u;
+            from_pointers<G, NE>(p, x, a, b, ei, v, act, cs, gl);
+        } else {
+            count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, nullptr, a, top, v, act, cs, gl);
+        }
 #pragma unroll
         for (int u = 0; u < NE; u++) {
             if (i0 + u <= W) {
@@ -442,7 +504,7 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, uint32_t
 //     packed into LDS;
 //   phase 2, G lanes per root, 64 / G roots per round: the S + 1 window
 //     edges, then selection and emission of the root's S * k slots.
-template <int G, int MODE, bool LAST>
+template <int G, int MODE, bool LAST, bool PTR>
 __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots served per wavefront round
     constexpr int GPB = kBlock / G;
@@ -456,6 +518,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     __shared__ float r_l[kWavesPerBlock][kWave];
     __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
     __shared__ float r_t[kWavesPerBlock][kWave];
+    __shared__ int32_t r_x[kWavesPerBlock][kWave];
     __shared__ uint32_t edges[GPB * (TGL_MAX_SNAPSHOTS + 1)];
     uint32_t *my_edges = edges + (w * GPW + gw) * (TGL_MAX_SNAPSHOTS + 1);
 
@@ -482,6 +545,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
             r_l[w][lane] = run.last;
             r_hp[w][lane] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ (p.root_base + static_cast<uint64_t>(v))) : 0;
             r_t[w][lane] = t;
+            r_x[w][lane] = x;
         }
         wave_sync_lds();
         // ---- phase 2: G lanes per root ----
@@ -490,8 +554,8 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
         for (int base = 0; base < nvalid; base += GPW) {
             const int i = base + gw;
             if (i < nvalid) {                       // group-uniform
-                multi_root<G, MODE, LAST>(p, c * kWave + i, r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i], r_t[w][i],
-                                          r_hp[w][i], gl, my_edges);
+                multi_root<G, MODE, LAST, PTR>(p, c * kWave + i, r_x[w][i], r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i],
+                                          r_t[w][i], r_hp[w][i], gl, my_edges);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows
@@ -505,7 +569,8 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
 // else 2.
 template <int G, int NB>
 __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint32_t a, uint32_t b, float first,
-                                              float last, float vh, float vl, int gl, uint32_t &lo, uint32_t &hi) {
+                                              float last, float vh, float vl, bool use_ptr, int gl, uint32_t &lo,
+                                              uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     // a non-empty run belongs to a node inside the graph
     const int4 *rec = b > a && b - a <= TGL_NODE_INLINE ? p.nodes + static_cast<int64_t>(x) * 8 : nullptr;
@@ -519,7 +584,14 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
         act[i] = !edge_from_summary(a, b, first, last, v[i], c[i]);
     }
     uint32_t cs[NB];
-    count_below_n<G, NB>(p.tsa, M, p.tsx, p.nx, rec, a, b, v, act, cs, gl);
+    if (use_ptr && !rec && b - a > HeldRun<G>::span) {   // group-uniform: hop 1, saved positions kept
+        int ei[NB];
+#pragma unroll
+        for (int i = 0; i < NB; i++) ei[i] = i;             // hop 1 with one window: edges t and t - D
+        from_pointers<G, NB>(p, x, a, b, ei, v, act, cs, gl);
+    } else {
+        count_below_n<G, NB>(p.tsa, M, p.tsx, p.nx, rec, a, b, v, act, cs, gl);
+    }
     hi = act[0] ? cs[0] : c[0];
     lo = NB == 1 ? a : (act[NB - 1] ? cs[NB - 1] : c[NB - 1]);
     if (lo > hi) lo = hi;
@@ -665,7 +737,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                 const int i = r_need[w][base + gw];
                 uint32_t wlo, whi;
                 locate_window<G, NB>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_vh[w][i],
-                                     NB == 2 ? r_vl[w][i] : 0.0f, gl, wlo, whi);
+                                     NB == 2 ? r_vl[w][i] : 0.0f, FIRST && p.ptr != nullptr, gl, wlo, whi);
                 if (gl == 0) {
                     r_lo[w][i] = wlo;
                     r_n[w][i] = whi - wlo;
@@ -726,11 +798,17 @@ void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t w
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxGrid) blocks = kMaxGrid;
     const unsigned nb = static_cast<unsigned>(blocks);
-    if (multi) {                              // first hop only
+    if (multi && a.ptr) {                     // first hop only; saved window edges kept
         switch (G) {
-            case 16: hop_multi_kernel<16, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
-            case 32: hop_multi_kernel<32, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
-            default: hop_multi_kernel<64, MODE, LAST><<<nb, kBlock, 0, st>>>(a); break;
+            case 16: hop_multi_kernel<16, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_kernel<32, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_kernel<64, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+        }
+    } else if (multi) {                       // first hop only
+        switch (G) {
+            case 16: hop_multi_kernel<16, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_kernel<32, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_kernel<64, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
         }
     } else {
         // the window search uses 8 lanes per root whatever the fanout; one
@@ -762,6 +840,19 @@ int pick_group(int64_t slots_per_root) {
     int g = 16;
     while (g < 64 && g < slots_per_root) g <<= 1;
     return g;
+}
+
+// Saved window edges at the start of every run: pointers[i * N + x] = indptr[x]
+// (clamped into [0, M]).
+__global__ __launch_bounds__(kBlock) void pointers_reset_kernel(const int64_t *__restrict__ indptr, int64_t N,
+                                                                 int64_t M, int64_t n, uint32_t *__restrict__ ptr) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; e < n; e += stride) {
+        const int64_t x = e % N;
+        int64_t a = indptr[x];
+        a = a < 0 ? 0 : (a > M ? M : a);
+        ptr[e] = static_cast<uint32_t>(a);
+    }
 }
 
 constexpr int64_t kCapLimit = int64_t(1) << 62;
@@ -858,6 +949,8 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
     if (!g || !outs || !counts) return TGL_EINVAL;
     const int32_t anchor = opts ? opts->anchor : TGL_ANCHOR_OWN;
     if (anchor != TGL_ANCHOR_OWN && anchor != TGL_ANCHOR_ROOT) return TGL_EINVAL;
+    uint32_t *const pointers = opts ? opts->pointers : nullptr;
+    if ((reinterpret_cast<uintptr_t>(pointers) & 3u) != 0) return TGL_EINVAL;
     if (!sample_args_ok(num_roots, hops, fanouts, num_snapshots)) return TGL_EINVAL;
     if (mode != TGL_MOST_RECENT && mode != TGL_UNIFORM) return TGL_EINVAL;
     if (snapshot_len != snapshot_len || !(snapshot_len > 0.0f)) return TGL_EINVAL;
@@ -912,6 +1005,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         const tgl_hop_out &o = outs[h - 1];
         a.hop = h;
         a.k = k;
+        a.ptr = h == 1 ? pointers : nullptr;
         a.windows = h == 1 ? S : 1;
         a.o_nbr = o.nbr;
         a.o_eid = o.eid;
@@ -961,6 +1055,21 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
     }
     return TGL_OK;
+}
+
+tgl_status tgl_pointers_reset(const tgl_tcsr *g, int32_t num_snapshots, uint32_t *pointers, void *stream) {
+    if (!g || !pointers || num_snapshots < 1 || num_snapshots > TGL_MAX_SNAPSHOTS) return TGL_EINVAL;
+    if (g->num_nodes < 1 || g->num_nodes > INT32_MAX || !g->indptr) return TGL_EINVAL;
+    if (g->num_entries < 0 || g->num_entries > static_cast<int64_t>(UINT32_MAX)) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(pointers) & 3u) != 0) return TGL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    const int64_t n = (static_cast<int64_t>(num_snapshots) + 1) * g->num_nodes;
+    int64_t blocks = (n + kBlock - 1) / kBlock;
+    if (blocks > kMaxGrid) blocks = kMaxGrid;
+    pointers_reset_kernel<<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(g->indptr, g->num_nodes, g->num_entries,
+                                                                          n, pointers);
+    return launch_status();
 }
 
 tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,

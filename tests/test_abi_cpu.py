@@ -216,3 +216,25 @@ def test_sample_ex_rejects_unknown_anchor():
         opts = B.c_sample_opts(anchor, 0)
         assert L.tgl_sample_ex(C.byref(g), FAKE, FAKE, 5, 2, fp, 1, 1, C.c_float(math.inf), C.c_uint64(1),
                                C.c_uint64(0), C.byref(opts), outs, FAKE, FAKE, 1 << 30, None) == B.EINVAL
+
+
+def test_pointers_reset_rejects_invalid_arguments():
+    L = P.lib()
+    g = B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE)
+    assert L.tgl_pointers_reset(None, 1, FAKE, None) == B.EINVAL
+    assert L.tgl_pointers_reset(C.byref(g), 0, FAKE, None) == B.EINVAL
+    assert L.tgl_pointers_reset(C.byref(g), 65, FAKE, None) == B.EINVAL
+    assert L.tgl_pointers_reset(C.byref(g), 1, None, None) == B.EINVAL
+    assert L.tgl_pointers_reset(C.byref(g), 1, FAKE + 2, None) == B.EINVAL
+    bad = B.c_tcsr(0, 100, FAKE, FAKE, FAKE, FAKE)
+    assert L.tgl_pointers_reset(C.byref(bad), 1, FAKE, None) == B.EINVAL
+
+
+def test_sample_ex_rejects_misaligned_pointers():
+    L = P.lib()
+    fa, fp = _fan([10, 10])
+    outs = (B.c_hop_out * 2)(*[B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE) for _ in range(2)])
+    g = B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE)
+    opts = B.c_sample_opts(0, 0, FAKE + 2)
+    assert L.tgl_sample_ex(C.byref(g), FAKE, FAKE, 5, 2, fp, 1, 1, C.c_float(math.inf), C.c_uint64(1),
+                           C.c_uint64(0), C.byref(opts), outs, FAKE, FAKE, 1 << 30, None) == B.EINVAL
