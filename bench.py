@@ -59,6 +59,10 @@ def parse():
                          "f2: time encoding of the sampled slots")
     ap.add_argument("--gather-steps", type=int, default=8,
                     help="f1, f2: sampler steps whose slots are processed in the timed region")
+    ap.add_argument("--consecutive", action="store_true",
+                    help="time consecutive super-batches from the middle of the epoch (warm-up: the ones before)")
+    ap.add_argument("--pointers", action="store_true",
+                    help="hop 1 from saved window edges (Sec. 3.1 pointers), reset before warm-up; implies --consecutive")
     ap.add_argument("--chunk", type=int, default=None,
                     help="f1, f2: slots per launch (default 2^20 for f1, 2^23 for f2)")
     return ap.parse_args()
@@ -462,10 +466,19 @@ def main():
 
     B = args.batches_per_step or {"c2": w.num_batches(), "c3": 64, "c4": 64, "c5": 1}[args.workload]
     B = min(B, w.num_batches())
-    # timed steps are spread evenly over the epoch; warm-up steps sit between them
-    timed_pos = step_positions(w.num_batches(), B, args.steps)
-    span = max(w.num_batches() - B, 1)
-    warm_pos = [(p + max(span // (2 * max(args.steps, 1)), 1)) % span for p in timed_pos[:args.warmup]]
+    if args.consecutive or args.pointers:
+        # consecutive super-batches in chronological order, warm-up steps right before them
+        nsteps = args.warmup + args.steps
+        b0 = max(0, min(w.num_batches() // 2 - (nsteps * B) // 2, w.num_batches() - nsteps * B))
+        if b0 + nsteps * B > w.num_batches():
+            raise SystemExit("--consecutive: the epoch has fewer than %d super-batches of %d batches" % (nsteps, B))
+        warm_pos = [b0 + i * B for i in range(args.warmup)]
+        timed_pos = [b0 + (args.warmup + i) * B for i in range(args.steps)]
+    else:
+        # timed steps are spread evenly over the epoch; warm-up steps sit between them
+        timed_pos = step_positions(w.num_batches(), B, args.steps)
+        span = max(w.num_batches() - B, 1)
+        warm_pos = [(p + max(span // (2 * max(args.steps, 1)), 1)) % span for p in timed_pos[:args.warmup]]
     inputs = {}
     for b in sorted(set(timed_pos + warm_pos)):
         r, t_, base = w.batches(b, b + B)
@@ -476,9 +489,11 @@ def main():
         % (max_roots, sum(x.numel() * x.element_size() for x in
                           smp.nbr + smp.eid + smp.ts + smp.dt + [smp.workspace]) / 1e9))
 
+    ptr = P.pointers_reset(g, w.snapshots) if args.pointers else None
+
     def run(b):
         r, t_, base, n = inputs[b]
-        smp.run(g, r, t_, w.mode, w.snapshot_len, w.sample_seed, base, num_roots=n)
+        smp.run(g, r, t_, w.mode, w.snapshot_len, w.sample_seed, base, num_roots=n, pointers=ptr)
 
     if args.row == "f1":
         measure_gather(args, w, g, smp, run, timed_pos, B, dev)
@@ -562,6 +577,8 @@ def main():
                            w.snapshots, "" if math.isinf(w.snapshot_len) else " of %g" % w.snapshot_len,
                            B, w.batch_edges),
             "roots_per_step": max_roots,
+            "step_order": "consecutive" if (args.consecutive or args.pointers) else "spread over the epoch",
+            "hop1_pointers": bool(args.pointers),
             "neighbours_per_step": nbrs_total / args.steps,
             "slots_per_step": slots_total / args.steps,
             "tcsr_build_ms": build_ms,

@@ -277,6 +277,51 @@ __device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uin
     for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0;
 }
 
+// count_below_n with a range per threshold: out[i] = lo0[i] + #{p in
+// [lo0[i], hi0[i]): ts[p] < v[i]} for each i with act[i] (lo0[i] otherwise),
+// each range a stretch of one sorted run.  Ranges longer than one probe round
+// are narrowed on the search index first when there is one.
+template <int G, int NE>
+__device__ __forceinline__ void count_below_ranges(const float *__restrict__ tsa, uint32_t M,
+                                                   const float *__restrict__ tsx, uint32_t nx,
+                                                   const uint32_t (&lo0)[NE], const uint32_t (&hi0)[NE],
+                                                   const float (&v)[NE], const bool (&act)[NE],
+                                                   uint32_t (&out)[NE], int gl) {
+    constexpr uint32_t X = TGL_INDEX_STRIDE;
+    uint32_t lo[NE], hi[NE];
+    bool any_index = false;
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        const bool use = act[i] && tsx && hi0[i] - lo0[i] > HeldRun<G>::span * (G + 1);
+        const uint32_t ja = lo0[i] / X + (lo0[i] % X != 0);
+        const uint32_t jb = hi0[i] / X + (hi0[i] % X != 0);
+        lo[i] = use ? ja : lo0[i];
+        hi[i] = use ? jb : lo0[i];
+        any_index |= use;
+    }
+    if (any_index) {                                // group-uniform
+        search_n<G, NE>(tsx, nx, lo, hi, v, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            const bool use = act[i] && tsx && hi0[i] - lo0[i] > HeldRun<G>::span * (G + 1);
+            const uint32_t ja = lo0[i] / X + (lo0[i] % X != 0);
+            const uint32_t jb = hi0[i] / X + (hi0[i] % X != 0);
+            const uint32_t r = lo[i];
+            lo[i] = use ? (r > ja ? (r - 1) * X + 1 : lo0[i]) : lo0[i];   // ts[(r-1) X] < v[i]
+            hi[i] = use ? (r < jb ? r * X : hi0[i]) : (act[i] ? hi0[i] : lo0[i]);   // ts[r X] >= v[i]
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            lo[i] = lo0[i];
+            hi[i] = act[i] ? hi0[i] : lo0[i];
+        }
+    }
+    search_n<G, NE>(tsa, M, lo, hi, v, gl);
+#pragma unroll
+    for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0[i];
+}
+
 // Window edges of a long run [a, b) found from saved positions -- the
 // per-node pointers of Section 3.1, kept for hop 1 -- by the G lanes of one
 // group: edge i (threshold v[i]) is first looked for in the held stretch that
@@ -292,13 +337,14 @@ __device__ __forceinline__ void from_pointers(const HopArgs &p, int32_t x, uint3
                                               uint32_t (&out)[NE], int gl) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     constexpr uint32_t span = HeldRun<G>::span;
-    uint32_t lo[NE], hi[NE];
+    uint32_t lo[NE], hi[NE], saved[NE];
 #pragma unroll
     for (int i = 0; i < NE; i++) {
         uint32_t p0 = a;
+        saved[i] = 0;
         if (act[i]) {
-            p0 = p.ptr[static_cast<int64_t>(ei[i]) * p.num_nodes + x];
-            p0 = p0 < a ? a : (p0 > b ? b : p0);
+            saved[i] = p.ptr[static_cast<int64_t>(ei[i]) * p.num_nodes + x];
+            p0 = saved[i] < a ? a : (saved[i] > b ? b : saved[i]);
         }
         lo[i] = p0 > a ? p0 - 1 : a;
         hi[i] = act[i] ? (b - lo[i] > span ? lo[i] + span : b) : lo[i];
@@ -318,15 +364,18 @@ __device__ __forceinline__ void from_pointers(const HopArgs &p, int32_t x, uint3
         any |= fb[i];
     }
     if (any) {                                      // group-uniform
-        search_n<G, NE>(p.tsa, M, flo, fhi, v, gl);
+        uint32_t fo[NE];
+        count_below_ranges<G, NE>(p.tsa, M, p.tsx, p.nx, flo, fhi, v, fb, fo, gl);
 #pragma unroll
         for (int i = 0; i < NE; i++)
-            if (fb[i]) out[i] = flo[i];
+            if (fb[i]) out[i] = fo[i];
     }
+    // raise the saved position only when this edge lies beyond it: roots of a
+    // hot node mostly find it already there, and skip the atomic
     if (gl == 0) {
 #pragma unroll
         for (int i = 0; i < NE; i++)
-            if (act[i]) atomicMax(p.ptr + static_cast<int64_t>(ei[i]) * p.num_nodes + x, out[i]);
+            if (act[i] && out[i] > saved[i]) atomicMax(p.ptr + static_cast<int64_t>(ei[i]) * p.num_nodes + x, out[i]);
     }
 }
 
@@ -567,10 +616,9 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
 // that the run's first and last timestamps decide is not searched.  NB is
 // the number of window edges: 1 when windows are unbounded below (lo = a),
 // else 2.
-template <int G, int NB>
+template <int G, int NB, bool PTR>
 __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint32_t a, uint32_t b, float first,
-                                              float last, float vh, float vl, bool use_ptr, int gl, uint32_t &lo,
-                                              uint32_t &hi) {
+                                              float last, float vh, float vl, int gl, uint32_t &lo, uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     // a non-empty run belongs to a node inside the graph
     const int4 *rec = b > a && b - a <= TGL_NODE_INLINE ? p.nodes + static_cast<int64_t>(x) * 8 : nullptr;
@@ -584,7 +632,7 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
         act[i] = !edge_from_summary(a, b, first, last, v[i], c[i]);
     }
     uint32_t cs[NB];
-    if (use_ptr && !rec && b - a > HeldRun<G>::span) {   // group-uniform: hop 1, saved positions kept
+    if (PTR && !rec && b - a > HeldRun<G>::span) {       // group-uniform: hop 1, saved positions kept
         int ei[NB];
 #pragma unroll
         for (int i = 0; i < NB; i++) ei[i] = i;             // hop 1 with one window: edges t and t - D
@@ -608,8 +656,9 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
 //   phase 3, one lane per slot: selection, gather and emit.  The packed roots
 //     have consecutive indices, so the slots of a chunk are one contiguous
 //     range of the output and the stores coalesce.
-template <int G, int MODE, bool LAST, bool FIRST, int NB>
+template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 7 : 6))) void hop_single_kernel(const HopArgs p) {
+    static_assert(FIRST || !PTR, "saved window edges are kept for hop 1 only");
     constexpr int GPW = kWave / G;            // roots located per wavefront round
     constexpr int U = 4;                      // slots per lane whose loads are in flight together
     const int lane = lane_id();
@@ -736,8 +785,8 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
             if (base + gw < nneed) {                // group-uniform
                 const int i = r_need[w][base + gw];
                 uint32_t wlo, whi;
-                locate_window<G, NB>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_vh[w][i],
-                                     NB == 2 ? r_vl[w][i] : 0.0f, FIRST && p.ptr != nullptr, gl, wlo, whi);
+                locate_window<G, NB, PTR>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_vh[w][i],
+                                          NB == 2 ? r_vl[w][i] : 0.0f, gl, wlo, whi);
                 if (gl == 0) {
                     r_lo[w][i] = wlo;
                     r_n[w][i] = whi - wlo;
@@ -813,12 +862,15 @@ void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t w
     } else {
         // the window search uses 8 lanes per root whatever the fanout; one
         // window edge when windows are unbounded below, else two
+        const bool ptr = first && a.ptr;
         if (a.delta_inf) {
-            if (first) hop_single_kernel<8, MODE, LAST, true, 1><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 1><<<nb, kBlock, 0, st>>>(a);
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 1, false><<<nb, kBlock, 0, st>>>(a);
         } else {
-            if (first) hop_single_kernel<8, MODE, LAST, true, 2><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 2><<<nb, kBlock, 0, st>>>(a);
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 2, true><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 2, false><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 2, false><<<nb, kBlock, 0, st>>>(a);
         }
     }
 }
