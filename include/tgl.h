@@ -309,6 +309,65 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
 tgl_status tgl_pointers_reset(const tgl_tcsr *g, int32_t num_snapshots, uint32_t *pointers, void *stream);
 
 /* ------------------------------------------------------------------------ */
+/* Message-flow-graph blocks of a hop (Algorithm 1, "generate DGL MFGs")    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * One hop's sampled slots as a bipartite block for message passing, in
+ * compressed sparse column form (edges grouped by destination):
+ *   destination nodes  the hop's groups, G of them: hop 1 has one group per
+ *                      (root, window), in root-major order; a later hop one
+ *                      per root;
+ *   edges              the valid slots, E of them, in slot order (a group's
+ *                      valid slots are a prefix of its k slots);
+ *   source nodes       the G destination nodes first, then one node per edge
+ *                      (the sampled neighbour at its edge time: temporal
+ *                      nodes are not merged), so edge e runs from source
+ *                      G + e to its group.
+ * Outputs (device arrays, capacities from groups_cap and k):
+ *   indptr   int64[groups_cap + 1]  edges of group g: [indptr[g], indptr[g+1])
+ *   edge_dst int64[groups_cap * k]  group of each edge, or NULL
+ *   edge_eid int64[groups_cap * k]  edge id
+ *   edge_dt  float[groups_cap * k]  time difference (the slot's dt)
+ *   src_nid  int32[groups_cap * (k + 1)]  node of each source node
+ *   src_ts   float[groups_cap * (k + 1)]  time of each source node
+ *   sizes    int64[2]               G and E, written on the device
+ * Only the first G + 1, E and G + E entries are written.
+ */
+typedef struct tgl_mfg {
+    int64_t *indptr;
+    int64_t *edge_dst;
+    int64_t *edge_eid;
+    float *edge_dt;
+    int32_t *src_nid;
+    float *src_ts;
+    int64_t *sizes;
+} tgl_mfg;
+
+/* Workspace bytes for tgl_mfg_export with at most groups_cap groups (0 for a
+ * negative count). */
+size_t tgl_mfg_workspace(int64_t groups_cap);
+
+/*
+ * Builds the block of one hop from tgl_sample's outputs.
+ *   hop        [host] the hop's tgl_hop_out (nbr, eid, ts, dt; parent for hop >= 2)
+ *   prev       [host] the previous hop's tgl_hop_out (hop >= 2), or NULL for hop 1
+ *   roots, root_ts  [device] the call's roots (hop 1: destination nodes); both
+ *              NULL is accepted for a call with no roots (they are read only
+ *              for groups below count * windows)
+ *   count      [device] int64: roots of this hop (counts[h] of tgl_sample)
+ *   windows    S for hop 1, 1 for a later hop
+ *   k          the hop's fanout, in [1, TGL_MAX_FANOUT]
+ *   groups_cap upper bound of count * windows (the output capacities)
+ * Never synchronises.  Errors: TGL_EINVAL, TGL_ENOSPACE (workspace),
+ * TGL_EDEVICE.
+ */
+tgl_status tgl_mfg_export(const tgl_hop_out *hop, const tgl_hop_out *prev, const int32_t *roots,
+                          const float *root_ts, const int64_t *count, int32_t windows, int32_t k,
+                          int64_t groups_cap, const tgl_mfg *out, void *workspace, size_t workspace_bytes,
+                          void *stream);
+
+/* ------------------------------------------------------------------------ */
 /* Feature / state gather for sampled slots (Figure 2, steps 2 and 3)       */
 /* ------------------------------------------------------------------------ */
 
@@ -399,7 +458,8 @@ tgl_status tgl_time_encode(const float *dt, int64_t n, const int64_t *count, int
 #define TGL_TIMER_BUILD   3  /* whole tgl_tcsr_build                          */
 #define TGL_TIMER_GATHER  4  /* tgl_gather                                    */
 #define TGL_TIMER_TIMEENC 5  /* tgl_time_encode                               */
-#define TGL_TIMER_KINDS   6
+#define TGL_TIMER_MFG     6  /* tgl_mfg_export                                */
+#define TGL_TIMER_KINDS   7
 
 /*
  * Starts recording HIP events around every kernel of the kinds above, on the

@@ -37,7 +37,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
            "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
-           "tgl_sample_ex", "tgl_pointers_reset",
+           "tgl_sample_ex", "tgl_pointers_reset", "tgl_mfg_workspace", "tgl_mfg_export",
            "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
 
@@ -64,6 +64,12 @@ class c_sample_opts(C.Structure):
 
 
 ANCHORS = {"own": 0, "root": 1, 0: 0, 1: 1}
+
+
+class c_mfg(C.Structure):
+    _fields_ = [("indptr", C.c_void_p), ("edge_dst", C.c_void_p), ("edge_eid", C.c_void_p),
+                ("edge_dt", C.c_void_p), ("src_nid", C.c_void_p), ("src_ts", C.c_void_p),
+                ("sizes", C.c_void_p)]
 
 
 class c_hop_out(C.Structure):
@@ -108,6 +114,11 @@ def lib() -> C.CDLL:
                                 C.POINTER(c_sample_opts), C.POINTER(c_hop_out), P, P, C.c_size_t, P]
     L.tgl_pointers_reset.restype = i32
     L.tgl_pointers_reset.argtypes = [C.POINTER(c_tcsr), i32, P, P]
+    L.tgl_mfg_workspace.restype = C.c_size_t
+    L.tgl_mfg_workspace.argtypes = [i64]
+    L.tgl_mfg_export.restype = i32
+    L.tgl_mfg_export.argtypes = [C.POINTER(c_hop_out), C.POINTER(c_hop_out), P, P, P, i32, i32, i64,
+                                 C.POINTER(c_mfg), P, C.c_size_t, P]
     L.tgl_gather.restype = i32
     L.tgl_gather.argtypes = [P, P, i64, P, i64, C.POINTER(c_table), i32, P]
     L.tgl_time_encode.restype = i32
@@ -356,6 +367,56 @@ class Sampler:
             out.append(Hop(self.nbr[h][:n], self.eid[h][:n], self.ts[h][:n], self.dt[h][:n],
                            None if h == 0 else self.parent[h][:nr], nr))
         return out
+
+
+@dataclass
+class MFG:
+    """One hop's block (Alg. 1, "generate DGL MFGs") in CSC form, at capacity:
+    the first G + 1 entries of ``indptr``, E of the edge arrays and G + E of
+    the source arrays are valid, with (G, E) in the device tensor ``sizes``.
+    Edge e runs from source node G + e to destination group ``edge_dst[e]``;
+    source nodes 0..G-1 are the destination groups themselves."""
+    indptr: torch.Tensor
+    edge_dst: torch.Tensor
+    edge_eid: torch.Tensor
+    edge_dt: torch.Tensor
+    src_nid: torch.Tensor
+    src_ts: torch.Tensor
+    sizes: torch.Tensor
+
+    def sliced(self) -> "MFG":
+        """The valid parts (synchronises to read the sizes)."""
+        G, E = (int(v) for v in self.sizes.cpu().tolist())
+        return MFG(self.indptr[:G + 1], self.edge_dst[:E], self.edge_eid[:E], self.edge_dt[:E],
+                   self.src_nid[:G + E], self.src_ts[:G + E], self.sizes)
+
+
+def mfg_export(smp: "Sampler", h: int, roots: torch.Tensor, root_ts: torch.Tensor, stream=None) -> MFG:
+    """Block of hop ``h`` (0-based) of the sampler's last call, built on the
+    device from its outputs without synchronising."""
+    L = lib()
+    windows = smp.snapshots if h == 0 else 1
+    k = smp.fanouts[h]
+    gcap = smp.caps[h] * windows
+    dev = smp.counts.device
+    m = MFG(torch.empty(gcap + 1, dtype=torch.int64, device=dev),
+            torch.empty(max(gcap * k, 1), dtype=torch.int64, device=dev),
+            torch.empty(max(gcap * k, 1), dtype=torch.int64, device=dev),
+            torch.empty(max(gcap * k, 1), dtype=torch.float32, device=dev),
+            torch.empty(max(gcap * (k + 1), 1), dtype=torch.int32, device=dev),
+            torch.empty(max(gcap * (k + 1), 1), dtype=torch.float32, device=dev),
+            torch.zeros(2, dtype=torch.int64, device=dev))
+    ws_bytes = int(L.tgl_mfg_workspace(gcap))
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    out = c_mfg(m.indptr.data_ptr(), m.edge_dst.data_ptr(), m.edge_eid.data_ptr(), m.edge_dt.data_ptr(),
+                m.src_nid.data_ptr(), m.src_ts.data_ptr(), m.sizes.data_ptr())
+    prev = C.byref(smp._outs[h - 1]) if h > 0 else None
+    s = L.tgl_mfg_export(C.byref(smp._outs[h]), prev, _p(roots), _p(root_ts),
+                         smp.counts.data_ptr() + 8 * h, windows, k, gcap, C.byref(out), _p(ws), ws.numel(),
+                         _stream(stream))
+    _check(s, "tgl_mfg_export")
+    m._ws = ws          # keep the workspace alive until the stream has used it
+    return m
 
 
 def pointers_reset(g: TCSR, snapshots: int = 1, pointers: Optional[torch.Tensor] = None,

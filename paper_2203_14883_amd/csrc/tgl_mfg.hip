@@ -1,0 +1,181 @@
+// tgl_mfg.hip -- one hop's sampled slots as a message-flow-graph block in
+// compressed sparse column form (Algorithm 1 of TGL ends every layer with
+// "generate DGL MFGs"; the sampler breakdown of Section 4 counts that step as
+// "Oth.").
+//
+// The block is a relabelling of the slot arrays: destinations are the hop's
+// groups, edges its valid slots, sources the destinations followed by one
+// temporal node per edge.  Its one non-local quantity is each group's first
+// edge, the exclusive scan of the per-group valid counts, so the export is
+// four short passes that never leave the device: the group count, per-group
+// valid counts (with the destination nodes), the scan, and the scatter of the
+// valid slots.  A group's valid slots are a prefix of its k slots (tgl_sample
+// fills a group newest-first or all-or-nothing); slots after a group's first
+// PAD are not exported.
+#include "tgl_internal.hpp"
+
+namespace tgl {
+namespace {
+
+// sizes[0] = G = min(count * windows, cap)
+__global__ void mfg_groups_kernel(const int64_t *__restrict__ count, int64_t windows, int64_t cap,
+                                  int64_t *__restrict__ sizes) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        int64_t c = *count;
+        c = c < 0 ? 0 : c;
+        sizes[0] = c > cap / windows ? cap : c * windows;
+    }
+}
+
+// Per group: length of its valid prefix, and its destination node (hop 1:
+// the root of the group; later hops: the previous hop's slot it came from).
+__global__ __launch_bounds__(kBlock) void mfg_count_kernel(const int32_t *__restrict__ nbr, int32_t k,
+                                                           const int32_t *__restrict__ roots,
+                                                           const float *__restrict__ root_ts, int32_t windows,
+                                                           const int32_t *__restrict__ prev_nbr,
+                                                           const float *__restrict__ prev_ts,
+                                                           const int64_t *__restrict__ parent,
+                                                           const int64_t *__restrict__ sizes,
+                                                           int32_t *__restrict__ cnt, int32_t *__restrict__ src_nid,
+                                                           float *__restrict__ src_ts) {
+    const int64_t G = sizes[0];
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; g < G; g += stride) {
+        const int32_t *s = nbr + g * k;
+        int32_t c = 0;
+        while (c < k && s[c] >= 0) c++;
+        cnt[g] = c;
+        if (prev_nbr) {
+            const int64_t p = parent[g];
+            src_nid[g] = prev_nbr[p];
+            src_ts[g] = prev_ts[p];
+        } else if (roots) {
+            const int64_t r = g / windows;
+            src_nid[g] = roots[r];
+            src_ts[g] = root_ts[r];
+        } else {                                    // no roots given for a positive count: PAD-like
+            src_nid[g] = -1;
+            src_ts[g] = -1.0f;
+        }
+    }
+}
+
+// indptr[G] = E
+__global__ void mfg_close_kernel(const int64_t *__restrict__ sizes, int64_t *__restrict__ indptr) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) indptr[sizes[0]] = sizes[1];
+}
+
+// One thread per slot i = g * k + j of the G groups: valid slot j < cnt[g]
+// becomes edge indptr[g] + j and source node G + that edge.  I is the index
+// type (32-bit when the slot capacity allows it).
+template <class I>
+__global__ __launch_bounds__(kBlock) void mfg_scatter_kernel(const int32_t *__restrict__ nbr,
+                                                             const int64_t *__restrict__ eid,
+                                                             const float *__restrict__ ts,
+                                                             const float *__restrict__ dt, int32_t k,
+                                                             const int64_t *__restrict__ sizes,
+                                                             const int32_t *__restrict__ cnt,
+                                                             const int64_t *__restrict__ indptr,
+                                                             int64_t *__restrict__ edge_dst,
+                                                             int64_t *__restrict__ edge_eid,
+                                                             float *__restrict__ edge_dt, int32_t *__restrict__ src_nid,
+                                                             float *__restrict__ src_ts) {
+    const int64_t G = sizes[0];
+    const I total = static_cast<I>(G) * static_cast<I>(k);
+    const I kk = static_cast<I>(k);
+    const I stride = static_cast<I>(gridDim.x) * kBlock;
+    for (I i = static_cast<I>(blockIdx.x) * kBlock + threadIdx.x; i < total; i += stride) {
+        const I g = i / kk;
+        const I j = i - g * kk;
+        if (static_cast<int32_t>(j) >= cnt[g]) continue;
+        const int64_t e = indptr[g] + static_cast<int64_t>(j);
+        if (edge_dst) edge_dst[e] = static_cast<int64_t>(g);
+        edge_eid[e] = eid[i];
+        edge_dt[e] = dt[i];
+        src_nid[G + e] = nbr[i];
+        src_ts[G + e] = ts[i];
+    }
+}
+
+struct MfgWs {
+    int32_t *cnt = nullptr;
+    int64_t *partials = nullptr;
+    size_t bytes = 0;
+};
+
+MfgWs carve_mfg_ws(void *base, int64_t groups_cap) {
+    MfgWs w;
+    Carver cv(base);
+    w.cnt = cv.take<int32_t>(static_cast<size_t>(groups_cap > 0 ? groups_cap : 1));
+    w.partials = cv.take<int64_t>(static_cast<size_t>(scan_tiles(groups_cap) + 1));
+    w.bytes = cv.size();
+    return w;
+}
+
+unsigned grid_of(int64_t n) {
+    int64_t b = (n + kBlock - 1) / kBlock;
+    if (b < 1) b = 1;
+    if (b > (1 << 16)) b = 1 << 16;
+    return static_cast<unsigned>(b);
+}
+
+}  // namespace
+}  // namespace tgl
+
+using namespace tgl;
+
+extern "C" {
+
+size_t tgl_mfg_workspace(int64_t groups_cap) {
+    if (groups_cap < 0) return 0;
+    return carve_mfg_ws(nullptr, groups_cap).bytes;
+}
+
+tgl_status tgl_mfg_export(const tgl_hop_out *hop, const tgl_hop_out *prev, const int32_t *roots,
+                          const float *root_ts, const int64_t *count, int32_t windows, int32_t k,
+                          int64_t groups_cap, const tgl_mfg *out, void *workspace, size_t workspace_bytes,
+                          void *stream) {
+    if (!hop || !out || !count) return TGL_EINVAL;
+    if (windows < 1 || windows > TGL_MAX_SNAPSHOTS || k < 1 || k > TGL_MAX_FANOUT) return TGL_EINVAL;
+    if (groups_cap < 0 || groups_cap > (int64_t(1) << 62) / (k + 1)) return TGL_EINVAL;
+    if (!out->indptr || !out->sizes) return TGL_EINVAL;
+    if (groups_cap > 0) {
+        if (!hop->nbr || !hop->eid || !hop->ts || !hop->dt) return TGL_EINVAL;
+        if (!out->edge_eid || !out->edge_dt || !out->src_nid || !out->src_ts) return TGL_EINVAL;
+        // roots are read only for groups below count * windows, a device value:
+        // they may be NULL when the call had no roots
+        if (prev && (!prev->nbr || !prev->ts || !hop->parent)) return TGL_EINVAL;
+        if (!prev && (!roots) != (!root_ts)) return TGL_EINVAL;
+    }
+    if (prev && windows != 1) return TGL_EINVAL;
+    const MfgWs need = carve_mfg_ws(nullptr, groups_cap);
+    if (!workspace || workspace_bytes < need.bytes) return TGL_ENOSPACE;
+    const MfgWs ws = carve_mfg_ws(workspace, groups_cap);
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    ScopedTimer tm(TGL_TIMER_MFG, st);
+    mfg_groups_kernel<<<1, 64, 0, st>>>(count, windows, groups_cap, out->sizes);
+    mfg_count_kernel<<<grid_of(groups_cap), kBlock, 0, st>>>(
+        hop->nbr, k, roots, root_ts, windows, prev ? prev->nbr : nullptr, prev ? prev->ts : nullptr,
+        prev ? hop->parent : nullptr, out->sizes, ws.cnt, out->src_nid, out->src_ts);
+    const int64_t tiles = scan_tiles(groups_cap) > 0 ? scan_tiles(groups_cap) : 1;
+    scan_reduce_kernel<int32_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(ws.cnt, groups_cap, out->sizes,
+                                                                                  ws.partials);
+    launch_scan_partials(ws.partials, tiles, out->sizes + 1, st);
+    scan_apply_kernel<int32_t, int64_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
+        ws.cnt, out->indptr, groups_cap, out->sizes, ws.partials);
+    mfg_close_kernel<<<1, 64, 0, st>>>(out->sizes, out->indptr);
+    const int64_t slots = groups_cap * k;
+    if (slots < (int64_t(1) << 32) - kBlock * 65536ll)
+        mfg_scatter_kernel<uint32_t><<<grid_of(slots), kBlock, 0, st>>>(
+            hop->nbr, hop->eid, hop->ts, hop->dt, k, out->sizes, ws.cnt, out->indptr, out->edge_dst, out->edge_eid,
+            out->edge_dt, out->src_nid, out->src_ts);
+    else
+        mfg_scatter_kernel<uint64_t><<<grid_of(slots), kBlock, 0, st>>>(
+            hop->nbr, hop->eid, hop->ts, hop->dt, k, out->sizes, ws.cnt, out->indptr, out->edge_dst, out->edge_eid,
+            out->edge_dt, out->src_nid, out->src_ts);
+    return launch_status();
+}
+
+}  // extern "C"

@@ -158,7 +158,7 @@ def test_index_len():
 def test_timer_argument_checks():
     L = P.lib()
     ms, n = C.c_double(), C.c_int64()
-    assert L.tgl_timer_read(6, C.byref(ms), C.byref(n)) == B.EINVAL
+    assert L.tgl_timer_read(7, C.byref(ms), C.byref(n)) == B.EINVAL
     assert L.tgl_timer_read(-1, C.byref(ms), C.byref(n)) == B.EINVAL
     assert L.tgl_timer_read(0, None, C.byref(n)) == B.EINVAL
     assert L.tgl_timer_enable(0) == B.EINVAL
@@ -238,3 +238,27 @@ def test_sample_ex_rejects_misaligned_pointers():
     opts = B.c_sample_opts(0, 0, FAKE + 2)
     assert L.tgl_sample_ex(C.byref(g), FAKE, FAKE, 5, 2, fp, 1, 1, C.c_float(math.inf), C.c_uint64(1),
                            C.c_uint64(0), C.byref(opts), outs, FAKE, FAKE, 1 << 30, None) == B.EINVAL
+
+
+def test_mfg_argument_checks():
+    L = P.lib()
+    assert L.tgl_mfg_workspace(-1) == 0 and L.tgl_mfg_workspace(10) > 0
+    hop = B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE)
+    out = B.c_mfg(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)
+
+    def call(hop_=hop, prev=None, roots=FAKE, rts=FAKE, count=FAKE, windows=1, k=10, cap=100, out_=out,
+             ws=FAKE, ws_bytes=1 << 30):
+        return L.tgl_mfg_export(C.byref(hop_) if hop_ is not None else None,
+                                C.byref(prev) if prev is not None else None, roots, rts, count, windows, k, cap,
+                                C.byref(out_) if out_ is not None else None, ws, ws_bytes, None)
+    for kw in [dict(hop_=None), dict(out_=None), dict(count=None), dict(windows=0), dict(windows=65), dict(k=0),
+               dict(k=1025), dict(cap=-1), dict(roots=None), dict(rts=None, roots=FAKE),
+               dict(out_=B.c_mfg(FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE)),
+               dict(out_=B.c_mfg(None, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE)),
+               dict(hop_=B.c_hop_out(FAKE, None, FAKE, FAKE, FAKE)),
+               dict(prev=B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE), windows=2),
+               dict(prev=B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE), hop_=B.c_hop_out(FAKE, FAKE, FAKE, FAKE, None))]:
+        assert call(**kw) == B.EINVAL, kw
+    assert call(ws_bytes=8) == B.ENOSPACE
+    assert call(roots=None, rts=None, ws_bytes=8) == B.ENOSPACE   # no roots: accepted up to the workspace
+    assert call(ws=None) == B.ENOSPACE
