@@ -54,9 +54,9 @@ def parse():
                     help="first run a plain 4 GiB device copy (for scaling byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--small", action="store_true", help="reduced graph size (development only)")
-    ap.add_argument("--row", default="sample", choices=["sample", "f1", "f2"],
+    ap.add_argument("--row", default="sample", choices=["sample", "f1", "f2", "f4"],
                     help="sample: the sampler step (default); f1: node-feature lookup of the sampled slots; "
-                         "f2: time encoding of the sampled slots")
+                         "f2: time encoding of the sampled slots; f4: MFG block export of the sampled hops")
     ap.add_argument("--gather-steps", type=int, default=8,
                     help="f1, f2: sampler steps whose slots are processed in the timed region")
     ap.add_argument("--consecutive", action="store_true",
@@ -401,6 +401,128 @@ def measure_timeenc(args, w, smp, run, timed_pos, B, dev):
     print(json.dumps(line), flush=True)
 
 
+MFG_METRIC = "exported MFG edges/sec (CSC blocks of every hop of the sampler step) + achieved HBM GB/s vs peak"
+
+
+def measure_mfg(args, w, smp, run, inputs, timed_pos, B, dev):
+    """Row f4: the MFG blocks (Alg. 1, "generate DGL MFGs") of every hop of
+    sampler steps, exported on the device; only the export kernels are timed
+    (HIP events around each export).  Algorithmic bytes per hop: per slot its
+    nbr read; per group its valid count written and read, its indptr entry
+    and destination node written (and, after hop 1, its parent and the
+    parent slot's node and time read); per edge the slot's eid, ts, dt read
+    and the edge's dst, eid, dt and source node and time written."""
+    import torch
+    import paper_2203_14883_amd as P
+    from oracle import mfg as M
+
+    steps = timed_pos[:max(args.gather_steps, 1)]
+    run(steps[0])
+    r, t_, _, _ = inputs[steps[0]]
+    for h in range(len(w.fanouts)):
+        P.mfg_export(smp, h, r, t_)                  # warm-up
+    torch.cuda.synchronize()
+    P.timer_reset()
+    alg = 0.0
+    nedges = 0
+    launches = 0
+    blocks = None
+    for b in steps:
+        run(b)
+        r, t_, _, _ = inputs[b]
+        blocks = [P.mfg_export(smp, h, r, t_) for h in range(len(w.fanouts))]
+        hs = smp.hops()                              # syncs: sizes for the byte count
+        for h, (hop, blk) in enumerate(zip(hs, blocks)):
+            G, E = (int(v) for v in blk.sizes.cpu().tolist())
+            slots = hop.nbr.numel()
+            alg += slots * 4 + G * (4 + 4 + 8 + 8) + (G * (8 + 8) if h else 0) + E * (16 + 8 + 8 + 4 + 4 + 4)
+            nedges += E
+            launches += 1
+    k_ms, k_n = P.timer_read(P.binding.TIMER_MFG)
+    achieved = alg / (k_ms * 1e-3) / 1e9
+    value = nedges / (k_ms * 1e-3)
+    log("f4: %d exports, %d edges: kernels %.2f ms; %.3g edges/s; %.1f GB/s algorithmic"
+        % (k_n, nedges, k_ms, value, achieved))
+
+    # properties of the last step's blocks that hold at any size
+    hs = smp.hops()
+    for h, (hop, blk) in enumerate(zip(hs, blocks)):
+        s = blk.sliced()
+        G, E = (int(v) for v in s.sizes.cpu().tolist())
+        valid = hop.nbr >= 0
+        ok = E == int(valid.sum()) and int(s.indptr[-1]) == E and bool((s.indptr[1:] >= s.indptr[:-1]).all())
+        pick = torch.from_numpy(np.random.default_rng(h).choice(E, min(E, 4096), replace=False)).to(dev) if E else None
+        if ok and E:
+            src_t = s.src_ts[G + pick].double()
+            dst_t = s.src_ts[s.edge_dst[pick]].double()
+            ok = bool((src_t < dst_t).all())
+            slot_idx = torch.nonzero(valid).flatten()[pick]
+            ok = ok and torch.equal(s.edge_eid[pick], hop.eid[slot_idx]) and torch.equal(s.src_nid[G + pick], hop.nbr[slot_idx])
+        if not ok:
+            raise SystemExit("f4: block of hop %d fails its invariants" % (h + 1))
+    log("f4: blocks of the last step satisfy the size, order and slot invariants")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        # oracle block of hop 2 of a bounded sample: the first 2^20 hop-2 groups' slots of the last step,
+        # given as host arrays (their values are not checked here, only the oracle's time is taken)
+        hop = hs[-1]
+        k = w.fanouts[-1]
+        ng = min(hop.num_roots, 1 << 20)
+
+        class _H:
+            pass
+        hh = _H()
+        hh.nbr, hh.eid = hop.nbr[:ng * k].cpu().numpy(), hop.eid[:ng * k].cpu().numpy()
+        hh.ts, hh.dt = hop.ts[:ng * k].cpu().numpy(), hop.dt[:ng * k].cpu().numpy()
+        hh.parent, hh.num_roots = hop.parent[:ng].cpu().numpy(), ng
+        pp = _H()
+        pp.nbr, pp.ts = hs[-2].nbr.cpu().numpy(), hs[-2].ts.cpu().numpy()
+        t = time.perf_counter()
+        out = M.block(hh, pp, None, None, 1, k)
+        dt_ = time.perf_counter() - t
+        cpu = dict(value=out["E"] / dt_, unit="edges/s", cores=1, kind="oracle",
+                   sample="hop-2 block of the first %d groups of one c4 step (%d edges), %.2f s single-threaded (numpy)"
+                          % (ng, out["E"], dt_))
+        log("f4 CPU oracle: %.3g edges/s (%s)" % (cpu["value"], cpu["sample"]))
+    khash = kernel_source_hash(("tgl_internal.hpp", "tgl_mfg.hip"))
+    line = {
+        "metric": MFG_METRIC,
+        "value": value,
+        "unit": "edges/s",
+        "n_gpus": 1,
+        "steps": len(steps),
+        "warmup": 1,
+        "ms_per_step": k_ms / len(steps),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int64",
+        "data": "synthetic",
+        "config": {
+            "workload": "%s: MFG blocks (CSC) of every hop of %d sampler steps (%d-hop %s %s, %d batches of %d edges "
+                        "x 3 roots per step)" % (w.name, len(steps), len(w.fanouts), w.mode,
+                                                 "x".join(map(str, w.fanouts)), B, w.batch_edges),
+            "edges_per_step": nedges / len(steps),
+        },
+        "roofline": {
+            "kernel": "tgl_mfg_export (count, scan, scatter)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": achieved / PEAK_HBM_GBS,
+            "traffic": read_traffic(khash, w.name, "mfg_export"),
+            "algorithmic_bytes_per_launch": alg / max(launches, 1),
+            "avg_launch_ms": k_ms / max(k_n, 1),
+            "kernel_source_hash": khash,
+        },
+        "cpu_baseline": cpu,
+    }
+    P.timer_disable()
+    print(json.dumps(line), flush=True)
+
+
 def copy_calibration(dev, gib=4, reps=3):
     """A plain device copy of known size, so byte counters can be scaled."""
     import torch
@@ -500,6 +622,9 @@ def main():
         return
     if args.row == "f2":
         measure_timeenc(args, w, smp, run, timed_pos, B, dev)
+        return
+    if args.row == "f4":
+        measure_mfg(args, w, smp, run, inputs, timed_pos, B, dev)
         return
 
     for b in warm_pos:

@@ -22,7 +22,7 @@ OK, EINVAL, ERANGE, ENOSPACE, EDEVICE = 0, -1, -2, -3, -4
 MOST_RECENT, UNIFORM = 0, 1
 BUILD_UNDIRECTED = 1
 MAX_HOPS, MAX_FANOUT, MAX_SNAPSHOTS = 8, 1024, 64
-TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD, TIMER_GATHER, TIMER_TIMEENC = 0, 1, 2, 3, 4, 5
+TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD, TIMER_GATHER, TIMER_TIMEENC, TIMER_MFG = 0, 1, 2, 3, 4, 5, 6
 OUT_F32, OUT_BF16 = 0, 1
 KEY_NODE, KEY_EDGE = 0, 1
 MAX_TABLES = 8
