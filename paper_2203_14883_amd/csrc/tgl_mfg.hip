@@ -7,9 +7,10 @@
 // groups, edges its valid slots, sources the destinations followed by one
 // temporal node per edge.  Its one non-local quantity is each group's first
 // edge, the exclusive scan of the per-group valid counts, so the export is
-// four short passes that never leave the device: the group count, per-group
-// valid counts (with the destination nodes), the scan, and the scatter of the
-// valid slots.  A group's valid slots are a prefix of its k slots (tgl_sample
+// four passes that never leave the device: per-group valid counts (with the
+// destination nodes) and their totals per tile of kScanTile groups, the scan
+// of the tile totals, each group's first edge (indptr), and a copy of the
+// valid slots, one thread per slot.  A group's valid slots are a prefix of its k slots (tgl_sample
 // fills a group newest-first or all-or-nothing); slots after a group's first
 // PAD are not exported.
 #include "tgl_internal.hpp"
@@ -17,34 +18,54 @@
 namespace tgl {
 namespace {
 
-// sizes[0] = G = min(count * windows, cap)
-__global__ void mfg_groups_kernel(const int64_t *__restrict__ count, int64_t windows, int64_t cap,
-                                  int64_t *__restrict__ sizes) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-        int64_t c = *count;
-        c = c < 0 ? 0 : c;
-        sizes[0] = c > cap / windows ? cap : c * windows;
-    }
+// G = min(count * windows, cap), from the device count
+__device__ __forceinline__ int64_t mfg_groups(const int64_t *count, int64_t windows, int64_t cap) {
+    int64_t c = *count;
+    c = c < 0 ? 0 : c;
+    return c > cap / windows ? cap : c * windows;
 }
 
-// Per group: length of its valid prefix, and its destination node (hop 1:
-// the root of the group; later hops: the previous hop's slot it came from).
+// Pass 1, one tile of kScanTile groups per block, thread t owning groups
+// tile + t, tile + t + 256, ... (neighbouring lanes, neighbouring groups):
+// each group's valid prefix length and its destination node (hop 1: the
+// group's root; later hops: the previous hop's slot it came from), and the
+// tile's edge total.
 __global__ __launch_bounds__(kBlock) void mfg_count_kernel(const int32_t *__restrict__ nbr, int32_t k,
                                                            const int32_t *__restrict__ roots,
                                                            const float *__restrict__ root_ts, int32_t windows,
                                                            const int32_t *__restrict__ prev_nbr,
                                                            const float *__restrict__ prev_ts,
                                                            const int64_t *__restrict__ parent,
-                                                           const int64_t *__restrict__ sizes,
-                                                           int32_t *__restrict__ cnt, int32_t *__restrict__ src_nid,
-                                                           float *__restrict__ src_ts) {
-    const int64_t G = sizes[0];
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t g = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; g < G; g += stride) {
-        const int32_t *s = nbr + g * k;
+                                                           const int64_t *__restrict__ count, int64_t cap,
+                                                           int64_t *__restrict__ sizes, int32_t *__restrict__ cnt,
+                                                           int64_t *__restrict__ partials,
+                                                           int32_t *__restrict__ src_nid, float *__restrict__ src_ts) {
+    __shared__ int64_t lds[kBlock / kWave];
+    const int64_t G = mfg_groups(count, windows, cap);
+    if (blockIdx.x == 0 && threadIdx.x == 0) sizes[0] = G;
+    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kScanTile;
+    int64_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; i++) {
+        const int64_t g = tile0 + i * kBlock + threadIdx.x;
+        if (g >= G) continue;
+        // valid prefix length: slots are read eight at a time, all in flight,
+        // and the first PAD among them ends the prefix
+        const int32_t *sl = nbr + g * k;
         int32_t c = 0;
-        while (c < k && s[c] >= 0) c++;
+        for (int32_t j0 = 0; j0 < k; j0 += 8) {
+            int32_t v[8];
+#pragma unroll
+            for (int u = 0; u < 8; u++) v[u] = j0 + u < k ? sl[j0 + u] : -1;
+            int32_t run = 8;
+#pragma unroll
+            for (int u = 7; u >= 0; u--)
+                if (v[u] < 0) run = u;
+            c += run;
+            if (run < 8) break;
+        }
         cnt[g] = c;
+        sum += c;
         if (prev_nbr) {
             const int64_t p = parent[g];
             src_nid[g] = prev_nbr[p];
@@ -58,16 +79,15 @@ __global__ __launch_bounds__(kBlock) void mfg_count_kernel(const int32_t *__rest
             src_ts[g] = -1.0f;
         }
     }
+    int64_t total;
+    block_exclusive_sum<int64_t>(sum, lds, &total);
+    if (threadIdx.x == 0) partials[blockIdx.x] = total;
 }
 
-// indptr[G] = E
-__global__ void mfg_close_kernel(const int64_t *__restrict__ sizes, int64_t *__restrict__ indptr) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) indptr[sizes[0]] = sizes[1];
-}
-
-// One thread per slot i = g * k + j of the G groups: valid slot j < cnt[g]
-// becomes edge indptr[g] + j and source node G + that edge.  I is the index
-// type (32-bit when the slot capacity allows it).
+// Pass 4, one thread per slot i = g * k + j of the G groups: valid slot
+// j < cnt[g] becomes edge indptr[g] + j and source node G + that edge.  I is
+// the index type (32-bit when the slot capacity allows it).  Also closes
+// indptr with indptr[G] = E.
 template <class I>
 __global__ __launch_bounds__(kBlock) void mfg_scatter_kernel(const int32_t *__restrict__ nbr,
                                                              const int64_t *__restrict__ eid,
@@ -75,12 +95,13 @@ __global__ __launch_bounds__(kBlock) void mfg_scatter_kernel(const int32_t *__re
                                                              const float *__restrict__ dt, int32_t k,
                                                              const int64_t *__restrict__ sizes,
                                                              const int32_t *__restrict__ cnt,
-                                                             const int64_t *__restrict__ indptr,
+                                                             int64_t *__restrict__ indptr,
                                                              int64_t *__restrict__ edge_dst,
                                                              int64_t *__restrict__ edge_eid,
                                                              float *__restrict__ edge_dt, int32_t *__restrict__ src_nid,
                                                              float *__restrict__ src_ts) {
     const int64_t G = sizes[0];
+    if (blockIdx.x == 0 && threadIdx.x == 0) indptr[G] = sizes[1];
     const I total = static_cast<I>(G) * static_cast<I>(k);
     const I kk = static_cast<I>(k);
     const I stride = static_cast<I>(gridDim.x) * kBlock;
@@ -97,6 +118,13 @@ __global__ __launch_bounds__(kBlock) void mfg_scatter_kernel(const int32_t *__re
     }
 }
 
+unsigned grid_of(int64_t n) {
+    int64_t b = (n + kBlock - 1) / kBlock;
+    if (b < 1) b = 1;
+    if (b > (1 << 16)) b = 1 << 16;
+    return static_cast<unsigned>(b);
+}
+
 struct MfgWs {
     int32_t *cnt = nullptr;
     int64_t *partials = nullptr;
@@ -110,13 +138,6 @@ MfgWs carve_mfg_ws(void *base, int64_t groups_cap) {
     w.partials = cv.take<int64_t>(static_cast<size_t>(scan_tiles(groups_cap) + 1));
     w.bytes = cv.size();
     return w;
-}
-
-unsigned grid_of(int64_t n) {
-    int64_t b = (n + kBlock - 1) / kBlock;
-    if (b < 1) b = 1;
-    if (b > (1 << 16)) b = 1 << 16;
-    return static_cast<unsigned>(b);
 }
 
 }  // namespace
@@ -155,17 +176,13 @@ tgl_status tgl_mfg_export(const tgl_hop_out *hop, const tgl_hop_out *prev, const
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     ScopedTimer tm(TGL_TIMER_MFG, st);
-    mfg_groups_kernel<<<1, 64, 0, st>>>(count, windows, groups_cap, out->sizes);
-    mfg_count_kernel<<<grid_of(groups_cap), kBlock, 0, st>>>(
-        hop->nbr, k, roots, root_ts, windows, prev ? prev->nbr : nullptr, prev ? prev->ts : nullptr,
-        prev ? hop->parent : nullptr, out->sizes, ws.cnt, out->src_nid, out->src_ts);
     const int64_t tiles = scan_tiles(groups_cap) > 0 ? scan_tiles(groups_cap) : 1;
-    scan_reduce_kernel<int32_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(ws.cnt, groups_cap, out->sizes,
-                                                                                  ws.partials);
+    mfg_count_kernel<<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
+        hop->nbr, k, roots, root_ts, windows, prev ? prev->nbr : nullptr, prev ? prev->ts : nullptr,
+        prev ? hop->parent : nullptr, count, groups_cap, out->sizes, ws.cnt, ws.partials, out->src_nid, out->src_ts);
     launch_scan_partials(ws.partials, tiles, out->sizes + 1, st);
     scan_apply_kernel<int32_t, int64_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
         ws.cnt, out->indptr, groups_cap, out->sizes, ws.partials);
-    mfg_close_kernel<<<1, 64, 0, st>>>(out->sizes, out->indptr);
     const int64_t slots = groups_cap * k;
     if (slots < (int64_t(1) << 32) - kBlock * 65536ll)
         mfg_scatter_kernel<uint32_t><<<grid_of(slots), kBlock, 0, st>>>(
