@@ -49,7 +49,7 @@ def parse():
     ap.add_argument("--batches-per-step", type=int, default=None,
                     help="batches fused into one sampler call (default: 64 for c3/c4, 1 for c5, 263 for c2)")
     ap.add_argument("--cpu-batches", type=int, default=None,
-                    help="batches in the CPU oracle sample (default: one step)")
+                    help="batches in the CPU oracle sample (default: eight steps' worth, about 10 s of oracle time on c4)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="first run a plain 4 GiB device copy (for scaling byte counters)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -117,9 +117,10 @@ def step_positions(nb, B, n):
 
 def cpu_baseline(w, nbatches):
     """The oracle, single-threaded, on a bounded sample: the roots of
-    ``nbatches`` consecutive batches from the middle of the epoch (one GPU step
-    at the default size), over an oracle T-CSR that holds the full runs of every
-    node the sample reaches.  Only the oracle's sampling call is timed."""
+    ``nbatches`` consecutive batches from the middle of the epoch (eight GPU
+    steps at the default size), over an oracle T-CSR that holds the full runs
+    of every node the sample reaches.  Only the oracle's sampling call is
+    timed."""
     import oracle
     from oracle import subgraph
     nbatches = min(nbatches, w.num_batches())
@@ -679,7 +680,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("CPU oracle baseline")
-        cpu = cpu_baseline(w, args.cpu_batches or B)
+        cpu = cpu_baseline(w, args.cpu_batches or 8 * B)
         log("CPU oracle: %.3g neighbours/s (%s)" % (cpu["value"], cpu["sample"]))
 
     line = {
