@@ -127,8 +127,10 @@ def cpu_baseline(w, nbatches):
     b0 = min(w.num_batches() // 2, w.num_batches() - nbatches)
     roots, rts, base = w.batches(b0, b0 + nbatches)
     src, dst, ts, eid = w.build_input()
+    t = time.perf_counter()
     g = subgraph.reach_tcsr(src, dst, ts, eid, w.num_nodes, w.undirected, roots, rts, w.fanouts,
                             w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
+    log("CPU oracle: sub-graph of %d entries built in %.1f s" % (len(g.nbr), time.perf_counter() - t))
     t = time.perf_counter()
     out = oracle.sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
                         w.sample_seed, base)
