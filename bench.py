@@ -43,7 +43,8 @@ T0 = time.time()
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=160,
+                    help="timed steps (default 160: on c4, 160 x 64 batches spread over the epoch = 3.2%% of it)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c4", choices=["c2", "c3", "c4", "c5"])
     ap.add_argument("--batches-per-step", type=int, default=None,
@@ -115,6 +116,16 @@ def step_positions(nb, B, n):
     return [int(round(i * last / (n - 1))) for i in range(n)]
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.partition(":")[2].strip()
+    except OSError:
+        pass
+    return "unknown CPU"
+
+
 def cpu_baseline(w, nbatches):
     """The oracle, single-threaded, on a bounded sample: the roots of
     ``nbatches`` consecutive batches from the middle of the epoch (eight GPU
@@ -130,7 +141,8 @@ def cpu_baseline(w, nbatches):
     t = time.perf_counter()
     g = subgraph.reach_tcsr(src, dst, ts, eid, w.num_nodes, w.undirected, roots, rts, w.fanouts,
                             w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
-    log("CPU oracle: sub-graph of %d entries built in %.1f s" % (len(g.nbr), time.perf_counter() - t))
+    build_s = time.perf_counter() - t
+    log("CPU oracle: sub-graph of %d entries built in %.1f s" % (len(g.nbr), build_s))
     t = time.perf_counter()
     out = oracle.sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
                         w.sample_seed, base)
@@ -138,8 +150,10 @@ def cpu_baseline(w, nbatches):
     nbrs = int(sum(int((h.nbr >= 0).sum()) for h in out))
     return dict(value=nbrs / dt, unit="neighbours/s", cores=1, kind="oracle",
                 sample="%d roots (%d consecutive batches from batch %d) of %s, %d hops, %d neighbours, "
-                       "%.2f s single-threaded (sampling call only; T-CSR of the reached sub-graph built beforehand)"
-                       % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, dt))
+                       "%.2f s single-threaded on %s (sampling call only; T-CSR of the reached sub-graph, "
+                       "%d entries, built beforehand in %.1f s)"
+                       % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, dt, cpu_model(),
+                          len(g.nbr), build_s))
 
 
 GATHER_DIM = 768             # MAG node features (Table 3), bfloat16
@@ -654,6 +668,7 @@ def main():
     nbrs_total = 0
     slots_total = 0
     hopn_bytes = 0.0
+    hopn_slots = 0
     for b in timed_pos:
         run(b)
         hs = smp.hops()
@@ -663,6 +678,7 @@ def main():
             nbrs_total += nv
             slots_total += hop.nbr.numel()
             if h >= 1:
+                hopn_slots += hop.nbr.numel()
                 roots2 = hs[h - 1].nbr[hs[h - 1].nbr >= 0].long()
                 deg = (indptr[roots2 + 1] - indptr[roots2]).double()
                 bounds = 1 if math.isinf(w.snapshot_len) else 2
@@ -671,6 +687,7 @@ def main():
                 # per slot: 16-byte entry read when valid, 20 bytes written
                 hopn_bytes += (hop.num_roots * (8 + 16 + 8) + search + nv * 16 + hop.nbr.numel() * 20)
     hopn_bytes_per_launch = hopn_bytes / max(len(timed_pos), 1)
+    hopn_slots_per_launch = hopn_slots / max(len(timed_pos), 1)
     avg_hopn_ms = hopn_ms / max(hopn_n, 1)
     achieved = hopn_bytes_per_launch / (avg_hopn_ms * 1e-3) / 1e9 if avg_hopn_ms > 0 else 0.0
     value = nbrs_total / (total_ms * 1e-3)
@@ -721,6 +738,12 @@ def main():
             "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBS,
             "traffic": traffic,
+            # DRAM-level view of the same launches: counted bytes / kernel time, and both
+            # byte counts per output slot (traffic / algorithmic = the overfetch ratio)
+            "traffic_gbs": traffic / (avg_hopn_ms * 1e-3) / 1e9 if traffic and avg_hopn_ms > 0 else None,
+            "traffic_frac": traffic / (avg_hopn_ms * 1e-3) / 1e9 / PEAK_HBM_GBS if traffic and avg_hopn_ms > 0 else None,
+            "traffic_bytes_per_slot": traffic / hopn_slots_per_launch if traffic and hopn_slots_per_launch else None,
+            "algorithmic_bytes_per_slot": hopn_bytes_per_launch / hopn_slots_per_launch if hopn_slots_per_launch else None,
             "algorithmic_bytes_per_launch": hopn_bytes_per_launch,
             "avg_launch_ms": avg_hopn_ms,
             "kernel_source_hash": khash,
