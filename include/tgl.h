@@ -50,11 +50,22 @@ typedef int32_t tgl_status;
 
 /*
  * One T-CSR entry: an edge leaving the owner node (whose run contains the
- * entry) towards `nbr`, at time `ts`, with the caller's edge id `eid`.
- * Section 3.1 keeps indices and times as separate arrays; here they are
- * interleaved into one 16-byte record so that a sampled slot is fetched with
- * a single aligned 16-byte load.
+ * entry) towards node `nbr & TGL_NBR_MASK`, at time `ts`, with the caller's
+ * edge id `eid`.  Section 3.1 keeps indices and times as separate arrays;
+ * here they are interleaved into one 16-byte record so that a sampled slot is
+ * fetched with a single aligned 16-byte load.
+ *
+ * Node ids are below 2^31, so bit 31 of `nbr` is free; it holds a hint,
+ * TGL_NBR_FIRST: when set, the neighbour's own run has no entry with a
+ * timestamp below this entry's ts.  A later hop's root (nbr, ts) then has an
+ * empty window whatever its snapshot, because every window lies below the
+ * root's time, so the sampler skips the neighbour's node record.  A clear bit
+ * promises nothing: results are the same with the bit set exactly as defined
+ * or clear everywhere.  tgl_tcsr_build sets it exactly; tgl_tcsr_nodes can
+ * set it for a T-CSR built elsewhere.
  */
+#define TGL_NBR_MASK  0x7fffffffu
+#define TGL_NBR_FIRST 0x80000000u
 typedef struct tgl_entry {
     int32_t nbr;
     float ts;
@@ -171,6 +182,7 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
  * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
  * dst[i], nbr src[i]).  Each node's run is sorted by (ts, entry index).
+ * Every entry's TGL_NBR_FIRST bit is set exactly as defined at tgl_entry.
  * Synchronises `stream` once, to read the device-side range check; returns
  * TGL_ERANGE (outputs unspecified) if any endpoint or timestamp is invalid.
  */
@@ -185,19 +197,25 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
 int64_t tgl_index_len(int64_t num_entries);
 
 /*
- * Writes the per-node summaries and, if ts_index is not NULL, the search index
- * of a T-CSR given by its indptr and timestamp arrays (for a T-CSR built
- * elsewhere and uploaded).
+ * Writes the per-node summaries, the search index (if ts_index is not NULL)
+ * and the TGL_NBR_FIRST hints (if entries is not NULL) of a T-CSR given by its
+ * indptr and timestamp arrays (for a T-CSR built elsewhere and uploaded).
  *   indptr     [device] int64[num_nodes + 1]
  *   ts         [device] float[num_entries]
  *   num_nodes  in [1, 2^31 - 1];  num_entries in [0, 2^32 - 1]
  *   nodes      [device] tgl_node[num_nodes], 128-byte aligned, output
  *   ts_index   [device] float[tgl_index_len(num_entries)], 16-byte aligned,
  *              output, or NULL
+ *   entries    [device] tgl_entry[num_entries], 16-byte aligned, or NULL:
+ *              bit 31 of each nbr is rewritten (set exactly when the
+ *              neighbour's run has no timestamp below the entry's ts; clear
+ *              for a neighbour id outside [0, num_nodes)), the other fields
+ *              are left alone
  * indptr values are clamped into [0, num_entries].  Never synchronises.
  */
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
-                          int64_t num_entries, tgl_node *nodes, float *ts_index, void *stream);
+                          int64_t num_entries, tgl_node *nodes, float *ts_index,
+                          tgl_entry *entries, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */

@@ -29,6 +29,8 @@ MAX_TABLES = 8
 
 NODE_WORDS = 32     # int32 words of one node record (128 bytes)
 NODE_INLINE = 28    # timestamps held inline in a node record
+NBR_MASK = 0x7FFFFFFF     # neighbour id bits of a T-CSR entry's nbr field
+NBR_FIRST = -0x80000000   # bit 31: the neighbour-first hint (as int32)
 INDEX_STRIDE = 32   # entries per sample of the search index
 
 MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
@@ -101,7 +103,7 @@ def lib() -> C.CDLL:
     L.tgl_index_len.restype = i64
     L.tgl_index_len.argtypes = [i64]
     L.tgl_tcsr_nodes.restype = i32
-    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P]
+    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -165,8 +167,9 @@ def _i32_array(v: Sequence[int]):
 @dataclass
 class TCSR:
     """Device T-CSR: indptr int64[N+1]; entries int64[M, 2] holding the 16-byte
-    records (int32 nbr, float32 ts | int64 eid); ts float32[M], the entries'
-    timestamps as the separate search array; nodes int32[N, 32], the per-node
+    records (int32 nbr, float32 ts | int64 eid), bit 31 of nbr being the
+    neighbour-first hint (set: the neighbour has no entry below this entry's
+    ts); ts float32[M], the entries' timestamps as the separate search array; nodes int32[N, 32], the per-node
     128-byte records (uint32 start, uint32 end, float32 first ts, float32 last
     ts, then float32 ts of the run's first 28 entries, +inf beyond);
     ts_index float32[ceil(M / 32)], every 32nd timestamp (the search index), or
@@ -184,7 +187,13 @@ class TCSR:
 
     @property
     def nbr(self) -> torch.Tensor:
-        return self.entries.view(torch.int32)[:, 0]
+        """Neighbour ids (the hint bit cleared)."""
+        return self.entries.view(torch.int32)[:, 0] & NBR_MASK
+
+    @property
+    def first_hint(self) -> torch.Tensor:
+        """Per entry: the neighbour-first hint bit."""
+        return self.entries.view(torch.int32)[:, 0] < 0
 
     @property
     def entry_ts(self) -> torch.Tensor:
@@ -216,9 +225,10 @@ def index_len(num_entries: int) -> int:
     return int(lib().tgl_index_len(int(num_entries)))
 
 
-def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True) -> TCSR:
+def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hints: bool = True) -> TCSR:
     """Uploads a T-CSR given as host arrays (e.g. one built elsewhere) and
-    computes its node summaries and, if `index`, its search index."""
+    computes its node summaries, if `index` its search index, and if `hints`
+    the neighbour-first hint bits (else they stay clear)."""
     rec = pack_entries(nbr, ts, eid)
     ent = torch.from_numpy(rec).to(device)
     tsa = torch.from_numpy(np.ascontiguousarray(np.asarray(ts, np.float32))).to(device)
@@ -231,7 +241,8 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True) -> T
     m = int(ent.shape[0])
     tsx = torch.empty(index_len(m), dtype=torch.float32, device=device) if index else None
     _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if m else None, n, m, _p(nodes),
-                                _p(tsx) if index and m else None, _stream()), "tgl_tcsr_nodes")
+                                _p(tsx) if index and m else None, _p(ent) if hints and m else None,
+                                _stream()), "tgl_tcsr_nodes")
     return TCSR(ip, ent, tsa, nodes, n, tsx)
 
 

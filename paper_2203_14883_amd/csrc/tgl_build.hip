@@ -260,10 +260,11 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
 }
 
 // Per-node records {start, end, first ts, last ts, ts[0..27]}: eight lanes per
-// node, lane i writing the i-th 16 bytes of the node's 128-byte record.
+// node, lane i writing the i-th 16 bytes of the node's 128-byte record.  If
+// first_out is given, the first timestamps also go to first_out[x].
 __global__ __launch_bounds__(kBlock) void nodes_kernel(const int64_t *__restrict__ indptr,
                                                        const float *__restrict__ ts, int64_t N, int64_t M,
-                                                       int4 *__restrict__ nodes) {
+                                                       int4 *__restrict__ nodes, float *__restrict__ first_out) {
     constexpr int kParts = static_cast<int>(sizeof(tgl_node) / 16);
     static_assert(sizeof(tgl_node) == 128 && TGL_NODE_INLINE == 4 * (kParts - 1), "node record layout");
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
@@ -281,6 +282,7 @@ __global__ __launch_bounds__(kBlock) void nodes_kernel(const int64_t *__restrict
             const float last = b > a ? ts[b - 1] : -__builtin_inff();
             v = make_int4(static_cast<int>(static_cast<uint32_t>(a)), static_cast<int>(static_cast<uint32_t>(b)),
                           __float_as_int(first), __float_as_int(last));
+            if (first_out) first_out[x] = first;
         } else {
             const int64_t p = a + 4 * (part - 1);
             const float inf = __builtin_inff();
@@ -288,6 +290,27 @@ __global__ __launch_bounds__(kBlock) void nodes_kernel(const int64_t *__restrict
                           __float_as_int(p + 2 < b ? ts[p + 2] : inf), __float_as_int(p + 3 < b ? ts[p + 3] : inf));
         }
         nodes[g] = v;
+    }
+}
+
+// TGL_NBR_FIRST hints: bit 31 of entry p's neighbour id is set exactly when
+// the neighbour's first timestamp is not below ts[p] (its run is sorted, so
+// no entry of it lies below ts[p]).  first[x * stride] is node x's first
+// timestamp (+inf for an empty run): a compact array (stride 1) or the node
+// records (stride 32, offset to the first_ts word by the caller).  Neighbour
+// ids outside [0, N) get a clear bit.
+__global__ __launch_bounds__(kBlock) void first_hint_kernel(int4 *__restrict__ ent, const float *__restrict__ ts,
+                                                            int64_t M, const float *__restrict__ first,
+                                                            int64_t stride, int64_t N) {
+    int32_t *const nb = reinterpret_cast<int32_t *>(ent);         // word 0 of every 16-byte entry
+    const int64_t gstride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += gstride) {
+        const uint32_t raw = static_cast<uint32_t>(nb[4 * p]);
+        const uint32_t x = raw & TGL_NBR_MASK;
+        bool hint = false;
+        if (static_cast<int64_t>(x) < N) hint = !(first[static_cast<int64_t>(x) * stride] < ts[p]);
+        const uint32_t out = x | (hint ? TGL_NBR_FIRST : 0u);
+        if (out != raw) nb[4 * p] = static_cast<int32_t>(out);
     }
 }
 
@@ -383,7 +406,7 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     if (M == 0) {
         fill_indptr_kernel<<<grid_for(num_nodes + 1), kBlock, 0, st>>>(indptr, num_nodes + 1, 0);
         nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, 0,
-                                                                 reinterpret_cast<int4 *>(nodes_out));
+                                                                 reinterpret_cast<int4 *>(nodes_out), nullptr);
         return launch_status();
     }
 
@@ -417,8 +440,14 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     }
     emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes,
                                                indptr, reinterpret_cast<int4 *>(entries), ts_out);
+    // first timestamps, compact, into the sort's spare key buffer when they fit
+    // (8 bytes per entry), else read from the node records
+    float *const first = num_nodes <= 2 * M ? reinterpret_cast<float *>(w.keys[cur ^ 1]) : nullptr;
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
-                                                             reinterpret_cast<int4 *>(nodes_out));
+                                                             reinterpret_cast<int4 *>(nodes_out), first);
+    first_hint_kernel<<<grid_for(M), kBlock, 0, st>>>(
+        reinterpret_cast<int4 *>(entries), ts_out, M,
+        first ? first : reinterpret_cast<const float *>(nodes_out) + 2, first ? 1 : 32, num_nodes);
     if (ts_index_out && M > 0) {
         const int64_t L = tgl_index_len(M);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts_out, L, ts_index_out);
@@ -432,16 +461,22 @@ int64_t tgl_index_len(int64_t num_entries) {
 }
 
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
-                          int64_t num_entries, tgl_node *nodes, float *ts_index, void *stream) {
+                          int64_t num_entries, tgl_node *nodes, float *ts_index, tgl_entry *entries,
+                          void *stream) {
     if (num_nodes < 1 || num_nodes > INT32_MAX) return TGL_EINVAL;
     if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
     if (!indptr || !nodes || (num_entries > 0 && !ts)) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(nodes) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_index) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
-                                                             reinterpret_cast<int4 *>(nodes));
+                                                             reinterpret_cast<int4 *>(nodes), nullptr);
+    if (entries && num_entries > 0)
+        first_hint_kernel<<<grid_for(num_entries), kBlock, 0, st>>>(
+            reinterpret_cast<int4 *>(entries), ts, num_entries, reinterpret_cast<const float *>(nodes) + 2, 32,
+            num_nodes);
     if (ts_index && num_entries > 0) {
         const int64_t L = tgl_index_len(num_entries);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts, L, ts_index);

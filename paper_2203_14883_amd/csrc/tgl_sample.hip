@@ -69,6 +69,7 @@ struct HopArgs {
     int32_t p_k;                // fanout of the previous hop
     int64_t p_groups_static;    // previous hop's groups (hop 1 groups: R*S) ...
     const int64_t *p_groups_dyn; // ... or read on the device (roots of hop >= 2)
+    const uint8_t *p_first;     // TGL_NBR_FIRST hint of each previous-hop slot, or null
     // parameters
     uint64_t root_base;
     int32_t S;                  // snapshots
@@ -90,6 +91,7 @@ struct HopArgs {
     int32_t *o_s;               // window of each root, for a later hop (or null)
     float *o_t0;                // hop-1 ancestor time of each root, for a later hop (anchor A, or null)
     uint64_t *o_path;           // path of each root, for a later hop (or null)
+    uint8_t *o_first;           // TGL_NBR_FIRST hint of each slot, for the next hop (or null)
     int64_t *count0_out;        // hop 1 stores its root count here
 };
 
@@ -430,13 +432,18 @@ __device__ __forceinline__ NodeRun node_run(const HopArgs &p, int32_t x, bool va
     return r;
 }
 
+// Writes slot o from entry v (valid) or as PAD; the neighbour id loses the
+// entry's hint bit, which goes to o_first for the next hop.
 template <bool LAST>
 __device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, bool valid, int4 v, float t) {
     int32_t nbr = -1;
     int64_t eid = -1;
     float ts = -1.0f, dt = -1.0f;
+    if constexpr (!LAST) {
+        if (p.o_first) p.o_first[o] = valid && v.x < 0 ? 1 : 0;
+    }
     if (valid) {
-        nbr = v.x;
+        nbr = static_cast<int32_t>(static_cast<uint32_t>(v.x) & TGL_NBR_MASK);
         ts = __int_as_float(v.y);
         eid = static_cast<int64_t>(static_cast<uint32_t>(v.z)) | (static_cast<int64_t>(v.w) << 32);
         dt = static_cast<float>(static_cast<double>(t) - static_cast<double>(ts));
@@ -741,7 +748,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                 }
             }
         }
-        const NodeRun run = node_run(p, x, valid);
+        // a root whose entry carried the hint has an empty window: its node
+        // record is not read
+        bool known_empty = false;
+        if constexpr (!FIRST) known_empty = valid && p.p_first && p.p_first[v] != 0;
+        const NodeRun run = node_run(p, x, valid && !known_empty);
         // window thresholds; with the root anchor the window also ends below t
         float vh = bound_value(ta, s, p.delta);
         if (p.anchor == TGL_ANCHOR_ROOT && t < vh) vh = t;
@@ -938,16 +949,22 @@ struct SampleWs {
     int32_t *s[2] = {nullptr, nullptr};       // window per root (hops 2..L-1)
     uint64_t *path[2] = {nullptr, nullptr};   // path per root (hops 2..L-1)
     float *t0[2] = {nullptr, nullptr};        // hop-1 ancestor time per root (hops 2..L-1, root anchor)
+    uint8_t *first[2] = {nullptr, nullptr};   // TGL_NBR_FIRST hint per slot (hops 1..L-1)
     size_t bytes = 0;
 };
 
 // Workspace: per-group counts, offsets and scan partials for the largest hop
 // h < L; window, path and hop-1 ancestor time of the roots of hops 2..L-1
-// (two alternating buffers).
+// (two alternating buffers); the neighbour-first hint of the slots of hops
+// 1..L-1 (hop h writes buffer h & 1, hop h + 1 reads it).
 SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S) {
     SampleWs w;
     Carver cv(base);
     if (hops >= 2) {
+        int64_t max_slots = 0;                 // slots of hops 1..L-1
+        for (int h = 1; h < hops; h++) max_slots = cap[h] > max_slots ? cap[h] : max_slots;
+        const int nfirst = hops >= 3 ? 2 : 1;
+        for (int i = 0; i < nfirst; i++) w.first[(1 + i) & 1] = cv.take<uint8_t>(static_cast<size_t>(max_slots));
         int64_t max_groups = cap[0] * S;      // hop-1 groups
         for (int h = 2; h < hops; h++) max_groups = cap[h - 1] > max_groups ? cap[h - 1] : max_groups;
         w.cnt = cv.take<int32_t>(static_cast<size_t>(max_groups));
@@ -1071,6 +1088,8 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         a.o_s = keep ? ws.s[h & 1] : nullptr;
         a.o_path = keep ? ws.path[h & 1] : nullptr;
         a.o_t0 = keep && anchor == TGL_ANCHOR_ROOT ? ws.t0[h & 1] : nullptr;
+        a.o_first = last ? nullptr : ws.first[h & 1];
+        a.p_first = h >= 2 ? ws.first[(h - 1) & 1] : nullptr;
         a.count0_out = h == 1 ? counts : nullptr;
         if (h >= 2) {
             const tgl_hop_out &po = outs[h - 2];

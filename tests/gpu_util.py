@@ -32,14 +32,38 @@ def hops_to_numpy(hops):
                  num_roots=h.num_roots) for h in hops]
 
 
-def tcsr_to_host(g):
+def first_hints(indptr, nbr, ts):
+    """The neighbour-first hint of every entry, from its definition: the
+    neighbour's run (sorted by time) has no timestamp below the entry's, i.e.
+    the neighbour's first timestamp (+inf for an empty run) is not below it.
+    Neighbour ids outside the node range get no hint."""
+    indptr = np.asarray(indptr, np.int64)
+    nbr = np.asarray(nbr, np.int64)
+    ts = np.asarray(ts, np.float32)
+    n = len(indptr) - 1
+    first = np.full(n, np.inf, np.float32)
+    ne = indptr[1:] > indptr[:-1]
+    first[ne] = ts[indptr[:-1][ne]]
+    ok = (nbr >= 0) & (nbr < n)
+    h = np.zeros(len(nbr), bool)
+    h[ok] = ~(first[nbr[ok]] < ts[ok])
+    return h
+
+
+def tcsr_to_host(g, hints=True):
     """Host copy of a device T-CSR; checks that the separate timestamp array
-    equals the records' timestamps bit for bit."""
+    equals the records' timestamps bit for bit, and that the neighbour-first
+    hint bits follow their definition (or, with hints=False, are all clear)."""
     ent = g.entries.cpu().numpy().reshape(-1, 2)
     w = ent.view(np.int32).reshape(-1, 4)
     ts = g.ts.cpu().numpy()
     assert np.array_equal(ts.view(np.int32), w[:, 1]), "ts array differs from the records"
     ip = g.indptr.cpu().numpy()
+    nbr = w[:, 0] & 0x7FFFFFFF
+    got_hint = w[:, 0] < 0
+    want_hint = first_hints(ip, nbr, ts) if hints else np.zeros(len(nbr), bool)
+    assert np.array_equal(got_hint, want_hint), "neighbour-first hints: %d of %d differ" % (
+        int((got_hint != want_hint).sum()), len(nbr))
     nodes = g.nodes.cpu().numpy()
     assert np.array_equal(nodes[:, 0].view(np.uint32), ip[:-1]), "node summary start"
     assert np.array_equal(nodes[:, 1].view(np.uint32), ip[1:]), "node summary end"
@@ -57,7 +81,7 @@ def tcsr_to_host(g):
     if g.ts_index is not None:
         tsx = g.ts_index.cpu().numpy()
         assert np.array_equal(tsx.view(np.uint32), ts[::32].view(np.uint32)), "search index"
-    return oracle.TCSR(g.indptr.cpu().numpy(), w[:, 0].copy(), ent[:, 1].copy(),
+    return oracle.TCSR(g.indptr.cpu().numpy(), nbr.copy(), ent[:, 1].copy(),
                        w[:, 1].copy().view(np.float32))
 
 

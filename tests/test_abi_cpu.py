@@ -145,8 +145,9 @@ def test_nodes_rejects_invalid_arguments():
     for args in [(FAKE, FAKE, 0, 10, FAKE), (FAKE, FAKE, 2**31, 10, FAKE), (FAKE, FAKE, 5, -1, FAKE),
                  (FAKE, FAKE, 5, 2**32, FAKE), (None, FAKE, 5, 10, FAKE), (FAKE, None, 5, 10, FAKE),
                  (FAKE, FAKE, 5, 10, None), (FAKE, FAKE, 5, 10, FAKE + 4), (FAKE, FAKE, 5, 10, FAKE + 64)]:
-        assert L.tgl_tcsr_nodes(*args, None, None) == B.EINVAL, args
-    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, FAKE + 4, None) == B.EINVAL
+        assert L.tgl_tcsr_nodes(*args, None, None, None) == B.EINVAL, args
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, FAKE + 4, None, None) == B.EINVAL   # misaligned index
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, FAKE + 8, None) == B.EINVAL   # misaligned entries
 
 
 def test_index_len():

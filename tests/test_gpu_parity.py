@@ -274,3 +274,45 @@ def test_snapshot_anchor_root(torch):
         got = gpu_sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base,
                          anchor=anchor)
         assert_hops_equal(got, want, "c5 anchor %s" % anchor)
+
+
+def test_neighbour_first_hints(torch):
+    """The neighbour-first hint (bit 31 of a T-CSR entry's nbr) lets a later
+    hop skip the node record of a root with an empty window.  Samples must be
+    the oracle's with the hints set exactly (GPU build, upload), with the hints
+    clear everywhere, and with either snapshot anchor, on random graphs of 2-4
+    hops (directed and undirected, with finite and infinite windows) and on a
+    reduced c4, where about half of the hop-2 roots carry the hint."""
+    rng = np.random.default_rng(31)
+    trial = 0
+    while trial < 40:
+        N, src, dst, ts, eid, und, roots, rts, fan, mode, S, D, seed, base = _rand_case(rng)
+        if len(fan) < 2:
+            continue
+        trial += 1
+        anchor = "root" if trial % 3 == 0 and not math.isinf(D) else "own"
+        announce("hint trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s anchor=%s"
+                 % (trial, N, len(src), len(roots), fan, mode, S, D, anchor))
+        og = oracle.build_tcsr(src, dst, ts, eid, N, und)
+        want = oracle.sample(og, roots, rts, fan, mode, S, D, seed, base, anchor=anchor)
+        for hints in (True, False):
+            g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints)
+            assert_tcsr_equal(tcsr_to_host(g, hints=hints), og, "hint trial %d (hints=%s)" % (trial, hints))
+            got = gpu_sample(g, roots, rts, fan, mode, S, D, seed, base, anchor=anchor)
+            assert_hops_equal(got, want, "hint trial %d (hints=%s)" % (trial, hints))
+    w = W.make_c4(num_nodes=1_000_000, num_edges=10_700_000)
+    og = oracle.build_tcsr(w.src, w.dst, w.ts, None, w.num_nodes, True)
+    roots, rts, base = w.batches(2000, 2008)
+    want = oracle.sample(og, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
+    # hop-2 roots whose entry carries the hint: the path is exercised
+    first = np.full(w.num_nodes, np.inf, np.float32)
+    ne = og.indptr[1:] > og.indptr[:-1]
+    first[ne] = og.ts[og.indptr[:-1][ne]]
+    v = want[0].nbr >= 0
+    hinted = ~(first[want[0].nbr[v]] < want[0].ts[v])
+    assert hinted.mean() > 0.3, "reduced c4: only %.2f of the hop-2 roots are hinted" % hinted.mean()
+    for hints in (True, False):
+        announce("hints=%s on reduced c4" % hints)
+        g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints)
+        got = gpu_sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
+        assert_hops_equal(got, want, "reduced c4 (hints=%s)" % hints)
