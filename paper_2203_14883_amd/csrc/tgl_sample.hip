@@ -62,7 +62,8 @@ struct HopArgs {
     // hops >= 2: the previous hop's slots are the candidate roots
     const int32_t *p_nbr;
     const float *p_ts;
-    const int64_t *p_off;       // exclusive offsets of the previous hop's groups
+    const int32_t *p_local;     // previous hop's groups: exclusive offset within the scan tile ...
+    const int64_t *p_tile;      // ... plus the exclusive offset of the tile (kScanTile groups)
     const int32_t *p_s;         // window of each previous-hop group (null: hop 1 groups)
     const float *p_t0;          // hop-1 ancestor time of each previous-hop group (anchor A, hops >= 3)
     const uint64_t *p_path;     // path of each previous-hop group (null: hop 1 groups)
@@ -728,7 +729,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                 ta = t;
                 const int64_t g = v / pk;
                 const int64_t j = v - g * pk;
-                q = p.p_off[g] + j;
+                q = p.p_tile[g / kScanTile] + p.p_local[g] + j;
                 if (p.p_s) {
                     s = p.p_s[g];
                     path = p.p_path[g] * static_cast<uint64_t>(pk) + static_cast<uint64_t>(j);
@@ -942,10 +943,42 @@ bool sample_args_ok(int64_t R, int32_t hops, const int32_t *fanouts, int32_t S) 
     return true;
 }
 
+// Exclusive scan of a hop's per-group valid counts, first pass, tiles of
+// kScanTile groups per block: the counts are overwritten with each group's
+// offset within its tile, and the tile totals go to tile_off (which
+// launch_scan_partials then turns into exclusive tile offsets, writing the
+// grand total, the next hop's root count).  The next hop's index of group
+// g's slot j is tile_off[g / kScanTile] + cnt[g] + j.  Against a reduce pass
+// and an apply pass, this reads the counts once and writes 4 bytes per group
+// instead of 8.
+__global__ __launch_bounds__(kBlock) void group_scan_kernel(int32_t *__restrict__ cnt, int64_t n_static,
+                                                            const int64_t *__restrict__ n_dyn,
+                                                            int64_t *__restrict__ tile_off) {
+    __shared__ int64_t lds[kBlock / kWave];
+    const int64_t n = n_dyn ? *n_dyn : n_static;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanTile + static_cast<int64_t>(threadIdx.x) * kScanItems;
+    int32_t v[kScanItems];
+    int64_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; i++) {
+        const int64_t idx = base + i;
+        v[i] = idx < n ? cnt[idx] : 0;
+        sum += v[i];
+    }
+    int64_t total;
+    int64_t run = block_exclusive_sum<int64_t>(sum, lds, &total);
+#pragma unroll
+    for (int i = 0; i < kScanItems; i++) {
+        const int64_t idx = base + i;
+        if (idx < n) cnt[idx] = static_cast<int32_t>(run);        // < kScanTile * TGL_MAX_FANOUT
+        run += v[i];
+    }
+    if (threadIdx.x == 0) tile_off[blockIdx.x] = total;
+}
+
 struct SampleWs {
-    int32_t *cnt = nullptr;          // valid slots per group of the current hop
-    int64_t *off = nullptr;          // their exclusive scan
-    int64_t *partials = nullptr;
+    int32_t *cnt = nullptr;          // valid slots per group of the current hop, then their offsets in the tile
+    int64_t *tile_off = nullptr;     // per scan tile: total, then exclusive offset
     int32_t *s[2] = {nullptr, nullptr};       // window per root (hops 2..L-1)
     uint64_t *path[2] = {nullptr, nullptr};   // path per root (hops 2..L-1)
     float *t0[2] = {nullptr, nullptr};        // hop-1 ancestor time per root (hops 2..L-1, root anchor)
@@ -968,8 +1001,7 @@ SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S
         int64_t max_groups = cap[0] * S;      // hop-1 groups
         for (int h = 2; h < hops; h++) max_groups = cap[h - 1] > max_groups ? cap[h - 1] : max_groups;
         w.cnt = cv.take<int32_t>(static_cast<size_t>(max_groups));
-        w.off = cv.take<int64_t>(static_cast<size_t>(max_groups));
-        w.partials = cv.take<int64_t>(static_cast<size_t>(scan_tiles(max_groups) + 1));
+        w.tile_off = cv.take<int64_t>(static_cast<size_t>(scan_tiles(max_groups) + 1));
         if (hops >= 3) {
             int64_t max_mid = 0;               // roots of hops 2..L-1
             for (int h = 2; h < hops; h++) max_mid = cap[h - 1] > max_mid ? cap[h - 1] : max_mid;
@@ -1095,7 +1127,8 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
             const tgl_hop_out &po = outs[h - 2];
             a.p_nbr = po.nbr;
             a.p_ts = po.ts;
-            a.p_off = ws.off;
+            a.p_local = ws.cnt;
+            a.p_tile = ws.tile_off;
             a.p_k = fanouts[h - 2];
             a.p_s = h >= 3 ? ws.s[(h - 1) & 1] : nullptr;
             a.p_path = h >= 3 ? ws.path[(h - 1) & 1] : nullptr;
@@ -1118,11 +1151,9 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         const int64_t *groups_dyn = h == 1 ? nullptr : counts + (h - 1);
         const int64_t tiles = scan_tiles(groups_cap) > 0 ? scan_tiles(groups_cap) : 1;
         ScopedTimer tm(TGL_TIMER_COMPACT, st);
-        scan_reduce_kernel<int32_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
-            ws.cnt, groups_cap, groups_dyn, ws.partials);
-        launch_scan_partials(ws.partials, tiles, counts + h, st);
-        scan_apply_kernel<int32_t, int64_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
-            ws.cnt, ws.off, groups_cap, groups_dyn, ws.partials);
+        group_scan_kernel<<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(ws.cnt, groups_cap, groups_dyn,
+                                                                          ws.tile_off);
+        launch_scan_partials(ws.tile_off, tiles, counts + h, st);
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
     }
     return TGL_OK;
