@@ -10,17 +10,20 @@
 // lane l computes elements l, l + 64, ... of the row, so every store
 // instruction writes 64 consecutive elements and no row waits on a load.
 //
-// Accuracy: the argument a = omega * dt + phi is formed in double precision
-// (the product of two floats is exact there) and reduced in double to
-// x = a - k pi/2 with |x| <= pi/4, before anything is rounded to float.  A
-// plain float evaluation of the argument would be off by up to half an ulp of
-// omega * dt -- 0.125 at dt = 2.7e6 s, Wikipedia's time span -- which the
-// cosine passes on unchanged.  cos(a) is then +-cos(x) or +-sin(x) by the
-// quadrant k mod 4, each from its Taylor series to the x^8 / x^9 term: on
-// |x| <= pi/4 the first omitted terms are below 2.5e-8 and 2e-9, and the
-// float Horner evaluation (fused multiply-adds) adds a few float ulps.  The
-// result is within 1e-6 of cos(a).  Arguments of magnitude 2^31 or more,
-// where the double reduction loses accuracy, use the double cosine instead.
+// Accuracy: the argument is formed in turns, t = (omega / 2 pi) dt + phi / 2 pi,
+// in double precision, from per-column factors omega / 2 pi and phi / 2 pi
+// (each within 2^-52 relative of exact); below 2^24 turns t is within 5e-8
+// rad of the exact argument.  Its fraction f = t - rint(t) is exact, and
+// cos(2 pi f) = cos(2 pi g) for g = |f| in [0, 1/2]; above 1/4 it is
+// -cos(2 pi (1/2 - g)), also exact, so only [0, 1/4] is left: x = 2 pi g
+// in [0, pi/2], where the cosine's Taylor series to x^12, in powers of g^2,
+// leaves out less than 6.4e-9.  g is rounded to float (2.4e-8 rad) and the
+// series evaluated by fused multiply-adds in float (a few float ulps).  The
+// result is within 3e-7 of cos(omega dt + phi).  A plain float evaluation of
+// the argument would be off by up to half an ulp of omega * dt -- 0.125 at
+// dt = 2.7e6 s, Wikipedia's time span -- which the cosine passes on
+// unchanged.  Arguments of 2^24 turns or more, infinite or NaN use the double
+// cosine of the double argument instead.
 //
 // Padded slots (dt < 0) have no time difference: their rows are zeros, and a
 // row's dt is the same for the whole wavefront, so those rows branch to plain
@@ -31,29 +34,47 @@ namespace tgl {
 namespace {
 
 constexpr int kRows = 16;                                          // slots per wavefront pass
-constexpr double kTwoOverPi = 0.63661977236758134307553505349006;
-constexpr double kPiOver2 = 1.5707963267948966192313216916398;
+constexpr double kInvTwoPi = 0.15915494309189535;                  // 1 / (2 pi), nearest double
+constexpr double kTurnLimit = 0x1p24;                              // turns reduced in double below this
+constexpr int kMaxPre = 1024;                                      // columns whose factors fit in LDS
 
-__device__ __forceinline__ float encode(float w, float dt, float ph) {
-    const double a = fma(static_cast<double>(w), static_cast<double>(dt), static_cast<double>(ph));
-    if (!(fabs(a) < 0x1p31)) return static_cast<float>(cos(a));  // huge, infinite or NaN arguments
-    const double k = rint(a * kTwoOverPi);
-    const float x = static_cast<float>(fma(-k, kPiOver2, a));      // |x| <= pi/4 up to rounding
-    const float x2 = x * x;
-    // Taylor series of cos and sin about 0, Horner form
-    float c = __builtin_fmaf(x2, 1.0f / 40320.0f, -1.0f / 720.0f);
-    c = __builtin_fmaf(x2, c, 1.0f / 24.0f);
-    c = __builtin_fmaf(x2, c, -0.5f);
-    c = __builtin_fmaf(x2, c, 1.0f);
-    float sn = __builtin_fmaf(x2, 1.0f / 362880.0f, -1.0f / 5040.0f);
-    sn = __builtin_fmaf(x2, sn, 1.0f / 120.0f);
-    sn = __builtin_fmaf(x2, sn, -1.0f / 6.0f);
-    sn = __builtin_fmaf(x2, sn, 1.0f);
-    sn *= x;
-    // cos(x + k pi/2) = cos x, -sin x, -cos x, sin x for k = 0, 1, 2, 3 mod 4
-    const int q = static_cast<int>(static_cast<int64_t>(k) & 3);
-    const float v = (q & 1) ? sn : c;
-    return (q == 1 || q == 2) ? -v : v;
+// cos(2 pi g) = sum_n c_n g^(2n), c_n = (-1)^n (2 pi)^(2n) / (2n)!  (n <= 6)
+constexpr float kC1 = -19.739208802178717f;
+constexpr float kC2 = 64.93939402266829f;
+constexpr float kC3 = -85.45681720669373f;
+constexpr float kC4 = 60.24464137187666f;
+constexpr float kC5 = -26.426256783374397f;
+constexpr float kC6 = 7.903536371318469f;
+
+// cos(omega dt + phi) from wp = omega / 2 pi and pp = phi / 2 pi; omega[j] and
+// phi[j] are read only for the double-precision fallback.
+__device__ __forceinline__ float encode(double wp, double pp, float dt, const float *__restrict__ omega,
+                                        const float *__restrict__ phi, int j) {
+    const double t = fma(wp, static_cast<double>(dt), pp);        // the argument in turns
+    if (!(fabs(t) < kTurnLimit))                                   // huge, infinite or NaN
+        return static_cast<float>(cos(fma(static_cast<double>(omega[j]), static_cast<double>(dt),
+                                          static_cast<double>(phi[j]))));
+    const double f = t - rint(t);                                  // exact, in [-1/2, 1/2]
+    const double a = fabs(f);
+    const bool flip = a > 0.25;                                    // cos(2 pi a) = -cos(2 pi (1/2 - a))
+    const float g = static_cast<float>(flip ? 0.5 - a : a);        // 0.5 - a is exact
+    const float y = g * g;
+    float c = __builtin_fmaf(y, kC6, kC5);
+    c = __builtin_fmaf(y, c, kC4);
+    c = __builtin_fmaf(y, c, kC3);
+    c = __builtin_fmaf(y, c, kC2);
+    c = __builtin_fmaf(y, c, kC1);
+    c = __builtin_fmaf(y, c, 1.0f);
+    return flip ? -c : c;
+}
+
+// the per-column factors (omega / 2 pi, phi / 2 pi) of columns [0, dim), into
+// LDS by the whole block (dim <= kMaxPre)
+__device__ __forceinline__ void load_factors(double2 *__restrict__ f, const float *__restrict__ omega,
+                                             const float *__restrict__ phi, int dim) {
+    for (int j = threadIdx.x; j < dim; j += kBlock)
+        f[j] = make_double2(static_cast<double>(omega[j]) * kInvTwoPi, static_cast<double>(phi[j]) * kInvTwoPi);
+    __syncthreads();
 }
 
 // float -> bfloat16, round to nearest even (NaN stays a quiet NaN)
@@ -63,12 +84,14 @@ __device__ __forceinline__ uint16_t to_bf16(float v) {
     return static_cast<uint16_t>((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
 }
 
-template <int OUT>
+template <int OUT, bool PRE>
 __global__ __launch_bounds__(kBlock) void timeenc_kernel(const float *__restrict__ dt, int64_t n,
                                                          const int64_t *__restrict__ count, int64_t per,
                                                          const float *__restrict__ omega,
                                                          const float *__restrict__ phi, int dim,
                                                          void *__restrict__ out) {
+    __shared__ double2 fac[PRE ? kMaxPre : 1];
+    if constexpr (PRE) load_factors(fac, omega, phi, dim);
     const int lane = lane_id();
     constexpr int kWaves = kBlock / kWave;
     const int64_t waves = static_cast<int64_t>(gridDim.x) * kWaves;
@@ -89,7 +112,10 @@ __global__ __launch_bounds__(kBlock) void timeenc_kernel(const float *__restrict
             const int64_t base = row * dim;
             if (d >= 0.0f) {                                       // wavefront-uniform
                 for (int j = lane; j < dim; j += kWave) {
-                    const float v = encode(omega[j], d, phi[j]);
+                    const double2 fj = PRE ? fac[j]
+                                           : make_double2(static_cast<double>(omega[j]) * kInvTwoPi,
+                                                          static_cast<double>(phi[j]) * kInvTwoPi);
+                    const float v = encode(fj.x, fj.y, d, omega, phi, j);
                     if constexpr (OUT == TGL_OUT_F32)
                         __builtin_nontemporal_store(v, static_cast<float *>(out) + base + j);
                     else
@@ -112,13 +138,15 @@ __global__ __launch_bounds__(kBlock) void timeenc_kernel(const float *__restrict
 // bfloat16), so one store instruction writes 1 KB of contiguous output.  The
 // word's row and column come from one 32-bit division by the uniform number
 // of words per row.
-template <int OUT>
+template <int OUT, bool PRE>
 __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__restrict__ dt, int64_t n,
                                                              const int64_t *__restrict__ count, int64_t per,
                                                              const float *__restrict__ omega,
                                                              const float *__restrict__ phi, int dim,
                                                              void *__restrict__ out) {
     constexpr int EPW = OUT == TGL_OUT_F32 ? 4 : 8;                 // elements per 16-byte word
+    __shared__ double2 fac[PRE ? kMaxPre : 1];
+    if constexpr (PRE) load_factors(fac, omega, phi, dim);
     const int lane = lane_id();
     constexpr int kWaves = kBlock / kWave;
     const int64_t waves = static_cast<int64_t>(gridDim.x) * kWaves;
@@ -142,7 +170,12 @@ __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__rest
         float v[EPW];
         if (d >= 0.0f) {
 #pragma unroll
-            for (int e = 0; e < EPW; e++) v[e] = encode(omega[col + e], d, phi[col + e]);
+            for (int e = 0; e < EPW; e++) {
+                const double2 fj = PRE ? fac[col + e]
+                                       : make_double2(static_cast<double>(omega[col + e]) * kInvTwoPi,
+                                                      static_cast<double>(phi[col + e]) * kInvTwoPi);
+                v[e] = encode(fj.x, fj.y, d, omega, phi, col + e);
+            }
         } else {
 #pragma unroll
             for (int e = 0; e < EPW; e++) v[e] = 0.0f;
@@ -182,18 +215,21 @@ tgl_status tgl_time_encode(const float *dt, int64_t n, const int64_t *count, int
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     const int esize = out_type == TGL_OUT_F32 ? 4 : 2;
+    const bool pre = dim <= kMaxPre;                      // per-column factors staged in LDS
     const bool vec = (static_cast<int64_t>(dim) * esize) % 16 == 0 && (reinterpret_cast<uintptr_t>(out) & 15u) == 0;
     if (vec) {
         const int64_t words = n * (static_cast<int64_t>(dim) * esize / 16);
         int64_t blocks = (words + kBlock - 1) / kBlock;
         if (blocks > (1 << 16)) blocks = 1 << 16;
         ScopedTimer tm(TGL_TIMER_TIMEENC, st);
-        if (out_type == TGL_OUT_F32)
-            timeenc_vec_kernel<TGL_OUT_F32><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(
-                dt, n, count, per_count, omega, phi, dim, out);
-        else
-            timeenc_vec_kernel<TGL_OUT_BF16><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(
-                dt, n, count, per_count, omega, phi, dim, out);
+        const unsigned nb = static_cast<unsigned>(blocks);
+        if (out_type == TGL_OUT_F32) {
+            if (pre) timeenc_vec_kernel<TGL_OUT_F32, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+            else timeenc_vec_kernel<TGL_OUT_F32, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+        } else {
+            if (pre) timeenc_vec_kernel<TGL_OUT_BF16, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+            else timeenc_vec_kernel<TGL_OUT_BF16, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+        }
         return launch_status();
     }
     constexpr int64_t rows_per_block = static_cast<int64_t>(kBlock / kWave) * kRows;
@@ -201,12 +237,14 @@ tgl_status tgl_time_encode(const float *dt, int64_t n, const int64_t *count, int
     if (blocks > (1 << 16)) blocks = 1 << 16;
     {
         ScopedTimer tm(TGL_TIMER_TIMEENC, st);
-        if (out_type == TGL_OUT_F32)
-            timeenc_kernel<TGL_OUT_F32><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(dt, n, count, per_count,
-                                                                                         omega, phi, dim, out);
-        else
-            timeenc_kernel<TGL_OUT_BF16><<<static_cast<unsigned>(blocks), kBlock, 0, st>>>(dt, n, count, per_count,
-                                                                                          omega, phi, dim, out);
+        const unsigned nb = static_cast<unsigned>(blocks);
+        if (out_type == TGL_OUT_F32) {
+            if (pre) timeenc_kernel<TGL_OUT_F32, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+            else timeenc_kernel<TGL_OUT_F32, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+        } else {
+            if (pre) timeenc_kernel<TGL_OUT_BF16, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+            else timeenc_kernel<TGL_OUT_BF16, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+        }
     }
     return launch_status();
 }

@@ -1,12 +1,13 @@
 """tgl_time_encode (through the C ABI) against the Eq. 3 oracle.
 
-Tolerance, from the arithmetic: the kernel forms omega * dt + phi in double
-(exact product, one rounding of the sum), reduces it modulo 2 pi in double
-(error below 1e-7 for arguments up to 1e9), rounds the reduced argument to
-float (at most 2.4e-7 on [-pi, pi]) and takes a float cosine (a few ulp of a
-value in [-1, 1]).  So float32 rows are within 1e-6 of the float64 oracle;
-bfloat16 rows add the final rounding, at most half a bfloat16 ulp of a value
-below 1 in magnitude (2^-9).  PAD rows must be exactly zero."""
+Tolerance, from the arithmetic: the kernel forms the argument in turns,
+(omega / 2 pi) dt + phi / 2 pi, in double (within 5e-8 rad of exact below
+2^24 turns; beyond, a double cosine), takes its fraction exactly, rounds the
+folded fraction to float (2.4e-8 rad) and sums a cosine series to the x^12
+term (6.4e-9 left out) in float (a few ulp of a value in [-1, 1]): within
+3e-7 of cos(omega dt + phi).  So float32 rows are within 1e-6 of the float64
+oracle; bfloat16 rows add the final rounding, at most half a bfloat16 ulp of
+a value below 1 in magnitude (2^-9).  PAD rows must be exactly zero."""
 import math
 
 import numpy as np
