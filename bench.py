@@ -69,13 +69,38 @@ def parse():
     return ap.parse_args()
 
 
+def strip_comments(src):
+    """C++ source without comments, trailing blanks and empty lines (string
+    and character literals are kept as they are)."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        c = src[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and src[j] != c:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        elif src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return "\n".join(l.rstrip() for l in "".join(out).splitlines() if l.strip())
+
+
 def kernel_source_hash(files=("tgl_internal.hpp", "tgl_sample.hip")):
-    """Hash of the sources that define the measured kernels."""
+    """Hash of the code (comments left out) of the sources that define the
+    measured kernels, to tell whether committed counters still apply."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2203_14883_amd", "csrc")
     for f in files:
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + fh.read())
+        with open(os.path.join(csrc, f)) as fh:
+            h.update(f.encode() + strip_comments(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

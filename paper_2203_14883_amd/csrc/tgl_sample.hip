@@ -657,9 +657,11 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
 // snapshots).  Each wavefront takes chunks of 64 candidate roots:
 //   phase 1, one lane per candidate: hop 1 takes root v as given; later hops
 //     take slot v of the previous hop, valid when its nbr >= 0, as the root
-//     with index off[v / k_prev] + v % k_prev (and write its parent index).
-//     Every lane loads its root's time and run bounds; the valid roots are
-//     packed, in order, into LDS;
+//     with index off(g) + j for g = v / k_prev, j = v % k_prev, off the
+//     exclusive scan of the previous hop's group counts (and write its parent
+//     index).  Every lane loads its root's time and run bounds, except a root
+//     whose entry carried the neighbour-first hint (its window is empty); the
+//     valid roots are packed, in order, into LDS;
 //   phase 2, G lanes per root, 64 / G roots per round: the window [lo, hi);
 //   phase 3, one lane per slot: selection, gather and emit.  The packed roots
 //     have consecutive indices, so the slots of a chunk are one contiguous
