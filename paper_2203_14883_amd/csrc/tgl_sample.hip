@@ -35,7 +35,8 @@ namespace tgl {
 namespace {
 
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
-constexpr int kMaxGrid = 1 << 16;     // cap on blocks of the grid-stride hop kernels
+constexpr int kMaxGrid = 1 << 16;
+constexpr int kMultiEdges = 9;       // window edges per root held in LDS by hop_multi_kernel (S <= 8)     // cap on blocks of the grid-stride hop kernels
 constexpr int kWavesPerBlock = kBlock / kWave;
 
 __host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
@@ -556,13 +557,14 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, int32_t 
     wave_sync_lds();   // my_edges is rewritten by the group's next root
 }
 
-// First hop with S > 1 windows.  Each wavefront takes chunks of 64 roots:
+// First hop with more than kMultiEdges - 1 windows.  Each wavefront takes
+// chunks of 64 roots:
 //   phase 1, one lane per root: its time, path key and node summary are
 //     packed into LDS;
 //   phase 2, G lanes per root, 64 / G roots per round: the S + 1 window
 //     edges, then selection and emission of the root's S * k slots.
 template <int G, int MODE, bool LAST, bool PTR>
-__global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
+__global__ __launch_bounds__(kBlock) void hop_multi_wide_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots served per wavefront round
     constexpr int GPB = kBlock / G;
     const int lane = lane_id();
@@ -613,6 +615,168 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
             if (i < nvalid) {                       // group-uniform
                 multi_root<G, MODE, LAST, PTR>(p, c * kWave + i, r_x[w][i], r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i],
                                           r_t[w][i], r_hp[w][i], gl, my_edges);
+            }
+        }
+        wave_sync_lds();                            // the next chunk rewrites the LDS rows
+    }
+}
+
+// First hop with S > 1 windows, S + 1 <= kMultiEdges.  Each wavefront takes
+// chunks of 64 roots:
+//   phase 1, one lane per root: its time, path key and node summary are
+//     packed into LDS;
+//   phase 2, 8 lanes per root, 8 roots per round: the S + 1 window edges,
+//     four at a time, each batch searched below the lowest edge found so far
+//     (bounds fall with the window index), into LDS; then the per-window
+//     valid counts;
+//   phase 3, one lane per slot: selection, gather and emission.  Roots are
+//     dense on the first hop, so a chunk's slots are one contiguous range of
+//     the output and the stores coalesce.
+template <int MODE, bool LAST, bool PTR>
+__global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
+    constexpr int G = 8;
+    constexpr int GPW = kWave / G;            // roots located per wavefront round
+    constexpr int NE = 4;                     // window edges located together
+    constexpr int U = 4;                      // slots per lane whose loads are in flight together
+    const int lane = lane_id();
+    const int w = threadIdx.x / kWave;
+    const int gl = lane & (G - 1);
+    const int gw = lane / G;
+    __shared__ uint32_t r_a[kWavesPerBlock][kWave];
+    __shared__ uint32_t r_b[kWavesPerBlock][kWave];
+    __shared__ float r_f[kWavesPerBlock][kWave];
+    __shared__ float r_l[kWavesPerBlock][kWave];
+    __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
+    __shared__ float r_t[kWavesPerBlock][kWave];
+    __shared__ int32_t r_x[kWavesPerBlock][kWave];
+    __shared__ uint32_t r_e[kWavesPerBlock][kWave * kMultiEdges];   // window edges of each root
+
+    const uint32_t M = static_cast<uint32_t>(p.num_entries);
+    const int W = p.windows;
+    const int k = p.k;
+    const int nslots = W * k;                 // slots per root
+    const int64_t nv = p.num_roots;
+    if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = nv;
+    const int64_t nchunks = (nv + kWave - 1) / kWave;
+    const uint64_t hop_key = static_cast<uint64_t>(p.hop) << 40;
+
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w; c < nchunks;
+         c += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
+        // ---- phase 1: one lane per root ----
+        const int64_t v = c * kWave + lane;
+        const bool valid = v < nv;
+        int32_t x = -1;
+        float t = 0.0f;
+        if (valid) {
+            x = p.rx[v];
+            t = p.rt[v];
+        }
+        const NodeRun run = node_run(p, x, valid);
+        if (valid) {
+            r_a[w][lane] = run.a;
+            r_b[w][lane] = run.b;
+            r_f[w][lane] = run.first;
+            r_l[w][lane] = run.last;
+            r_hp[w][lane] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ (p.root_base + static_cast<uint64_t>(v))) : 0;
+            r_t[w][lane] = t;
+            r_x[w][lane] = x;
+        }
+        wave_sync_lds();
+        const int64_t rem = nv - c * kWave;
+        const int nvalid = rem < kWave ? static_cast<int>(rem) : kWave;
+
+        // ---- phase 2: G lanes per root locate its W + 1 window edges ----
+        for (int base = 0; base < nvalid; base += GPW) {
+            const int i = base + gw;
+            if (i < nvalid) {                       // group-uniform
+                const uint32_t a = r_a[w][i];
+                const uint32_t b = r_b[w][i];
+                const float first = r_f[w][i];
+                const float last = r_l[w][i];
+                const float ti = r_t[w][i];
+                const int32_t xi = r_x[w][i];
+                // a non-empty run belongs to a node inside the graph
+                const int4 *rec = b > a && b - a <= TGL_NODE_INLINE ? p.nodes + static_cast<int64_t>(xi) * 8 : nullptr;
+                uint32_t top = b;
+                for (int i0 = 0; i0 <= W; i0 += NE) {
+                    float vv[NE];
+                    bool act[NE];
+                    uint32_t cc[NE];
+#pragma unroll
+                    for (int u = 0; u < NE; u++) {
+                        vv[u] = bound_value(ti, i0 + u, p.delta);
+                        cc[u] = a;
+                        act[u] = i0 + u <= W && !edge_from_summary(a, b, first, last, vv[u], cc[u]);
+                    }
+                    uint32_t cs[NE];
+                    if (PTR && !rec && b - a > HeldRun<G>::span) {   // group-uniform: saved positions kept
+                        int ei[NE];
+#pragma unroll
+                        for (int u = 0; u < NE; u++) ei[u] = i0 + u;
+                        from_pointers<G, NE>(p, xi, a, b, ei, vv, act, cs, gl);
+                    } else {
+                        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, rec, a, top, vv, act, cs, gl);
+                    }
+#pragma unroll
+                    for (int u = 0; u < NE; u++) {
+                        if (i0 + u <= W) {
+                            const uint32_t e = act[u] ? cs[u] : cc[u];
+                            if (gl == 0) r_e[w][i * kMultiEdges + i0 + u] = e;
+                            top = e < top ? e : top;
+                        }
+                    }
+                }
+            }
+        }
+        wave_sync_lds();
+        // valid slots per (root, window) group, for the next hop
+        if (p.o_cnt) {
+            for (int g = lane; g < nvalid * W; g += kWave) {
+                const int i = g / W;
+                const int s = g - i * W;
+                const uint32_t whi = r_e[w][i * kMultiEdges + s];
+                const uint32_t wlo = r_e[w][i * kMultiEdges + s + 1];
+                const uint32_t n = wlo < whi ? whi - wlo : 0u;
+                p.o_cnt[(c * kWave + i) * W + s] = MODE == TGL_MOST_RECENT
+                                                       ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
+                                                       : (n > 0 ? k : 0);
+            }
+        }
+
+        // ---- phase 3: one lane per slot ----
+        const int total = nvalid * nslots;
+        const int64_t obase = c * kWave * static_cast<int64_t>(nslots);
+        for (int e0 = 0; e0 < total; e0 += U * kWave) {
+            uint32_t pick[U];                       // UINT32_MAX: PAD slot
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int e = e0 + u * kWave + lane;
+                const bool act = e < total;
+                const int i = act ? e / nslots : 0;
+                const int r = e - i * nslots;
+                const int s = act ? r / k : 0;
+                const int j = r - s * k;
+                const uint32_t whi = r_e[w][i * kMultiEdges + s];
+                uint32_t wlo = r_e[w][i * kMultiEdges + s + 1];
+                if (wlo > whi) wlo = whi;
+                const uint32_t n = whi - wlo;
+                if constexpr (MODE == TGL_MOST_RECENT) {
+                    pick[u] = act && static_cast<uint32_t>(j) < n ? whi - 1 - static_cast<uint32_t>(j) : UINT32_MAX;
+                } else {
+                    const uint64_t key = hop_key | (static_cast<uint64_t>(s) << 24) | static_cast<uint64_t>(j);
+                    pick[u] = act && n > 0
+                                  ? wlo + static_cast<uint32_t>(__umul64hi(mix64(r_hp[w][i] ^ key), static_cast<uint64_t>(n)))
+                                  : UINT32_MAX;
+                }
+            }
+            int4 rec[U];
+#pragma unroll
+            for (int u = 0; u < U; u++)
+                rec[u] = pick[u] != UINT32_MAX ? p.ent[pick[u]] : make_int4(-1, -1, -1, -1);
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int e = e0 + u * kWave + lane;
+                if (e < total) emit_slot<LAST>(p, obase + e, pick[u] != UINT32_MAX, rec[u], r_t[w][e / nslots]);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows
@@ -861,17 +1025,20 @@ void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t w
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxGrid) blocks = kMaxGrid;
     const unsigned nb = static_cast<unsigned>(blocks);
-    if (multi && a.ptr) {                     // first hop only; saved window edges kept
+    if (multi && a.windows + 1 <= kMultiEdges) {   // first hop only
+        if (a.ptr) hop_multi_kernel<MODE, LAST, true><<<nb, kBlock, 0, st>>>(a);
+        else hop_multi_kernel<MODE, LAST, false><<<nb, kBlock, 0, st>>>(a);
+    } else if (multi && a.ptr) {              // first hop only; saved window edges kept
         switch (G) {
-            case 16: hop_multi_kernel<16, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
-            case 32: hop_multi_kernel<32, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
-            default: hop_multi_kernel<64, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+            case 16: hop_multi_wide_kernel<16, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_wide_kernel<32, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_wide_kernel<64, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
         }
     } else if (multi) {                       // first hop only
         switch (G) {
-            case 16: hop_multi_kernel<16, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
-            case 32: hop_multi_kernel<32, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
-            default: hop_multi_kernel<64, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
+            case 16: hop_multi_wide_kernel<16, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_wide_kernel<32, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_wide_kernel<64, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
         }
     } else {
         // the window search uses 8 lanes per root whatever the fanout; one
