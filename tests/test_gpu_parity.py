@@ -316,3 +316,30 @@ def test_neighbour_first_hints(torch):
         g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints)
         got = gpu_sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
         assert_hops_equal(got, want, "reduced c4 (hints=%s)" % hints)
+
+
+def test_many_windows(torch):
+    """First hops with 2-12 snapshot windows on either side of the switch
+    between the multi-window kernel (up to 8 windows, window edges held in
+    LDS) and the wide one (more windows), both modes, 1-3 hops, with long
+    runs (searched on the index) and short ones (node-record timestamps)."""
+    rng = np.random.default_rng(77)
+    N = 40
+    lens = [30_000, 2_000, 300, 61, 28, 5] + [int(x) for x in rng.integers(0, 50, N - 6)]
+    src = np.concatenate([np.full(L, x, np.int32) for x, L in enumerate(lens)])
+    dst = rng.integers(0, N, len(src)).astype(np.int32)
+    ts = rng.integers(0, 20_000, len(src)).astype(np.float32)
+    og = oracle.build_tcsr(src, dst, ts, None, N, True)
+    g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid)
+    for trial, S in enumerate((2, 7, 8, 9, 12)):
+        for mode in ("recent", "uniform"):
+            fan = [(3, 2), (5,), (2, 2, 2)][(trial + (mode == "uniform")) % 3]
+            D = float(rng.choice([250.0, 1000.0, 1500.5]))
+            R = 700
+            roots = rng.integers(-1, N + 1, R).astype(np.int32)
+            rts = rng.integers(0, 21_000, R).astype(np.float32)
+            seed, base = int(rng.integers(0, 2**62)), int(rng.integers(0, 2**40))
+            announce("many windows S=%d mode=%s fan=%s D=%s" % (S, mode, fan, D))
+            want = oracle.sample(og, roots, rts, fan, mode, S, D, seed, base)
+            got = gpu_sample(g, roots, rts, fan, mode, S, D, seed, base)
+            assert_hops_equal(got, want, "S=%d %s" % (S, mode))
