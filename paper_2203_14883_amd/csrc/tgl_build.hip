@@ -1,16 +1,22 @@
 // tgl_build.hip -- T-CSR build (Section 3.1, "The T-CSR Data Structure").
 //
-// Every directed entry i gets the 64-bit key (owner node << 32 | tskey),
-// where tskey maps a float timestamp to an unsigned integer with the same
-// order.  A stable least-significant-digit radix sort of (key, i) then leaves
-// each node's entries contiguous and sorted by (ts, i), which is the T-CSR
-// order.  The key-building kernel also OR- and AND-reduces all keys; digits on
-// which every key agrees are skipped (node ids above ceil(log2 N) bits, and
-// timestamp bytes that never change, e.g. the low mantissa bytes of integer
-// years).  Each radix pass is reduce-then-scan: per-tile digit counts, a
-// device-wide scan in digit-major order, and a scatter in which every
-// wavefront ranks its keys with ballots (stable within the tile), the tile is
-// reordered in LDS and written out bucket by bucket.
+// Every directed entry i gets a 64-bit sort key holding its owner node and
+// its timestamp (as tskey, an unsigned integer with the float order); a
+// stable least-significant-digit radix sort of (key, i) then leaves each
+// node's entries contiguous and sorted by (ts, i), which is the T-CSR order.
+// A first pass validates the edges and OR- and AND-reduces node ids and
+// tskeys, so bits on which every entry agrees are known before any key is
+// written.  When the varying node bits, the varying tskey bits and the
+// neighbour id fit in 64 bits together (c4: 27 + 8 + 27), a key packs them in
+// that order: the sort runs over the node and tskey fields only (five 8-bit
+// passes for c4 instead of six), and the neighbour id rides in the low bits,
+// so writing the entries reads the sorted keys and indices in order instead
+// of gathering each neighbour by original edge index.  Otherwise the key is
+// (node << 32 | tskey) and the digits every key shares are skipped.  Each
+// radix pass is reduce-then-scan: per-tile digit counts, a device-wide scan in
+// digit-major order, and a scatter in which every wavefront ranks its keys
+// with ballots (stable within the tile), the tile is reordered in LDS and
+// written out bucket by bucket.
 //
 // The paper builds the T-CSR once on the host; here the same structure is
 // produced on the device from a COO that may be in any order.
@@ -65,32 +71,64 @@ __global__ void init_flags_kernel(BuildFlags *f) {
     f->and_bits = ~0ull;
 }
 
-// Entry i < m0: (src[i] -> dst[i]); entry m0 + i: (dst[i] -> src[i]).
-__global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict__ src,
-                                                      const int32_t *__restrict__ dst,
-                                                      const float *__restrict__ ts, int64_t m0,
-                                                      int64_t M, int64_t N,
-                                                      uint64_t *__restrict__ keys,
-                                                      uint32_t *__restrict__ vals,
-                                                      BuildFlags *__restrict__ flags) {
+// How a sort key holds (owner node, tskey, neighbour).  Packed: node field,
+// tskey field, neighbour id, from the most significant bits down; a field
+// keeps bits [lo, lo + bits) of its value, the bits outside being the same in
+// every entry (konst).  Unpacked: node << 32 | tskey.
+struct KeyLayout {
+    int packed;
+    int nbr_bits;
+    int ts_lo, ts_bits;
+    int node_lo, node_bits;
+    uint32_t ts_konst, node_konst;
+};
+
+__host__ __device__ __forceinline__ uint64_t low_mask(int bits) {
+    return bits >= 64 ? ~0ull : (1ull << bits) - 1ull;
+}
+
+__device__ __forceinline__ uint64_t make_key(const KeyLayout &L, uint32_t u, uint32_t tk, uint32_t v) {
+    if (!L.packed) return (static_cast<uint64_t>(u) << 32) | tk;
+    const uint64_t nf = (static_cast<uint64_t>(u) >> L.node_lo) & low_mask(L.node_bits);
+    const uint64_t tf = (static_cast<uint64_t>(tk) >> L.ts_lo) & low_mask(L.ts_bits);
+    return (nf << (L.nbr_bits + L.ts_bits)) | (tf << L.nbr_bits) | static_cast<uint64_t>(v);
+}
+
+__device__ __forceinline__ uint32_t key_node(const KeyLayout &L, uint64_t k) {
+    if (!L.packed) return static_cast<uint32_t>(k >> 32);
+    const uint64_t nf = (k >> (L.nbr_bits + L.ts_bits)) & low_mask(L.node_bits);
+    return L.node_konst | static_cast<uint32_t>(nf << L.node_lo);
+}
+
+__device__ __forceinline__ uint32_t key_tskey(const KeyLayout &L, uint64_t k) {
+    if (!L.packed) return static_cast<uint32_t>(k);
+    const uint64_t tf = (k >> L.nbr_bits) & low_mask(L.ts_bits);
+    return L.ts_konst | static_cast<uint32_t>(tf << L.ts_lo);
+}
+
+// Validation and the OR / AND of the node ids and tskeys of every entry (one
+// read of each edge: both directions when undirected).
+__global__ __launch_bounds__(kBlock) void reduce_kernel(const int32_t *__restrict__ src,
+                                                        const int32_t *__restrict__ dst,
+                                                        const float *__restrict__ ts, int64_t m0, bool both,
+                                                        int64_t N, BuildFlags *__restrict__ flags) {
     uint64_t o = 0, a = ~0ull;
     bool bad = false;
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < M; i += stride) {
-        const bool fwd = i < m0;
-        const int64_t k = fwd ? i : i - m0;
-        const int32_t u = fwd ? src[k] : dst[k];
+    for (int64_t k = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; k < m0; k += stride) {
+        const int32_t u = src[k];
+        const int32_t v = dst[k];
         const float t = ts[k];
-        if (fwd) {
-            const int32_t v = dst[k];
-            bad |= v < 0 || v >= N;
+        bad |= u < 0 || u >= N || v < 0 || v >= N || t != t;
+        const uint64_t tk = ts_key(t);
+        const uint64_t ku = (static_cast<uint64_t>(static_cast<uint32_t>(u)) << 32) | tk;
+        o |= ku;
+        a &= ku;
+        if (both) {
+            const uint64_t kv = (static_cast<uint64_t>(static_cast<uint32_t>(v)) << 32) | tk;
+            o |= kv;
+            a &= kv;
         }
-        bad |= u < 0 || u >= N || t != t;
-        const uint64_t key = (static_cast<uint64_t>(static_cast<uint32_t>(u)) << 32) | ts_key(t);
-        keys[i] = key;
-        vals[i] = static_cast<uint32_t>(i);
-        o |= key;
-        a &= key;
     }
     o = wave_or(o);
     a = wave_and(a);
@@ -99,6 +137,23 @@ __global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict_
         atomicOr(reinterpret_cast<unsigned long long *>(&flags->or_bits), static_cast<unsigned long long>(o));
         atomicAnd(reinterpret_cast<unsigned long long *>(&flags->and_bits), static_cast<unsigned long long>(a));
         if (any_bad) atomicOr(&flags->err, 1u);
+    }
+}
+
+// Entry i < m0: (src[i] -> dst[i]); entry m0 + i: (dst[i] -> src[i]).  Keys
+// in the layout L, values the entry indices.
+__global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict__ src,
+                                                      const int32_t *__restrict__ dst, const float *__restrict__ ts,
+                                                      int64_t m0, int64_t M, const KeyLayout L,
+                                                      uint64_t *__restrict__ keys, uint32_t *__restrict__ vals) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < M; i += stride) {
+        const bool fwd = i < m0;
+        const int64_t k = fwd ? i : i - m0;
+        const uint32_t u = static_cast<uint32_t>(fwd ? src[k] : dst[k]);
+        const uint32_t v = L.packed ? static_cast<uint32_t>(fwd ? dst[k] : src[k]) : 0u;
+        keys[i] = make_key(L, u, ts_key(ts[k]), v);
+        vals[i] = static_cast<uint32_t>(i);
     }
 }
 
@@ -226,13 +281,33 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     }
 }
 
+// first[x] = timestamp of node x's first entry in the sorted keys (the caller
+// fills first with +inf beforehand, for nodes without entries).
+__global__ __launch_bounds__(kBlock) void first_ts_kernel(const uint64_t *__restrict__ keys, int64_t M,
+                                                          const KeyLayout L, float *__restrict__ first) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
+        const uint64_t k = keys[p];
+        const uint32_t u = key_node(L, k);
+        if (p == 0 || key_node(L, keys[p - 1]) != u) first[u] = key_ts(key_tskey(L, k));
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void fill_float_kernel(float *__restrict__ a, int64_t n, float value) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n; i += stride) a[i] = value;
+}
+
 // Writes entries[p] from the sorted (key, i) and fills indptr: node x starts
-// at the first p whose owner is >= x.
+// at the first p whose owner is >= x.  The neighbour comes from the key
+// (packed layout) or from the edge list; with `first` (each node's first
+// timestamp) the entry's TGL_NBR_FIRST hint is set here.
 __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict__ keys,
                                                       const uint32_t *__restrict__ vals, int64_t M,
                                                       int64_t m0, const int32_t *__restrict__ src,
                                                       const int32_t *__restrict__ dst,
                                                       const int64_t *__restrict__ eid, int64_t N,
+                                                      const KeyLayout L, const float *__restrict__ first,
                                                       int64_t *__restrict__ indptr,
                                                       int4 *__restrict__ ent,
                                                       float *__restrict__ ts_out) {
@@ -241,17 +316,19 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
         const uint64_t key = keys[p];
         int64_t i = static_cast<int64_t>(vals[p]);
         if (i >= M) i = 0;       // never taken for a permutation; keeps loads in bounds
-        const int64_t u = static_cast<int64_t>(key >> 32);
-        const float t = key_ts(static_cast<uint32_t>(key));
+        const int64_t u = static_cast<int64_t>(key_node(L, key));
+        const float t = key_ts(key_tskey(L, key));
         const bool fwd = i < m0;
         const int64_t k = fwd ? i : i - m0;
-        const int32_t v = fwd ? dst[k] : src[k];
+        const int32_t v = L.packed ? static_cast<int32_t>(key & low_mask(L.nbr_bits)) : (fwd ? dst[k] : src[k]);
         const int64_t e = eid ? eid[k] : k;
-        ent[p] = make_int4(v, __float_as_int(t), static_cast<int>(static_cast<uint32_t>(e)),
+        uint32_t vw = static_cast<uint32_t>(v);
+        if (first && v >= 0 && v < N && !(first[v] < t)) vw |= TGL_NBR_FIRST;
+        ent[p] = make_int4(static_cast<int>(vw), __float_as_int(t), static_cast<int>(static_cast<uint32_t>(e)),
                            static_cast<int>(static_cast<uint64_t>(e) >> 32));
         ts_out[p] = t;
         // owners are in [0, N) after validation; the clamps only bound the stores
-        const int64_t uprev = p == 0 ? -1 : static_cast<int64_t>(keys[p - 1] >> 32);
+        const int64_t uprev = p == 0 ? -1 : static_cast<int64_t>(key_node(L, keys[p - 1]));
         const int64_t x1 = u < N ? u : N - 1;
         for (int64_t x = uprev + 1; x <= x1; x++) indptr[x] = p;
         if (p == M - 1)
@@ -362,6 +439,44 @@ bool build_args_ok(int64_t num_edges, int64_t num_nodes, uint32_t flags) {
     return M <= kMaxEntries && num_edges <= kMaxEntries;
 }
 
+// Lowest varying bit and number of bits from it to the highest varying bit.
+void field_of(uint32_t varying, int *lo, int *bits) {
+    if (varying == 0) {
+        *lo = 0;
+        *bits = 0;
+        return;
+    }
+    *lo = __builtin_ctz(varying);
+    *bits = 32 - __builtin_clz(varying) - *lo;
+}
+
+// The packed layout when node field, tskey field and neighbour id fit in 64
+// bits, else the plain one.  Neighbour ids take the bits of N - 1.
+KeyLayout key_layout(const BuildFlags &f, int64_t N) {
+    KeyLayout L{};
+    const uint32_t node_or = static_cast<uint32_t>(f.or_bits >> 32), node_and = static_cast<uint32_t>(f.and_bits >> 32);
+    const uint32_t ts_or = static_cast<uint32_t>(f.or_bits), ts_and = static_cast<uint32_t>(f.and_bits);
+    field_of(node_or ^ node_and, &L.node_lo, &L.node_bits);
+    field_of(ts_or ^ ts_and, &L.ts_lo, &L.ts_bits);
+    const uint32_t top = static_cast<uint32_t>(N - 1);
+    L.nbr_bits = top == 0 ? 0 : 32 - __builtin_clz(top);
+    L.node_konst = node_and & ~static_cast<uint32_t>(low_mask(L.node_bits) << L.node_lo);
+    L.ts_konst = ts_and & ~static_cast<uint32_t>(low_mask(L.ts_bits) << L.ts_lo);
+    L.packed = L.node_bits + L.ts_bits + L.nbr_bits <= 64;
+    return L;
+}
+
+// Key bits the sort must order by: the varying node and tskey bits where the
+// layout puts them (never the neighbour bits, so ties keep input order).
+uint64_t sort_bits(const KeyLayout &L, const BuildFlags &f) {
+    const uint64_t var = f.or_bits ^ f.and_bits;
+    if (!L.packed) return var;
+    const uint64_t nv = ((var >> 32) >> L.node_lo) & low_mask(L.node_bits);
+    const uint64_t tv = ((var & 0xFFFFFFFFull) >> L.ts_lo) & low_mask(L.ts_bits);
+    const int node_at = L.nbr_bits + L.ts_bits;
+    return (node_at < 64 ? nv << node_at : 0ull) | (tv << L.nbr_bits);
+}
+
 unsigned grid_for(int64_t n, int64_t cap = 1 << 16) {
     int64_t b = (n + kBlock - 1) / kBlock;
     if (b < 1) b = 1;
@@ -411,8 +526,7 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     }
 
     init_flags_kernel<<<1, 1, 0, st>>>(w.flags);
-    keys_kernel<<<grid_for(M), kBlock, 0, st>>>(src, dst, ts, m0, M, num_nodes, w.keys[0], w.vals[0],
-                                                w.flags);
+    reduce_kernel<<<grid_for(m0), kBlock, 0, st>>>(src, dst, ts, m0, M != m0, num_nodes, w.flags);
     if (launch_status() != TGL_OK) return TGL_EDEVICE;
     BuildFlags hf{};
     if (hipMemcpyAsync(&hf, w.flags, sizeof(hf), hipMemcpyDeviceToHost, st) != hipSuccess)
@@ -420,11 +534,15 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     if (hipStreamSynchronize(st) != hipSuccess) return TGL_EDEVICE;
     if (hf.err) return TGL_ERANGE;
 
-    const uint64_t varying = hf.or_bits ^ hf.and_bits;
+    const KeyLayout L = key_layout(hf, num_nodes);
+    const uint64_t varying = sort_bits(L, hf);
+    keys_kernel<<<grid_for(M), kBlock, 0, st>>>(src, dst, ts, m0, M, L, w.keys[0], w.vals[0]);
     int cur = 0;
     const int64_t nh = w.ntiles * kBins;
     const int64_t sc_tiles = scan_tiles(nh);
-    for (int shift = 0; shift < 64; shift += kRadixBits) {
+    // digits from the lowest sort bit up: in the packed layout the neighbour
+    // bits below it must not take part, or ties would leave input order
+    for (int shift = L.packed ? L.nbr_bits : 0; shift < 64; shift += kRadixBits) {
         if (((varying >> shift) & (kBins - 1)) == 0) continue;   // every key has this digit
         radix_upsweep_kernel<<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift,
                                                                                 w.hist, w.ntiles);
@@ -438,16 +556,23 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
         cur ^= 1;
     }
-    emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes,
-                                               indptr, reinterpret_cast<int4 *>(entries), ts_out);
-    // first timestamps, compact, into the sort's spare key buffer when they fit
-    // (8 bytes per entry), else read from the node records
+    // Each node's first timestamp, read from the sorted keys into the sort's
+    // spare key buffer (8 bytes per entry) when it fits, so that the entries
+    // are written with their neighbour-first hints; otherwise the hints are
+    // set afterwards from the node records.
     float *const first = num_nodes <= 2 * M ? reinterpret_cast<float *>(w.keys[cur ^ 1]) : nullptr;
+    if (first) {
+        fill_float_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(first, num_nodes, __builtin_inff());
+        first_ts_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], M, L, first);
+    }
+    emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes, L,
+                                               first, indptr, reinterpret_cast<int4 *>(entries), ts_out);
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
-                                                             reinterpret_cast<int4 *>(nodes_out), first);
-    first_hint_kernel<<<grid_for(M), kBlock, 0, st>>>(
-        reinterpret_cast<int4 *>(entries), ts_out, M,
-        first ? first : reinterpret_cast<const float *>(nodes_out) + 2, first ? 1 : 32, num_nodes);
+                                                             reinterpret_cast<int4 *>(nodes_out), nullptr);
+    if (!first)
+        first_hint_kernel<<<grid_for(M), kBlock, 0, st>>>(reinterpret_cast<int4 *>(entries), ts_out, M,
+                                                          reinterpret_cast<const float *>(nodes_out) + 2, 32,
+                                                          num_nodes);
     if (ts_index_out && M > 0) {
         const int64_t L = tgl_index_len(M);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts_out, L, ts_index_out);

@@ -173,6 +173,42 @@ def test_build_range_errors(torch):
             assert e.value.status == -2
 
 
+def test_build_key_layouts(torch):
+    """Sort keys of both forms: packed (node field, timestamp field and
+    neighbour id in 64 bits, the neighbour below the sort digits) and plain
+    (node << 32 | timestamp key), fields with no varying bit (one owner, one
+    timestamp, one node), ties on every key, and graphs with more nodes than
+    twice the entries, whose hints are set after the node records."""
+    rng = np.random.default_rng(1234)
+    N20 = 1 << 20
+    cases = []
+    for und in (False, True):
+        m0 = 3000
+        cases += [
+            ("plain: random float ts, N=2^20", N20, rng.integers(0, N20, m0), rng.integers(0, N20, m0),
+             rng.uniform(-1e6, 1e6, m0), und),
+            ("packed: years, N=2^20", N20, rng.integers(0, N20, m0), rng.integers(0, N20, m0),
+             rng.integers(1900, 2022, m0), und),
+            ("packed: one owner", 5000, np.full(m0, 77), rng.integers(0, 5000, m0), rng.integers(0, 50, m0), und),
+            ("packed: one timestamp", 5000, rng.integers(0, 5000, m0), rng.integers(0, 5000, m0),
+             np.full(m0, 3.5), und),
+            ("packed: one node", 1, np.zeros(m0), np.zeros(m0), rng.integers(0, 9, m0), und),
+            ("plain: one owner, random ts", N20, np.full(m0, N20 - 1), rng.integers(0, N20, m0),
+             rng.uniform(-1e30, 1e30, m0), und),
+            ("packed: N > 2M", 4000, rng.integers(0, 4000, 300), rng.integers(0, 4000, 300),
+             rng.integers(0, 20, 300), und),
+            ("plain: N > 2M", N20, rng.integers(0, N20, 300), rng.integers(0, N20, 300),
+             rng.uniform(0, 1e8, 300), und),
+        ]
+    for what, N, src, dst, ts, und in cases:
+        src, dst, ts = src.astype(np.int32), dst.astype(np.int32), ts.astype(np.float32)
+        eid = rng.integers(0, 2**40, len(src)).astype(np.int64) if und else None
+        announce("key layout: %s und=%s" % (what, und))
+        want = oracle.build_tcsr(src, dst, ts, eid, N, und)
+        g = gpu_build(src, dst, ts, eid, N, und)
+        assert_tcsr_equal(tcsr_to_host(g), want, "%s und=%s" % (what, und))
+
+
 def test_degenerate_cases(torch):
     # empty graph: every root PAD; zero roots; single-node graph with a self-loop
     announce("empty graph")
