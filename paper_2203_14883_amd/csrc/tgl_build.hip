@@ -281,58 +281,149 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     }
 }
 
-// first[x] = timestamp of node x's first entry in the sorted keys (the caller
-// fills first with +inf beforehand, for nodes without entries).
-__global__ __launch_bounds__(kBlock) void first_ts_kernel(const uint64_t *__restrict__ keys, int64_t M,
-                                                          const KeyLayout L, float *__restrict__ first) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
-        const uint64_t k = keys[p];
-        const uint32_t u = key_node(L, k);
-        if (p == 0 || key_node(L, keys[p - 1]) != u) first[u] = key_ts(key_tskey(L, k));
+// Each node's first timestamp as a value of type F that orders like it: the
+// float itself, or (packed layout, F = uint8_t / uint16_t) the key's
+// timestamp field, whose bits outside the field are the same in every entry.
+template <class F>
+__device__ __forceinline__ F first_value(const KeyLayout &L, uint64_t k) {
+    if constexpr (sizeof(F) == sizeof(float)) {
+        return key_ts(key_tskey(L, k));
+    } else {
+        return static_cast<F>((k >> L.nbr_bits) & low_mask(L.ts_bits));
     }
 }
 
-__global__ __launch_bounds__(kBlock) void fill_float_kernel(float *__restrict__ a, int64_t n, float value) {
+// A value above every first_value<F>, for nodes without entries: +inf, or all
+// ones (not below any field value, which decides the hint as +inf does).
+template <class F>
+__host__ __device__ __forceinline__ F first_none() {
+    if constexpr (sizeof(F) == sizeof(float)) {
+        return __builtin_inff();
+    } else {
+        return static_cast<F>(~static_cast<F>(0));
+    }
+}
+
+// Entries handled per lane by the wavefront-tiled kernels below: a wavefront
+// takes kEmitPerLane * 64 consecutive sorted entries, lane l the entries
+// base + l + 64 j, so every load and store of a round is coalesced and all of
+// them are in flight together.
+constexpr int kEmitPerLane = 4;
+constexpr int kEmitSpan = kEmitPerLane * kWave;
+
+// 64-bit lane shuffle (two 32-bit halves).
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+    const uint32_t lo = static_cast<uint32_t>(__shfl(static_cast<int>(static_cast<uint32_t>(v)), src, kWave));
+    const uint32_t hi = static_cast<uint32_t>(__shfl(static_cast<int>(static_cast<uint32_t>(v >> 32)), src, kWave));
+    return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Sorted keys base + l + 64 j (j < kEmitPerLane) and the key before each:
+// the lane below, lane 63 of the previous round, or keys[base - 1].  Entries
+// at or past M get key ~0 (never read as an owner).
+__device__ __forceinline__ void load_keys_prev(const uint64_t *__restrict__ keys, int64_t M, int64_t base, int lane,
+                                               uint64_t (&key)[kEmitPerLane], uint64_t (&prev)[kEmitPerLane]) {
+#pragma unroll
+    for (int j = 0; j < kEmitPerLane; j++) {
+        const int64_t p = base + j * kWave + lane;
+        key[j] = p < M ? keys[p] : ~0ull;
+    }
+    const uint64_t before = base > 0 ? keys[base - 1] : ~0ull;   // same address in every lane
+#pragma unroll
+    for (int j = 0; j < kEmitPerLane; j++) {
+        const uint64_t below = shfl64(key[j], lane == 0 ? 0 : lane - 1);
+        const uint64_t wrap = j > 0 ? shfl64(key[j - 1], kWave - 1) : before;
+        prev[j] = lane == 0 ? wrap : below;
+    }
+}
+
+// first[x] = first_value of node x's first entry in the sorted keys (the
+// caller fills first with first_none beforehand, for nodes without entries).
+template <class F>
+__global__ __launch_bounds__(kBlock) void first_ts_kernel(const uint64_t *__restrict__ keys, int64_t M,
+                                                          const KeyLayout L, F *__restrict__ first) {
+    const int lane = lane_id();
+    const int64_t wave = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / kWave;
+    const int64_t waves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+    for (int64_t base = wave * kEmitSpan; base < M; base += waves * kEmitSpan) {
+        uint64_t key[kEmitPerLane], prev[kEmitPerLane];
+        load_keys_prev(keys, M, base, lane, key, prev);
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++) {
+            const int64_t p = base + j * kWave + lane;
+            const uint32_t u = key_node(L, key[j]);
+            if (p < M && (p == 0 || key_node(L, prev[j]) != u)) first[u] = first_value<F>(L, key[j]);
+        }
+    }
+}
+
+template <class F>
+__global__ __launch_bounds__(kBlock) void fill_first_kernel(F *__restrict__ a, int64_t n) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n; i += stride) a[i] = value;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n; i += stride)
+        a[i] = first_none<F>();
 }
 
 // Writes entries[p] from the sorted (key, i) and fills indptr: node x starts
 // at the first p whose owner is >= x.  The neighbour comes from the key
-// (packed layout) or from the edge list; with `first` (each node's first
-// timestamp) the entry's TGL_NBR_FIRST hint is set here.
+// (packed layout) or from the edge list; with `first` (each node's
+// first_value) the entry's TGL_NBR_FIRST hint is set here.  Wavefront-tiled
+// like first_ts_kernel: each lane's gathers (neighbour, eid, first value) for
+// its kEmitPerLane entries are issued together.
+template <class F>
 __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict__ keys,
                                                       const uint32_t *__restrict__ vals, int64_t M,
                                                       int64_t m0, const int32_t *__restrict__ src,
                                                       const int32_t *__restrict__ dst,
                                                       const int64_t *__restrict__ eid, int64_t N,
-                                                      const KeyLayout L, const float *__restrict__ first,
+                                                      const KeyLayout L, const F *__restrict__ first,
                                                       int64_t *__restrict__ indptr,
                                                       int4 *__restrict__ ent,
                                                       float *__restrict__ ts_out) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
-        const uint64_t key = keys[p];
-        int64_t i = static_cast<int64_t>(vals[p]);
-        if (i >= M) i = 0;       // never taken for a permutation; keeps loads in bounds
-        const int64_t u = static_cast<int64_t>(key_node(L, key));
-        const float t = key_ts(key_tskey(L, key));
-        const bool fwd = i < m0;
-        const int64_t k = fwd ? i : i - m0;
-        const int32_t v = L.packed ? static_cast<int32_t>(key & low_mask(L.nbr_bits)) : (fwd ? dst[k] : src[k]);
-        const int64_t e = eid ? eid[k] : k;
-        uint32_t vw = static_cast<uint32_t>(v);
-        if (first && v >= 0 && v < N && !(first[v] < t)) vw |= TGL_NBR_FIRST;
-        ent[p] = make_int4(static_cast<int>(vw), __float_as_int(t), static_cast<int>(static_cast<uint32_t>(e)),
-                           static_cast<int>(static_cast<uint64_t>(e) >> 32));
-        ts_out[p] = t;
-        // owners are in [0, N) after validation; the clamps only bound the stores
-        const int64_t uprev = p == 0 ? -1 : static_cast<int64_t>(key_node(L, keys[p - 1]));
-        const int64_t x1 = u < N ? u : N - 1;
-        for (int64_t x = uprev + 1; x <= x1; x++) indptr[x] = p;
-        if (p == M - 1)
-            for (int64_t x = (u < N ? u : N - 1) + 1; x <= N; x++) indptr[x] = M;
+    const int lane = lane_id();
+    const int64_t wave = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / kWave;
+    const int64_t waves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+    for (int64_t base = wave * kEmitSpan; base < M; base += waves * kEmitSpan) {
+        uint64_t key[kEmitPerLane], prev[kEmitPerLane];
+        int64_t k[kEmitPerLane];
+        bool fwd[kEmitPerLane];
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++) {
+            const int64_t p = base + j * kWave + lane;
+            int64_t i = p < M ? static_cast<int64_t>(vals[p]) : 0;
+            if (i >= M) i = 0;   // never taken for a permutation; keeps loads in bounds
+            fwd[j] = i < m0;
+            k[j] = fwd[j] ? i : i - m0;
+        }
+        load_keys_prev(keys, M, base, lane, key, prev);
+        int32_t v[kEmitPerLane];
+        int64_t e[kEmitPerLane];
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++) {
+            v[j] = L.packed ? static_cast<int32_t>(key[j] & low_mask(L.nbr_bits)) : (fwd[j] ? dst[k[j]] : src[k[j]]);
+            e[j] = eid ? eid[k[j]] : k[j];
+        }
+        bool hint[kEmitPerLane];
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++)
+            hint[j] = first && v[j] >= 0 && v[j] < N && !(first[v[j]] < first_value<F>(L, key[j]));
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++) {
+            const int64_t p = base + j * kWave + lane;
+            if (p >= M) continue;
+            const int64_t u = static_cast<int64_t>(key_node(L, key[j]));
+            const float t = key_ts(key_tskey(L, key[j]));
+            const uint32_t vw = static_cast<uint32_t>(v[j]) | (hint[j] ? TGL_NBR_FIRST : 0u);
+            ent[p] = make_int4(static_cast<int>(vw), __float_as_int(t), static_cast<int>(static_cast<uint32_t>(e[j])),
+                               static_cast<int>(static_cast<uint64_t>(e[j]) >> 32));
+            ts_out[p] = t;
+            // owners are in [0, N) after validation; the clamps only bound the stores
+            const int64_t uprev = p == 0 ? -1 : static_cast<int64_t>(key_node(L, prev[j]));
+            const int64_t x1 = u < N ? u : N - 1;
+            for (int64_t x = uprev + 1; x <= x1; x++) indptr[x] = p;
+            if (p == M - 1)
+                for (int64_t x = x1 + 1; x <= N; x++) indptr[x] = M;
+        }
     }
 }
 
@@ -560,13 +651,33 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     // spare key buffer (8 bytes per entry) when it fits, so that the entries
     // are written with their neighbour-first hints; otherwise the hints are
     // set afterwards from the node records.
-    float *const first = num_nodes <= 2 * M ? reinterpret_cast<float *>(w.keys[cur ^ 1]) : nullptr;
-    if (first) {
-        fill_float_kernel<<<grid_for(num_nodes), kBlock, 0, st>>>(first, num_nodes, __builtin_inff());
-        first_ts_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], M, L, first);
+    // A packed timestamp field of at most 16 bits stands in for the float, so
+    // that the neighbours' values are gathered from a smaller array.
+    const int fbytes = L.packed && L.ts_bits <= 8 ? 1 : (L.packed && L.ts_bits <= 16 ? 2 : 4);
+    void *const first = num_nodes * fbytes <= 8 * M ? static_cast<void *>(w.keys[cur ^ 1]) : nullptr;
+    const unsigned gm = grid_for(M), gn = grid_for(num_nodes);
+    int4 *const ent = reinterpret_cast<int4 *>(entries);
+    if (first && fbytes == 1) {
+        uint8_t *const f = static_cast<uint8_t *>(first);
+        fill_first_kernel<uint8_t><<<gn, kBlock, 0, st>>>(f, num_nodes);
+        first_ts_kernel<uint8_t><<<gm, kBlock, 0, st>>>(w.keys[cur], M, L, f);
+        emit_kernel<uint8_t><<<gm, kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes, L, f,
+                                                    indptr, ent, ts_out);
+    } else if (first && fbytes == 2) {
+        uint16_t *const f = static_cast<uint16_t *>(first);
+        fill_first_kernel<uint16_t><<<gn, kBlock, 0, st>>>(f, num_nodes);
+        first_ts_kernel<uint16_t><<<gm, kBlock, 0, st>>>(w.keys[cur], M, L, f);
+        emit_kernel<uint16_t><<<gm, kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes, L,
+                                                     f, indptr, ent, ts_out);
+    } else {
+        float *const f = static_cast<float *>(first);
+        if (f) {
+            fill_first_kernel<float><<<gn, kBlock, 0, st>>>(f, num_nodes);
+            first_ts_kernel<float><<<gm, kBlock, 0, st>>>(w.keys[cur], M, L, f);
+        }
+        emit_kernel<float><<<gm, kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes, L, f,
+                                                  indptr, ent, ts_out);
     }
-    emit_kernel<<<grid_for(M), kBlock, 0, st>>>(w.keys[cur], w.vals[cur], M, m0, src, dst, eid, num_nodes, L,
-                                               first, indptr, reinterpret_cast<int4 *>(entries), ts_out);
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
                                                              reinterpret_cast<int4 *>(nodes_out), nullptr);
     if (!first)

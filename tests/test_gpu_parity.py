@@ -177,8 +177,10 @@ def test_build_key_layouts(torch):
     """Sort keys of both forms: packed (node field, timestamp field and
     neighbour id in 64 bits, the neighbour below the sort digits) and plain
     (node << 32 | timestamp key), fields with no varying bit (one owner, one
-    timestamp, one node), ties on every key, and graphs with more nodes than
-    twice the entries, whose hints are set after the node records."""
+    timestamp, one node), timestamp fields of 1, 8 and 10 bits (the
+    neighbours' first timestamps then compared as 8- or 16-bit fields), ties on
+    every key, and graphs with more nodes than twice the entries, whose hints
+    are set after the node records."""
     rng = np.random.default_rng(1234)
     N20 = 1 << 20
     cases = []
@@ -193,6 +195,10 @@ def test_build_key_layouts(torch):
             ("packed: one timestamp", 5000, rng.integers(0, 5000, m0), rng.integers(0, 5000, m0),
              np.full(m0, 3.5), und),
             ("packed: one node", 1, np.zeros(m0), np.zeros(m0), rng.integers(0, 9, m0), und),
+            ("packed: 10-bit timestamp field", 5000, rng.integers(0, 5000, m0), rng.integers(0, 5000, m0),
+             rng.integers(1024, 2048, m0), und),
+            ("packed: 1-bit timestamp field", 700, rng.integers(0, 700, m0), rng.integers(0, 700, m0),
+             rng.choice([6.0, 7.0], m0), und),
             ("plain: one owner, random ts", N20, np.full(m0, N20 - 1), rng.integers(0, N20, m0),
              rng.uniform(-1e30, 1e30, m0), und),
             ("packed: N > 2M", 4000, rng.integers(0, 4000, 300), rng.integers(0, 4000, 300),
