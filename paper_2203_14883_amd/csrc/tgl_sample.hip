@@ -228,6 +228,65 @@ __device__ __forceinline__ void search_n(const float *__restrict__ arr, uint32_t
     for (int i = 0; i < NE; i++) lo[i] = count_in<G>(r[i], lo[i], hi[i], v[i]);
 }
 
+// A node's run [a, b) and its first and last timestamps: where a threshold
+// falls in it is estimated by linear interpolation between them.
+struct RunShape {
+    uint32_t a, b;
+    float first, last;
+};
+
+// Estimated position of threshold v in the run (lower bound: the count of
+// timestamps below v, plus a), and the spread of that estimate: if the
+// run's timestamps were independent draws between first and last, the count
+// below v would be binomial, with standard deviation at most sqrt(b - a) / 2.
+__device__ __forceinline__ void run_estimate(const RunShape &rs, float v, uint32_t &pos, uint32_t &spread) {
+    const float n = static_cast<float>(rs.b - rs.a);
+    float f = (v - rs.first) / (rs.last - rs.first);
+    if (!(f >= 0.0f)) f = f < 0.0f ? 0.0f : 0.5f;                 // below the run, or NaN
+    if (f > 1.0f) f = 1.0f;
+    const float o = f * n;                                         // <= n
+    pos = rs.a + (o < n ? static_cast<uint32_t>(o) : rs.b - rs.a);
+    spread = static_cast<uint32_t>(0.5f * __builtin_sqrtf(n)) + 1u;
+}
+
+// Probe g of a guided round: c + (g - G/2) d + d/2, clamped into [lo, hi).
+// Non-decreasing in g.
+template <int G>
+__device__ __forceinline__ uint32_t guided_pos(uint32_t lo, uint32_t hi, uint32_t c, uint32_t d, int g) {
+    const int64_t q = static_cast<int64_t>(c) + (static_cast<int64_t>(g) - G / 2) * static_cast<int64_t>(d) +
+                      static_cast<int64_t>(d / 2);
+    const int64_t last = static_cast<int64_t>(hi) - 1;
+    return static_cast<uint32_t>(q < static_cast<int64_t>(lo) ? static_cast<int64_t>(lo) : (q > last ? last : q));
+}
+
+// One round of the search of a sorted stretch of arr, guided by estimates:
+// for each i whose range [lo[i], hi[i]) is longer than a held stretch, the G
+// lanes probe positions d[i] apart around c[i].  The probes below v[i] form
+// a prefix (arr is sorted and the positions do not decrease), so the answer
+// lies after the last of them and at or before the next: the range shrinks
+// to about d[i] when the estimate is off by less than G/2 spacings, and
+// never grows.  lo[i] + #{p in [lo[i], hi[i]): arr[p] < v[i]} is unchanged.
+template <int G, int NE>
+__device__ __forceinline__ void guided_round(const float *__restrict__ arr, uint32_t (&lo)[NE], uint32_t (&hi)[NE],
+                                             const float (&v)[NE], const uint32_t (&c)[NE], const uint32_t (&d)[NE],
+                                             int gl) {
+    float probe[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        probe[i] = 0.0f;
+        if (hi[i] - lo[i] > HeldRun<G>::span) probe[i] = arr[guided_pos<G>(lo[i], hi[i], c[i], d[i], gl)];
+    }
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        if (hi[i] - lo[i] > HeldRun<G>::span) {     // group-uniform
+            const int n = __popcll(group_ballot<G>(probe[i] < v[i]));
+            const uint32_t nlo = n > 0 ? guided_pos<G>(lo[i], hi[i], c[i], d[i], n - 1) + 1 : lo[i];
+            if (n < G) hi[i] = guided_pos<G>(lo[i], hi[i], c[i], d[i], n);
+            lo[i] = nlo;
+        }
+    }
+}
+
 // Positions below NE thresholds in the time-sorted run [lo0, hi0) of the
 // timestamp array (M entries): out[i] = lo0 + #{p in [lo0, hi0): ts[p] < v[i]}
 // for each i with act[i] (out[i] = lo0 otherwise).  rec, when not null, is the
@@ -235,15 +294,17 @@ __device__ __forceinline__ void search_n(const float *__restrict__ arr, uint32_t
 // then read from there.  A run of at most one held stretch is loaded once and
 // serves every threshold.  A run long enough to
 // need more than one probe round is first narrowed on the search index tsx
-// (nx samples, tsx[j] = ts[j * TGL_INDEX_STRIDE]) when there is one: with r
+// (nx samples, tsx[j] = ts[j * TGL_INDEX_STRIDE]) when there is one, starting
+// with a round guided by the run shape rs (the run that holds the stretch,
+// lo0 its start): with r
 // the samples inside the run below v[i], the answer lies after sample r - 1
 // and at or before sample r, fewer than TGL_INDEX_STRIDE timestamps.
 template <int G, int NE>
 __device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uint32_t M,
                                               const float *__restrict__ tsx, uint32_t nx,
                                               const int4 *__restrict__ rec, uint32_t lo0, uint32_t hi0,
-                                              const float (&v)[NE], const bool (&act)[NE], uint32_t (&out)[NE],
-                                              int gl) {
+                                              const RunShape &rs, const float (&v)[NE], const bool (&act)[NE],
+                                              uint32_t (&out)[NE], int gl) {
     constexpr uint32_t X = TGL_INDEX_STRIDE;
     if (rec || hi0 - lo0 <= HeldRun<G>::span) {    // group-uniform: one load serves every bound
         const HeldRun<G> r = rec ? load_inline<G>(rec, lo0, gl) : load_run<G>(tsa, lo0, hi0, M, gl);
@@ -256,11 +317,17 @@ __device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uin
         // samples j in [ja, jb) are the positions j * X inside [lo0, hi0)
         const uint32_t ja = lo0 / X + (lo0 % X != 0);
         const uint32_t jb = hi0 / X + (hi0 % X != 0);
+        uint32_t gc[NE], gd[NE];
 #pragma unroll
         for (int i = 0; i < NE; i++) {
             lo[i] = ja;
             hi[i] = act[i] ? jb : ja;
+            uint32_t pos, spread;
+            run_estimate(rs, v[i], pos, spread);
+            gc[i] = pos / X;
+            gd[i] = spread / X > 0 ? spread / X : 1u;
         }
+        guided_round<G, NE>(tsx, lo, hi, v, gc, gd, gl);
         search_n<G, NE>(tsx, nx, lo, hi, v, gl);
 #pragma unroll
         for (int i = 0; i < NE; i++) {
@@ -503,7 +570,7 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, int32_t 
             for (int u = 0; u < NE; u++) ei[u] = i0 + u;
             from_pointers<G, NE>(p, x, a, b, ei, v, act, cs, gl);
         } else {
-            count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, nullptr, a, top, v, act, cs, gl);
+            count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, nullptr, a, top, RunShape{a, b, first, last}, v, act, cs, gl);
         }
 #pragma unroll
         for (int u = 0; u < NE; u++) {
@@ -715,7 +782,8 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                         for (int u = 0; u < NE; u++) ei[u] = i0 + u;
                         from_pointers<G, NE>(p, xi, a, b, ei, vv, act, cs, gl);
                     } else {
-                        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, rec, a, top, vv, act, cs, gl);
+                        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, rec, a, top, RunShape{a, b, first, last}, vv,
+                                             act, cs, gl);
                     }
 #pragma unroll
                     for (int u = 0; u < NE; u++) {
@@ -810,7 +878,7 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
         for (int i = 0; i < NB; i++) ei[i] = i;             // hop 1 with one window: edges t and t - D
         from_pointers<G, NB>(p, x, a, b, ei, v, act, cs, gl);
     } else {
-        count_below_n<G, NB>(p.tsa, M, p.tsx, p.nx, rec, a, b, v, act, cs, gl);
+        count_below_n<G, NB>(p.tsa, M, p.tsx, p.nx, rec, a, b, RunShape{a, b, first, last}, v, act, cs, gl);
     }
     hi = act[0] ? cs[0] : c[0];
     lo = NB == 1 ? a : (act[NB - 1] ? cs[NB - 1] : c[NB - 1]);
