@@ -265,6 +265,45 @@ def test_long_runs_and_off_grid_window_edges(torch):
                 assert_hops_equal(got, want, "S=%d D=%s %s %s" % (S, D, mode, what))
 
 
+def test_guided_search_on_skewed_runs(torch):
+    """The first round on the search index places its probes by interpolating
+    between a run's first and last timestamps; the window edges must not
+    depend on how good that guess is.  Long runs (indexed search) whose
+    timestamps are far from evenly spread -- nearly all at the start, nearly
+    all at the end, geometric, two clusters, one value with two outliers, and
+    an even spread for contrast -- queried at entry timestamps, between them
+    and outside the run, with 1-3 snapshots and 1-2 hops."""
+    rng = np.random.default_rng(4242)
+    L = 60_000
+    runs = [
+        np.sort(rng.random(L) * 1e6),                                           # even
+        np.sort(np.where(rng.random(L) < 0.98, rng.random(L), 1e6 * rng.random(L))),   # piled at the start
+        np.sort(np.where(rng.random(L) < 0.98, 1e6 - rng.random(L), 1e6 * rng.random(L))),   # piled at the end
+        np.sort(2.0 ** (rng.random(L) * 40.0)),                                 # geometric over 12 decades
+        np.sort(np.concatenate([rng.random(L // 2) * 10.0, 9.9e5 + rng.random(L - L // 2) * 10.0])),  # two clusters
+        np.concatenate([[-1e9], np.full(L - 2, 5.0), [1e9]]),                   # one value, two outliers
+    ]
+    N = len(runs)
+    src = np.concatenate([np.full(L, x, np.int32) for x in range(N)])
+    dst = rng.integers(0, N, len(src)).astype(np.int32)
+    ts = np.concatenate(runs).astype(np.float32)
+    want_g = oracle.build_tcsr(src, dst, ts, None, N, False)
+    g = gpu_build(src, dst, ts, None, N, False)
+    assert_tcsr_equal(tcsr_to_host(g), want_g, "skewed runs")
+    R = 4000
+    roots = rng.integers(0, N, R).astype(np.int32)
+    rts = ts[rng.integers(0, len(ts), R)].copy()                                 # equal to timestamps
+    rts[R // 4: R // 2] = np.nextafter(rts[R // 4: R // 2], np.float32(np.inf))  # just above them
+    rts[R // 2: 3 * R // 4] = (rng.random(R // 4) * 2e6 - 5e5).astype(np.float32)   # anywhere, also outside
+    rts[3 * R // 4:] = np.float32(2.0) ** rng.integers(0, 41, R - 3 * R // 4).astype(np.float32)
+    for S, D in [(1, math.inf), (1, 3e4), (3, 1e3), (3, 2.5)]:
+        for mode, fan in (("recent", [10]), ("uniform", [10, 3])):
+            announce("skewed runs S=%d D=%s mode=%s" % (S, D, mode))
+            want = oracle.sample(want_g, roots, rts, fan, mode, S, D, 5, 0)
+            got = gpu_sample(g, roots, rts, fan, mode, S, D, 5, 0)
+            assert_hops_equal(got, want, "skewed runs S=%d D=%s %s" % (S, D, mode))
+
+
 def test_chunk_scheduled_batches(torch):
     """Batches of random chunk scheduling (Alg. 2) -- edge ranges that start at
     chunk offsets, not at the batch grid -- fused into one GPU call, against the
