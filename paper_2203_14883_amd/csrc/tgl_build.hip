@@ -25,8 +25,8 @@
 namespace tgl {
 namespace {
 
-constexpr int kRadixBits = 8;
-constexpr int kBins = 1 << kRadixBits;
+constexpr int kMaxRadixBits = 8;                  // digits of 7 or 8 bits
+constexpr int kBins = 1 << kMaxRadixBits;         // histogram rows per tile (the most digits can need)
 constexpr int kTileItems = 16;                    // keys per thread per radix tile
 constexpr int kTile = kBlock * kTileItems;        // 4096 keys
 constexpr int kWaves = kBlock / kWave;
@@ -157,11 +157,12 @@ __global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict_
     }
 }
 
-// Lanes of the wave whose (valid) digit equals this lane's digit.
+// Lanes of the wave whose (valid) BITS-bit digit equals this lane's digit.
+template <int BITS>
 __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
     uint64_t m = __ballot(valid);
 #pragma unroll
-    for (int b = 0; b < kRadixBits; b++) {
+    for (int b = 0; b < BITS; b++) {
         const bool bit = (d >> b) & 1u;
         const uint64_t bb = __ballot(bit);
         m &= bit ? bb : ~bb;
@@ -169,13 +170,17 @@ __device__ __forceinline__ uint64_t match_digit(uint32_t d, bool valid) {
     return m;
 }
 
-// Per-tile digit counts, stored digit-major: hist[d * ntiles + tile].
+// Per-tile digit counts, stored digit-major: hist[d * ntiles + tile], for the
+// 2^BITS digits (key >> shift) & (2^BITS - 1).
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *__restrict__ keys,
                                                                int64_t M, int shift,
                                                                uint32_t *__restrict__ hist,
                                                                int64_t ntiles) {
-    __shared__ uint32_t cnt[kBins];
-    cnt[threadIdx.x] = 0;
+    constexpr int B = 1 << BITS;
+    static_assert(B <= kBlock, "one thread per digit");
+    __shared__ uint32_t cnt[B];
+    if (threadIdx.x < B) cnt[threadIdx.x] = 0;
     __syncthreads();
     const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
     const uint64_t lane_bit = 1ull << lane_id();
@@ -183,32 +188,38 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *_
     for (int r = 0; r < kTileItems; r++) {
         const int64_t idx = base + static_cast<int64_t>(r) * kBlock + threadIdx.x;
         const bool valid = idx < M;
-        const uint32_t d = valid ? static_cast<uint32_t>(keys[idx] >> shift) & (kBins - 1) : 0u;
-        const uint64_t peers = match_digit(d, valid);
+        const uint32_t d = valid ? static_cast<uint32_t>(keys[idx] >> shift) & (B - 1) : 0u;
+        const uint64_t peers = match_digit<BITS>(d, valid);
         if (valid && (peers & (lane_bit - 1)) == 0) atomicAdd(&cnt[d], static_cast<uint32_t>(__popcll(peers)));
     }
     __syncthreads();
-    hist[static_cast<int64_t>(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
+    if (threadIdx.x < B) hist[static_cast<int64_t>(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
 }
 
-// Stable scatter of one tile by digit.  hist_off holds the exclusive scan of
-// hist (digit-major), i.e. where this tile's keys of digit d start.
+// Stable scatter of one tile by its BITS-bit digit.  hist_off holds the
+// exclusive scan of hist (digit-major), i.e. where this tile's keys of digit
+// d start.
+template <int BITS>
 __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     const uint64_t *__restrict__ kin, const uint32_t *__restrict__ vin, uint64_t *__restrict__ kout,
     uint32_t *__restrict__ vout, int64_t M, int shift, const uint32_t *__restrict__ hist_off,
     int64_t ntiles) {
+    constexpr int B = 1 << BITS;
+    static_assert(B <= kBlock, "one thread per digit");
     __shared__ uint64_t sk[kTile];
     __shared__ uint32_t sv[kTile];
-    __shared__ uint32_t wcnt[kWaves][kBins];
-    __shared__ uint32_t bdo[kBins];
-    __shared__ uint32_t gofs[kBins];
+    __shared__ uint32_t wcnt[kWaves][B];
+    __shared__ uint32_t bdo[B];
+    __shared__ uint32_t gofs[B];
     __shared__ uint32_t scan_lds[kBlock / kWave];
 
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const uint64_t lane_bit = 1ull << lane;
+    if (threadIdx.x < B) {
 #pragma unroll
-    for (int i = 0; i < kWaves; i++) wcnt[i][threadIdx.x] = 0;
+        for (int i = 0; i < kWaves; i++) wcnt[i][threadIdx.x] = 0;
+    }
     __syncthreads();
 
     const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kTile;
@@ -227,8 +238,8 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     for (int r = 0; r < kTileItems; r++) {
         const int64_t idx = base + static_cast<int64_t>(r) * kWave + lane;
         const bool valid = idx < M;
-        const uint32_t d = static_cast<uint32_t>(key[r] >> shift) & (kBins - 1);
-        const uint64_t peers = match_digit(d, valid);
+        const uint32_t d = static_cast<uint32_t>(key[r] >> shift) & (B - 1);
+        const uint64_t peers = match_digit<BITS>(d, valid);
         const uint64_t below = peers & (lane_bit - 1);
         const uint32_t prior = wcnt[w][d];
         rank[r] = prior + static_cast<uint32_t>(__popcll(below));
@@ -244,15 +255,18 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     {
         const int d = threadIdx.x;
         uint32_t run = 0;
+        if (d < B) {
 #pragma unroll
-        for (int i = 0; i < kWaves; i++) {
-            const uint32_t c = wcnt[i][d];
-            wcnt[i][d] = run;
-            run += c;
+            for (int i = 0; i < kWaves; i++) {
+                const uint32_t c = wcnt[i][d];
+                wcnt[i][d] = run;
+                run += c;
+            }
+            gofs[d] = hist_off[static_cast<int64_t>(d) * ntiles + blockIdx.x];
         }
-        gofs[d] = hist_off[static_cast<int64_t>(d) * ntiles + blockIdx.x];
         uint32_t total;
-        bdo[d] = block_exclusive_sum<uint32_t>(run, scan_lds, &total);
+        const uint32_t ex = block_exclusive_sum<uint32_t>(run, scan_lds, &total);   // every thread takes part
+        if (d < B) bdo[d] = ex;
     }
     __syncthreads();
 
@@ -260,7 +274,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     for (int r = 0; r < kTileItems; r++) {
         const int64_t idx = base + static_cast<int64_t>(r) * kWave + lane;
         if (idx < M) {
-            const uint32_t d = static_cast<uint32_t>(key[r] >> shift) & (kBins - 1);
+            const uint32_t d = static_cast<uint32_t>(key[r] >> shift) & (B - 1);
             const uint32_t pos = bdo[d] + wcnt[w][d] + rank[r];
             sk[pos] = key[r];
             sv[pos] = val[r];
@@ -272,7 +286,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     const int n = left < kTile ? static_cast<int>(left) : kTile;
     for (int i = threadIdx.x; i < n; i += kBlock) {
         const uint64_t k = sk[i];
-        const uint32_t d = static_cast<uint32_t>(k >> shift) & (kBins - 1);
+        const uint32_t d = static_cast<uint32_t>(k >> shift) & (B - 1);
         const int64_t g = static_cast<int64_t>(gofs[d]) + (i - static_cast<int64_t>(bdo[d]));
         if (g >= 0 && g < M) {     // always true for consistent counts; keeps stores in bounds
             kout[g] = k;
@@ -629,21 +643,42 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     const uint64_t varying = sort_bits(L, hf);
     keys_kernel<<<grid_for(M), kBlock, 0, st>>>(src, dst, ts, m0, M, L, w.keys[0], w.vals[0]);
     int cur = 0;
-    const int64_t nh = w.ntiles * kBins;
+    // Digits from the lowest varying sort bit up (in the packed layout the
+    // neighbour bits lie below every sort bit: they must not take part, or
+    // ties would leave input order).  The span from there to the highest
+    // varying bit is cut into as few passes as 8-bit digits allow, `step`
+    // bits apart (c4: 35 bits, five 7-bit digits).  A pass reads a digit of
+    // kb = 7 or 8 bits at its shift; when step is below 7 the digits overlap,
+    // which leaves the LSD order unchanged.  A digit on which every key agrees
+    // is skipped.
+    const int lo_bit = varying == 0 ? 0 : __builtin_ctzll(varying);   // packed: never below the neighbour bits
+    const int hi_bit = varying == 0 ? lo_bit : 64 - __builtin_clzll(varying);
+    const int span = hi_bit > lo_bit ? hi_bit - lo_bit : 0;
+    const int npass = (span + kMaxRadixBits - 1) / kMaxRadixBits;
+    const int step = npass > 0 ? (span + npass - 1) / npass : kMaxRadixBits;
+    const int kb = step == 8 ? 8 : 7;
+    const int64_t nh = w.ntiles << kb;
     const int64_t sc_tiles = scan_tiles(nh);
-    // digits from the lowest sort bit up: in the packed layout the neighbour
-    // bits below it must not take part, or ties would leave input order
-    for (int shift = L.packed ? L.nbr_bits : 0; shift < 64; shift += kRadixBits) {
-        if (((varying >> shift) & (kBins - 1)) == 0) continue;   // every key has this digit
-        radix_upsweep_kernel<<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift,
-                                                                                w.hist, w.ntiles);
+    for (int pass = 0; pass < npass; pass++) {
+        const int shift = lo_bit + pass * step;
+        if (((varying >> shift) & ((uint64_t(1) << kb) - 1)) == 0) continue;   // every key has this digit
+        if (kb == 8)
+            radix_upsweep_kernel<8><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift, w.hist,
+                                                                                       w.ntiles);
+        else
+            radix_upsweep_kernel<7><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift, w.hist,
+                                                                                       w.ntiles);
         scan_reduce_kernel<uint32_t><<<static_cast<unsigned>(sc_tiles), kBlock, 0, st>>>(
             w.hist, nh, nullptr, w.partials);
         launch_scan_partials(w.partials, sc_tiles, nullptr, st);
         scan_apply_kernel<uint32_t, uint32_t><<<static_cast<unsigned>(sc_tiles), kBlock, 0, st>>>(
             w.hist, w.hist, nh, nullptr, w.partials);
-        radix_downsweep_kernel<<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(
-            w.keys[cur], w.vals[cur], w.keys[cur ^ 1], w.vals[cur ^ 1], M, shift, w.hist, w.ntiles);
+        if (kb == 8)
+            radix_downsweep_kernel<8><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(
+                w.keys[cur], w.vals[cur], w.keys[cur ^ 1], w.vals[cur ^ 1], M, shift, w.hist, w.ntiles);
+        else
+            radix_downsweep_kernel<7><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(
+                w.keys[cur], w.vals[cur], w.keys[cur ^ 1], w.vals[cur ^ 1], M, shift, w.hist, w.ntiles);
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
         cur ^= 1;
     }
