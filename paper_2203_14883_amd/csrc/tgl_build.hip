@@ -32,6 +32,24 @@ constexpr int kTile = kBlock * kTileItems;        // 4096 keys
 constexpr int kWaves = kBlock / kWave;
 constexpr int kWaveTile = kTile / kWaves;         // 1024 keys per wavefront
 constexpr int64_t kMaxEntries = (int64_t(1) << 32) - 1;
+constexpr int kXcds = 8;                          // accelerator dies, each with its own L2
+
+// Tile of block b in the radix kernels.  Workgroups are dealt to the dies
+// round-robin, so block b runs on die b % 8; each die takes a contiguous
+// range of tiles instead, so that neighbouring tiles -- which write adjacent
+// counts of each histogram row and adjacent pieces of each digit's output
+// run -- share one L2, where their partial lines merge.  Returns -1 for the
+// blocks past the last tile (the grid is a multiple of 8).
+__device__ __forceinline__ int64_t radix_tile(int64_t ntiles) {
+    const int64_t per = (ntiles + kXcds - 1) / kXcds;
+    const int64_t b = blockIdx.x;
+    const int64_t t = (b % kXcds) * per + b / kXcds;
+    return t < ntiles ? t : -1;
+}
+
+unsigned radix_grid(int64_t ntiles) {
+    return static_cast<unsigned>((ntiles + kXcds - 1) / kXcds * kXcds);
+}
 
 struct BuildFlags {
     uint32_t err;
@@ -180,9 +198,11 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *_
     constexpr int B = 1 << BITS;
     static_assert(B <= kBlock, "one thread per digit");
     __shared__ uint32_t cnt[B];
+    const int64_t tile = radix_tile(ntiles);
+    if (tile < 0) return;                           // block-uniform
     if (threadIdx.x < B) cnt[threadIdx.x] = 0;
     __syncthreads();
-    const int64_t base = static_cast<int64_t>(blockIdx.x) * kTile;
+    const int64_t base = tile * kTile;
     const uint64_t lane_bit = 1ull << lane_id();
 #pragma unroll 4
     for (int r = 0; r < kTileItems; r++) {
@@ -193,7 +213,7 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *_
         if (valid && (peers & (lane_bit - 1)) == 0) atomicAdd(&cnt[d], static_cast<uint32_t>(__popcll(peers)));
     }
     __syncthreads();
-    if (threadIdx.x < B) hist[static_cast<int64_t>(threadIdx.x) * ntiles + blockIdx.x] = cnt[threadIdx.x];
+    if (threadIdx.x < B) hist[static_cast<int64_t>(threadIdx.x) * ntiles + tile] = cnt[threadIdx.x];
 }
 
 // Stable scatter of one tile by its BITS-bit digit.  hist_off holds the
@@ -216,13 +236,15 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
     const int w = threadIdx.x / kWave;
     const int lane = lane_id();
     const uint64_t lane_bit = 1ull << lane;
+    const int64_t tile = radix_tile(ntiles);
+    if (tile < 0) return;                           // block-uniform
     if (threadIdx.x < B) {
 #pragma unroll
         for (int i = 0; i < kWaves; i++) wcnt[i][threadIdx.x] = 0;
     }
     __syncthreads();
 
-    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kTile;
+    const int64_t tile0 = tile * kTile;
     const int64_t base = tile0 + static_cast<int64_t>(w) * kWaveTile;
     uint64_t key[kTileItems];
     uint32_t val[kTileItems];
@@ -262,7 +284,7 @@ __global__ __launch_bounds__(kBlock) void radix_downsweep_kernel(
                 wcnt[i][d] = run;
                 run += c;
             }
-            gofs[d] = hist_off[static_cast<int64_t>(d) * ntiles + blockIdx.x];
+            gofs[d] = hist_off[static_cast<int64_t>(d) * ntiles + tile];
         }
         uint32_t total;
         const uint32_t ex = block_exclusive_sum<uint32_t>(run, scan_lds, &total);   // every thread takes part
@@ -663,10 +685,10 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         const int shift = lo_bit + pass * step;
         if (((varying >> shift) & ((uint64_t(1) << kb) - 1)) == 0) continue;   // every key has this digit
         if (kb == 8)
-            radix_upsweep_kernel<8><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift, w.hist,
+            radix_upsweep_kernel<8><<<radix_grid(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift, w.hist,
                                                                                        w.ntiles);
         else
-            radix_upsweep_kernel<7><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift, w.hist,
+            radix_upsweep_kernel<7><<<radix_grid(w.ntiles), kBlock, 0, st>>>(w.keys[cur], M, shift, w.hist,
                                                                                        w.ntiles);
         scan_reduce_kernel<uint32_t><<<static_cast<unsigned>(sc_tiles), kBlock, 0, st>>>(
             w.hist, nh, nullptr, w.partials);
@@ -674,10 +696,10 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         scan_apply_kernel<uint32_t, uint32_t><<<static_cast<unsigned>(sc_tiles), kBlock, 0, st>>>(
             w.hist, w.hist, nh, nullptr, w.partials);
         if (kb == 8)
-            radix_downsweep_kernel<8><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(
+            radix_downsweep_kernel<8><<<radix_grid(w.ntiles), kBlock, 0, st>>>(
                 w.keys[cur], w.vals[cur], w.keys[cur ^ 1], w.vals[cur ^ 1], M, shift, w.hist, w.ntiles);
         else
-            radix_downsweep_kernel<7><<<static_cast<unsigned>(w.ntiles), kBlock, 0, st>>>(
+            radix_downsweep_kernel<7><<<radix_grid(w.ntiles), kBlock, 0, st>>>(
                 w.keys[cur], w.vals[cur], w.keys[cur ^ 1], w.vals[cur ^ 1], M, shift, w.hist, w.ntiles);
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
         cur ^= 1;
