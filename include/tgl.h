@@ -499,6 +499,14 @@ tgl_status tgl_timer_read(int32_t kind, double *total_ms, int64_t *launches);
 /* Clears totals and recorded launches (keeps the events). */
 tgl_status tgl_timer_reset(void);
 
+/*
+ * Records only launches of the kinds whose bit is set in `kinds` (bit k for
+ * kind k; all kinds after tgl_timer_enable), so that a timed region carries
+ * the events of the kernels it measures and no others.  TGL_EINVAL for bits
+ * at or above TGL_TIMER_KINDS.
+ */
+tgl_status tgl_timer_select(uint32_t kinds);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,6 +23,7 @@ MOST_RECENT, UNIFORM = 0, 1
 BUILD_UNDIRECTED = 1
 MAX_HOPS, MAX_FANOUT, MAX_SNAPSHOTS = 8, 1024, 64
 TIMER_HOP1, TIMER_HOPN, TIMER_COMPACT, TIMER_BUILD, TIMER_GATHER, TIMER_TIMEENC, TIMER_MFG = 0, 1, 2, 3, 4, 5, 6
+TIMER_KINDS = 7
 OUT_F32, OUT_BF16 = 0, 1
 KEY_NODE, KEY_EDGE = 0, 1
 MAX_TABLES = 8
@@ -41,7 +42,7 @@ EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcs
            "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
            "tgl_sample_ex", "tgl_pointers_reset", "tgl_mfg_workspace", "tgl_mfg_export",
            "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
-           "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset")
+           "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset", "tgl_timer_select")
 
 
 class TglError(RuntimeError):
@@ -133,6 +134,8 @@ def lib() -> C.CDLL:
     L.tgl_timer_reset.argtypes = []
     L.tgl_timer_read.restype = i32
     L.tgl_timer_read.argtypes = [i32, C.POINTER(C.c_double), C.POINTER(C.c_int64)]
+    L.tgl_timer_select.restype = i32
+    L.tgl_timer_select.argtypes = [C.c_uint32]
     _lib = L
     return L
 
@@ -548,6 +551,14 @@ def timer_disable():
 
 def timer_reset():
     _check(lib().tgl_timer_reset(), "tgl_timer_reset")
+
+
+def timer_select(*kinds: int):
+    """Record only launches of the given timer kinds (none given: all)."""
+    mask = 0
+    for k in kinds:
+        mask |= 1 << int(k)
+    _check(lib().tgl_timer_select(mask if kinds else (1 << TIMER_KINDS) - 1), "tgl_timer_select")
 
 
 def timer_read(kind: int):

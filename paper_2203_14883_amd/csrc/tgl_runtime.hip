@@ -49,6 +49,7 @@ struct TimerState {
     std::vector<hipEvent_t> ev;        // 2 per slot
     std::vector<int> kind;             // kind of each used slot
     int used = 0;
+    uint32_t kinds = ~0u;              // bit k set: launches of kind k are recorded
 };
 TimerState &timers() {
     static TimerState t;
@@ -59,7 +60,7 @@ TimerState &timers() {
 int timer_begin(int k, hipStream_t s) {
     TimerState &t = timers();
     std::lock_guard<std::mutex> g(t.mu);
-    if (!t.on || t.used * 2 + 1 >= static_cast<int>(t.ev.size())) return -1;
+    if (!t.on || !((t.kinds >> k) & 1u) || t.used * 2 + 1 >= static_cast<int>(t.ev.size())) return -1;
     const int slot = t.used++;
     t.kind[slot] = k;
     if (hipEventRecord(t.ev[2 * slot], s) != hipSuccess) {
@@ -111,6 +112,7 @@ tgl_status tgl_timer_enable(int32_t capacity) {
         }
     }
     t.used = 0;
+    t.kinds = ~0u;
     t.on = true;
     return TGL_OK;
 }
@@ -123,6 +125,14 @@ tgl_status tgl_timer_disable(void) {
     t.kind.clear();
     t.used = 0;
     t.on = false;
+    return TGL_OK;
+}
+
+tgl_status tgl_timer_select(uint32_t kinds) {
+    if (kinds >> TGL_TIMER_KINDS) return TGL_EINVAL;
+    TimerState &t = timers();
+    std::lock_guard<std::mutex> g(t.mu);
+    t.kinds = kinds;
     return TGL_OK;
 }
 

@@ -164,6 +164,9 @@ def test_timer_argument_checks():
     assert L.tgl_timer_read(0, None, C.byref(n)) == B.EINVAL
     assert L.tgl_timer_enable(0) == B.EINVAL
     assert L.tgl_timer_read(0, C.byref(ms), C.byref(n)) == 0 and n.value == 0
+    assert L.tgl_timer_select(1 << 7) == B.EINVAL          # no kind 7
+    assert L.tgl_timer_select(0x7F) == 0 and L.tgl_timer_select(0) == 0
+    P.timer_select()                                        # back to every kind
 
 
 def _gather_call(n=10, per=1, nt=1, nbr=FAKE, eid=FAKE, count=None, **tab):
