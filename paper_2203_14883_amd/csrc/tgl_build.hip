@@ -124,54 +124,106 @@ __device__ __forceinline__ uint32_t key_tskey(const KeyLayout &L, uint64_t k) {
     return L.ts_konst | static_cast<uint32_t>(tf << L.ts_lo);
 }
 
+// Edges per thread and grid-stride round of the kernels that read the edge
+// list: their loads are issued together, one coalesced stream per array.
+constexpr int kEdgeUnroll = 4;
+
 // Validation and the OR / AND of the node ids and tskeys of every entry (one
-// read of each edge: both directions when undirected).
+// read of each edge: both directions when undirected).  One set of atomics
+// per block.
 __global__ __launch_bounds__(kBlock) void reduce_kernel(const int32_t *__restrict__ src,
                                                         const int32_t *__restrict__ dst,
                                                         const float *__restrict__ ts, int64_t m0, bool both,
                                                         int64_t N, BuildFlags *__restrict__ flags) {
+    __shared__ uint64_t s_or[kWaves], s_and[kWaves];
+    __shared__ uint32_t s_bad[kWaves];
     uint64_t o = 0, a = ~0ull;
     bool bad = false;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t k = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; k < m0; k += stride) {
-        const int32_t u = src[k];
-        const int32_t v = dst[k];
-        const float t = ts[k];
-        bad |= u < 0 || u >= N || v < 0 || v >= N || t != t;
-        const uint64_t tk = ts_key(t);
-        const uint64_t ku = (static_cast<uint64_t>(static_cast<uint32_t>(u)) << 32) | tk;
-        o |= ku;
-        a &= ku;
-        if (both) {
-            const uint64_t kv = (static_cast<uint64_t>(static_cast<uint32_t>(v)) << 32) | tk;
-            o |= kv;
-            a &= kv;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * kEdgeUnroll;
+    for (int64_t k0 = static_cast<int64_t>(blockIdx.x) * kBlock * kEdgeUnroll + threadIdx.x; k0 < m0; k0 += stride) {
+        int32_t u[kEdgeUnroll], v[kEdgeUnroll];
+        float t[kEdgeUnroll];
+#pragma unroll
+        for (int j = 0; j < kEdgeUnroll; j++) {
+            const int64_t k = k0 + static_cast<int64_t>(j) * kBlock;
+            const bool in = k < m0;
+            u[j] = in ? src[k] : 0;
+            v[j] = in ? dst[k] : 0;
+            t[j] = in ? ts[k] : 0.0f;
+            if (!in) {   // neutral for the OR / AND: repeat a key that is present (edge k0)
+                u[j] = u[0];
+                v[j] = v[0];
+                t[j] = t[0];
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kEdgeUnroll; j++) {
+            bad |= u[j] < 0 || u[j] >= N || v[j] < 0 || v[j] >= N || t[j] != t[j];
+            const uint64_t tk = ts_key(t[j]);
+            const uint64_t ku = (static_cast<uint64_t>(static_cast<uint32_t>(u[j])) << 32) | tk;
+            o |= ku;
+            a &= ku;
+            if (both) {
+                const uint64_t kv = (static_cast<uint64_t>(static_cast<uint32_t>(v[j])) << 32) | tk;
+                o |= kv;
+                a &= kv;
+            }
         }
     }
     o = wave_or(o);
     a = wave_and(a);
     const bool any_bad = __ballot(bad) != 0;
+    const int w = threadIdx.x / kWave;
     if (lane_id() == 0) {
+        s_or[w] = o;
+        s_and[w] = a;
+        s_bad[w] = any_bad ? 1u : 0u;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t bb = 0;
+#pragma unroll
+        for (int i = 1; i < kWaves; i++) {
+            o |= s_or[i];
+            a &= s_and[i];
+        }
+#pragma unroll
+        for (int i = 0; i < kWaves; i++) bb |= s_bad[i];
         atomicOr(reinterpret_cast<unsigned long long *>(&flags->or_bits), static_cast<unsigned long long>(o));
         atomicAnd(reinterpret_cast<unsigned long long *>(&flags->and_bits), static_cast<unsigned long long>(a));
-        if (any_bad) atomicOr(&flags->err, 1u);
+        if (bb) atomicOr(&flags->err, 1u);
     }
 }
 
-// Entry i < m0: (src[i] -> dst[i]); entry m0 + i: (dst[i] -> src[i]).  Keys
-// in the layout L, values the entry indices.
+// Entry k < m0: (src[k] -> dst[k]); entry m0 + k: (dst[k] -> src[k]) when
+// undirected, written from the same read of edge k.  Keys in the layout L,
+// values the entry indices.
 __global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict__ src,
                                                       const int32_t *__restrict__ dst, const float *__restrict__ ts,
-                                                      int64_t m0, int64_t M, const KeyLayout L,
+                                                      int64_t m0, bool both, const KeyLayout L,
                                                       uint64_t *__restrict__ keys, uint32_t *__restrict__ vals) {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < M; i += stride) {
-        const bool fwd = i < m0;
-        const int64_t k = fwd ? i : i - m0;
-        const uint32_t u = static_cast<uint32_t>(fwd ? src[k] : dst[k]);
-        const uint32_t v = L.packed ? static_cast<uint32_t>(fwd ? dst[k] : src[k]) : 0u;
-        keys[i] = make_key(L, u, ts_key(ts[k]), v);
-        vals[i] = static_cast<uint32_t>(i);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock * kEdgeUnroll;
+    for (int64_t k0 = static_cast<int64_t>(blockIdx.x) * kBlock * kEdgeUnroll + threadIdx.x; k0 < m0; k0 += stride) {
+        uint32_t u[kEdgeUnroll], v[kEdgeUnroll], tk[kEdgeUnroll];
+#pragma unroll
+        for (int j = 0; j < kEdgeUnroll; j++) {
+            const int64_t k = k0 + static_cast<int64_t>(j) * kBlock;
+            const bool in = k < m0;
+            u[j] = in ? static_cast<uint32_t>(src[k]) : 0u;
+            v[j] = in ? static_cast<uint32_t>(dst[k]) : 0u;
+            tk[j] = in ? ts_key(ts[k]) : 0u;
+        }
+#pragma unroll
+        for (int j = 0; j < kEdgeUnroll; j++) {
+            const int64_t k = k0 + static_cast<int64_t>(j) * kBlock;
+            if (k >= m0) continue;
+            keys[k] = make_key(L, u[j], tk[j], L.packed ? v[j] : 0u);
+            vals[k] = static_cast<uint32_t>(k);
+            if (both) {
+                keys[m0 + k] = make_key(L, v[j], tk[j], L.packed ? u[j] : 0u);
+                vals[m0 + k] = static_cast<uint32_t>(m0 + k);
+            }
+        }
     }
 }
 
@@ -204,13 +256,17 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *_
     __syncthreads();
     const int64_t base = tile * kTile;
     const uint64_t lane_bit = 1ull << lane_id();
-#pragma unroll 4
+    uint32_t dg[kTileItems];                        // every key of the tile is loaded before any is counted
+#pragma unroll
     for (int r = 0; r < kTileItems; r++) {
         const int64_t idx = base + static_cast<int64_t>(r) * kBlock + threadIdx.x;
-        const bool valid = idx < M;
-        const uint32_t d = valid ? static_cast<uint32_t>(keys[idx] >> shift) & (B - 1) : 0u;
-        const uint64_t peers = match_digit<BITS>(d, valid);
-        if (valid && (peers & (lane_bit - 1)) == 0) atomicAdd(&cnt[d], static_cast<uint32_t>(__popcll(peers)));
+        dg[r] = idx < M ? static_cast<uint32_t>(keys[idx] >> shift) & (B - 1) : 0u;
+    }
+#pragma unroll
+    for (int r = 0; r < kTileItems; r++) {
+        const bool valid = base + static_cast<int64_t>(r) * kBlock + threadIdx.x < M;
+        const uint64_t peers = match_digit<BITS>(dg[r], valid);
+        if (valid && (peers & (lane_bit - 1)) == 0) atomicAdd(&cnt[dg[r]], static_cast<uint32_t>(__popcll(peers)));
     }
     __syncthreads();
     if (threadIdx.x < B) hist[static_cast<int64_t>(threadIdx.x) * ntiles + tile] = cnt[threadIdx.x];
@@ -653,7 +709,8 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     }
 
     init_flags_kernel<<<1, 1, 0, st>>>(w.flags);
-    reduce_kernel<<<grid_for(m0), kBlock, 0, st>>>(src, dst, ts, m0, M != m0, num_nodes, w.flags);
+    const unsigned ge = grid_for((m0 + kEdgeUnroll - 1) / kEdgeUnroll);
+    reduce_kernel<<<ge, kBlock, 0, st>>>(src, dst, ts, m0, M != m0, num_nodes, w.flags);
     if (launch_status() != TGL_OK) return TGL_EDEVICE;
     BuildFlags hf{};
     if (hipMemcpyAsync(&hf, w.flags, sizeof(hf), hipMemcpyDeviceToHost, st) != hipSuccess)
@@ -663,7 +720,7 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
 
     const KeyLayout L = key_layout(hf, num_nodes);
     const uint64_t varying = sort_bits(L, hf);
-    keys_kernel<<<grid_for(M), kBlock, 0, st>>>(src, dst, ts, m0, M, L, w.keys[0], w.vals[0]);
+    keys_kernel<<<ge, kBlock, 0, st>>>(src, dst, ts, m0, M != m0, L, w.keys[0], w.vals[0]);
     int cur = 0;
     // Digits from the lowest varying sort bit up (in the packed layout the
     // neighbour bits lie below every sort bit: they must not take part, or
