@@ -703,7 +703,7 @@ template <int MODE, bool LAST, bool PTR>
 __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     constexpr int G = 8;
     constexpr int GPW = kWave / G;            // roots located per wavefront round
-    constexpr int NE = 4;                     // window edges located together
+    constexpr int NE = 2;                     // window edges located together
     constexpr int U = 4;                      // slots per lane whose loads are in flight together
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
