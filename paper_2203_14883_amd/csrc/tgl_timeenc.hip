@@ -156,42 +156,61 @@ __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__rest
         const int64_t lim = c <= 0 ? 0 : (c > n / per ? n : c * per);
         n = lim < n ? lim : n;
     }
-    const uint32_t wpr = static_cast<uint32_t>(dim / EPW);           // words per row
+    const uint32_t wpr = static_cast<uint32_t>(dim / EPW);           // words per row, at most 1024
     const int64_t total = n * wpr;
     int4 *const o = static_cast<int4 *>(out);
-    for (int64_t w0 = wave * kWave; w0 < total; w0 += waves * kWave) {
-        const int64_t row0 = w0 / wpr;                                // wavefront-uniform
-        const uint32_t r = static_cast<uint32_t>(w0 - row0 * wpr) + static_cast<uint32_t>(lane);
-        const uint32_t dr = r / wpr;
-        const int64_t row = row0 + dr;
-        const int col = static_cast<int>(r - dr * wpr) * EPW;
-        if (w0 + lane >= total) continue;
-        const float d = dt[row];
-        float v[EPW];
-        if (d >= 0.0f) {
+    // The wavefront's first word w0 as (row0, off0), advanced by the grid
+    // stride without dividing; a lane's word w0 + lane is off0 + lane < wpr + 64
+    // words past row0's start, split by a float reciprocal (exact after one
+    // correction: the quotient is at most 64 and the product is within 2^-22
+    // of it).
+    const float inv_wpr = 1.0f / static_cast<float>(wpr);
+    const int64_t step = waves * kWave;
+    const int64_t step_q = step / wpr;
+    const uint32_t step_r = static_cast<uint32_t>(step - step_q * wpr);
+    int64_t w0 = wave * kWave;
+    int64_t row0 = w0 / wpr;
+    uint32_t off0 = static_cast<uint32_t>(w0 - row0 * wpr);
+    for (; w0 < total; w0 += step) {
+        if (w0 + lane < total) {
+            const uint32_t r = off0 + static_cast<uint32_t>(lane);
+            uint32_t dr = static_cast<uint32_t>(static_cast<float>(r) * inv_wpr);
+            if ((dr + 1) * wpr <= r) dr++;
+            const int64_t row = row0 + dr;
+            const int col = static_cast<int>(r - dr * wpr) * EPW;
+            const float d = dt[row];
+            float v[EPW];
+            if (d >= 0.0f) {
 #pragma unroll
-            for (int e = 0; e < EPW; e++) {
-                const double2 fj = PRE ? fac[col + e]
-                                       : make_double2(static_cast<double>(omega[col + e]) * kInvTwoPi,
-                                                      static_cast<double>(phi[col + e]) * kInvTwoPi);
-                v[e] = encode(fj.x, fj.y, d, omega, phi, col + e);
+                for (int e = 0; e < EPW; e++) {
+                    const double2 fj = PRE ? fac[col + e]
+                                           : make_double2(static_cast<double>(omega[col + e]) * kInvTwoPi,
+                                                          static_cast<double>(phi[col + e]) * kInvTwoPi);
+                    v[e] = encode(fj.x, fj.y, d, omega, phi, col + e);
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < EPW; e++) v[e] = 0.0f;
             }
-        } else {
+            int4 word;
+            if constexpr (OUT == TGL_OUT_F32) {
+                word = make_int4(__float_as_int(v[0]), __float_as_int(v[1]), __float_as_int(v[2]), __float_as_int(v[3]));
+            } else {
+                uint32_t pk[4];
 #pragma unroll
-            for (int e = 0; e < EPW; e++) v[e] = 0.0f;
+                for (int e = 0; e < 4; e++)
+                    pk[e] = static_cast<uint32_t>(to_bf16(v[2 * e])) | (static_cast<uint32_t>(to_bf16(v[2 * e + 1])) << 16);
+                word = make_int4(static_cast<int>(pk[0]), static_cast<int>(pk[1]), static_cast<int>(pk[2]),
+                                 static_cast<int>(pk[3]));
+            }
+            o[w0 + lane] = word;
         }
-        int4 word;
-        if constexpr (OUT == TGL_OUT_F32) {
-            word = make_int4(__float_as_int(v[0]), __float_as_int(v[1]), __float_as_int(v[2]), __float_as_int(v[3]));
-        } else {
-            uint32_t pk[4];
-#pragma unroll
-            for (int e = 0; e < 4; e++)
-                pk[e] = static_cast<uint32_t>(to_bf16(v[2 * e])) | (static_cast<uint32_t>(to_bf16(v[2 * e + 1])) << 16);
-            word = make_int4(static_cast<int>(pk[0]), static_cast<int>(pk[1]), static_cast<int>(pk[2]),
-                             static_cast<int>(pk[3]));
+        row0 += step_q;
+        off0 += step_r;
+        if (off0 >= wpr) {
+            off0 -= wpr;
+            row0++;
         }
-        o[w0 + lane] = word;
     }
 }
 
