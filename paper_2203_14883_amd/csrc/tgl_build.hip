@@ -207,11 +207,12 @@ __global__ __launch_bounds__(kBlock) void keys_kernel(const int32_t *__restrict_
         uint32_t u[kEdgeUnroll], v[kEdgeUnroll], tk[kEdgeUnroll];
 #pragma unroll
         for (int j = 0; j < kEdgeUnroll; j++) {
+            // clamped, not predicated, so that the loads issue back to back
             const int64_t k = k0 + static_cast<int64_t>(j) * kBlock;
-            const bool in = k < m0;
-            u[j] = in ? static_cast<uint32_t>(src[k]) : 0u;
-            v[j] = in ? static_cast<uint32_t>(dst[k]) : 0u;
-            tk[j] = in ? ts_key(ts[k]) : 0u;
+            const int64_t kc = k < m0 ? k : m0 - 1;
+            u[j] = static_cast<uint32_t>(src[kc]);
+            v[j] = static_cast<uint32_t>(dst[kc]);
+            tk[j] = ts_key(ts[kc]);
         }
 #pragma unroll
         for (int j = 0; j < kEdgeUnroll; j++) {
@@ -256,11 +257,14 @@ __global__ __launch_bounds__(kBlock) void radix_upsweep_kernel(const uint64_t *_
     __syncthreads();
     const int64_t base = tile * kTile;
     const uint64_t lane_bit = 1ull << lane_id();
-    uint32_t dg[kTileItems];                        // every key of the tile is loaded before any is counted
+    // every key of the tile is loaded before any is counted: the index is
+    // clamped rather than the load predicated, so that the loads issue back to
+    // back (a key past M is read from M - 1 and not counted)
+    uint32_t dg[kTileItems];
 #pragma unroll
     for (int r = 0; r < kTileItems; r++) {
         const int64_t idx = base + static_cast<int64_t>(r) * kBlock + threadIdx.x;
-        dg[r] = idx < M ? static_cast<uint32_t>(keys[idx] >> shift) & (B - 1) : 0u;
+        dg[r] = static_cast<uint32_t>(keys[idx < M ? idx : M - 1] >> shift) & (B - 1);
     }
 #pragma unroll
     for (int r = 0; r < kTileItems; r++) {
@@ -412,13 +416,15 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
 
 // Sorted keys base + l + 64 j (j < kEmitPerLane) and the key before each:
 // the lane below, lane 63 of the previous round, or keys[base - 1].  Entries
-// at or past M get key ~0 (never read as an owner).
+// at or past M get the last key; callers skip them.
 __device__ __forceinline__ void load_keys_prev(const uint64_t *__restrict__ keys, int64_t M, int64_t base, int lane,
                                                uint64_t (&key)[kEmitPerLane], uint64_t (&prev)[kEmitPerLane]) {
 #pragma unroll
     for (int j = 0; j < kEmitPerLane; j++) {
         const int64_t p = base + j * kWave + lane;
-        key[j] = p < M ? keys[p] : ~0ull;
+        // clamped, not predicated, so that the loads issue together: a lane past
+        // the end holds the last key, and its caller skips it
+        key[j] = keys[p < M ? p : M - 1];
     }
     const uint64_t before = base > 0 ? keys[base - 1] : ~0ull;   // same address in every lane
 #pragma unroll
@@ -482,7 +488,7 @@ __global__ __launch_bounds__(kBlock) void emit_kernel(const uint64_t *__restrict
 #pragma unroll
         for (int j = 0; j < kEmitPerLane; j++) {
             const int64_t p = base + j * kWave + lane;
-            int64_t i = p < M ? static_cast<int64_t>(vals[p]) : 0;
+            int64_t i = static_cast<int64_t>(vals[p < M ? p : M - 1]);   // past the end: the last entry's
             if (i >= M) i = 0;   // never taken for a permutation; keeps loads in bounds
             fwd[j] = i < m0;
             k[j] = fwd[j] ? i : i - m0;
