@@ -530,6 +530,22 @@ __device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, bool vali
     }
 }
 
+// The T-CSR records of U picks (UINT32_MAX: no pick), with all U loads in
+// flight together.  A lane without a pick reads entry 0 and its caller
+// ignores the record: predicating the loads instead would put each behind a
+// branch and a wait of its own.
+template <int U>
+__device__ __forceinline__ void gather_records(const int4 *__restrict__ ent, uint32_t M, const uint32_t (&pick)[U],
+                                               int4 (&rec)[U]) {
+    if (M == 0) {                                   // uniform: nothing to read
+#pragma unroll
+        for (int u = 0; u < U; u++) rec[u] = make_int4(-1, -1, -1, -1);
+        return;
+    }
+#pragma unroll
+    for (int u = 0; u < U; u++) rec[u] = ent[pick[u] != UINT32_MAX ? pick[u] : 0u];
+}
+
 __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -838,9 +854,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                 }
             }
             int4 rec[U];
-#pragma unroll
-            for (int u = 0; u < U; u++)
-                rec[u] = pick[u] != UINT32_MAX ? p.ent[pick[u]] : make_int4(-1, -1, -1, -1);
+            gather_records<U>(p.ent, static_cast<uint32_t>(p.num_entries), pick, rec);
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
@@ -1069,9 +1083,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                 }
             }
             int4 rec[U];
-#pragma unroll
-            for (int u = 0; u < U; u++)
-                rec[u] = pick[u] != UINT32_MAX ? p.ent[pick[u]] : make_int4(-1, -1, -1, -1);
+            gather_records<U>(p.ent, static_cast<uint32_t>(p.num_entries), pick, rec);
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
