@@ -56,7 +56,10 @@ __global__ __launch_bounds__(kBlock) void mfg_count_kernel(const int32_t *__rest
         for (int32_t j0 = 0; j0 < k; j0 += 8) {
             int32_t v[8];
 #pragma unroll
-            for (int u = 0; u < 8; u++) v[u] = j0 + u < k ? sl[j0 + u] : -1;
+            for (int u = 0; u < 8; u++) v[u] = sl[j0 + u < k ? j0 + u : k - 1];   // clamped: loads issue together
+#pragma unroll
+            for (int u = 0; u < 8; u++)
+                if (j0 + u >= k) v[u] = -1;
             int32_t run = 8;
 #pragma unroll
             for (int u = 7; u >= 0; u--)
@@ -84,10 +87,16 @@ __global__ __launch_bounds__(kBlock) void mfg_count_kernel(const int32_t *__rest
     if (threadIdx.x == 0) partials[blockIdx.x] = total;
 }
 
-// Pass 4, one thread per slot i = g * k + j of the G groups: valid slot
-// j < cnt[g] becomes edge indptr[g] + j and source node G + that edge.  I is
-// the index type (32-bit when the slot capacity allows it).  Also closes
-// indptr with indptr[G] = E.
+// Slots per lane and round of the scatter: their loads are issued together.
+constexpr int kScatterUnroll = 4;
+
+// Pass 4, slots i = g * k + j of the G groups, kScatterUnroll per lane and
+// round: valid slot j < cnt[g] becomes edge indptr[g] + j and source node
+// G + that edge.  The counts and first edges of a lane's slots are loaded
+// together, then their fields; a slot past its group's prefix reads slot 0
+// (one cached line) and stores nothing, rather than each load waiting behind
+// a branch of its own.  I is the index type (32-bit when the slot capacity
+// allows it).  Also closes indptr with indptr[G] = E.
 template <class I>
 __global__ __launch_bounds__(kBlock) void mfg_scatter_kernel(const int32_t *__restrict__ nbr,
                                                              const int64_t *__restrict__ eid,
@@ -100,21 +109,53 @@ __global__ __launch_bounds__(kBlock) void mfg_scatter_kernel(const int32_t *__re
                                                              int64_t *__restrict__ edge_eid,
                                                              float *__restrict__ edge_dt, int32_t *__restrict__ src_nid,
                                                              float *__restrict__ src_ts) {
+    constexpr int U = kScatterUnroll;
     const int64_t G = sizes[0];
     if (blockIdx.x == 0 && threadIdx.x == 0) indptr[G] = sizes[1];
     const I total = static_cast<I>(G) * static_cast<I>(k);
     const I kk = static_cast<I>(k);
-    const I stride = static_cast<I>(gridDim.x) * kBlock;
-    for (I i = static_cast<I>(blockIdx.x) * kBlock + threadIdx.x; i < total; i += stride) {
-        const I g = i / kk;
-        const I j = i - g * kk;
-        if (static_cast<int32_t>(j) >= cnt[g]) continue;
-        const int64_t e = indptr[g] + static_cast<int64_t>(j);
-        if (edge_dst) edge_dst[e] = static_cast<int64_t>(g);
-        edge_eid[e] = eid[i];
-        edge_dt[e] = dt[i];
-        src_nid[G + e] = nbr[i];
-        src_ts[G + e] = ts[i];
+    const I stride = static_cast<I>(gridDim.x) * kBlock * U;
+    for (I i0 = static_cast<I>(blockIdx.x) * kBlock * U + threadIdx.x; i0 < total; i0 += stride) {
+        I g[U];
+        int32_t j[U], c[U];
+        int64_t first[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const I i = i0 + static_cast<I>(u) * kBlock;
+            const I ic = i < total ? i : total - 1;
+            g[u] = ic / kk;
+            j[u] = static_cast<int32_t>(ic - g[u] * kk);
+            c[u] = cnt[g[u]];
+            first[u] = indptr[g[u]];
+        }
+        I at[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const I i = i0 + static_cast<I>(u) * kBlock;
+            ok[u] = i < total && j[u] < c[u];
+            at[u] = ok[u] ? i : 0;
+        }
+        int64_t ve[U];
+        float vd[U], vt[U];
+        int32_t vn[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            ve[u] = eid[at[u]];
+            vd[u] = dt[at[u]];
+            vn[u] = nbr[at[u]];
+            vt[u] = ts[at[u]];
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            if (!ok[u]) continue;
+            const int64_t e = first[u] + static_cast<int64_t>(j[u]);
+            if (edge_dst) edge_dst[e] = static_cast<int64_t>(g[u]);
+            edge_eid[e] = ve[u];
+            edge_dt[e] = vd[u];
+            src_nid[G + e] = vn[u];
+            src_ts[G + e] = vt[u];
+        }
     }
 }
 
@@ -184,12 +225,12 @@ tgl_status tgl_mfg_export(const tgl_hop_out *hop, const tgl_hop_out *prev, const
     scan_apply_kernel<int32_t, int64_t><<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(
         ws.cnt, out->indptr, groups_cap, out->sizes, ws.partials);
     const int64_t slots = groups_cap * k;
-    if (slots < (int64_t(1) << 32) - kBlock * 65536ll)
-        mfg_scatter_kernel<uint32_t><<<grid_of(slots), kBlock, 0, st>>>(
+    if (slots < (int64_t(1) << 32) - kBlock * 65536ll * kScatterUnroll)   // no 32-bit wrap past the last round
+        mfg_scatter_kernel<uint32_t><<<grid_of((slots + kScatterUnroll - 1) / kScatterUnroll), kBlock, 0, st>>>(
             hop->nbr, hop->eid, hop->ts, hop->dt, k, out->sizes, ws.cnt, out->indptr, out->edge_dst, out->edge_eid,
             out->edge_dt, out->src_nid, out->src_ts);
     else
-        mfg_scatter_kernel<uint64_t><<<grid_of(slots), kBlock, 0, st>>>(
+        mfg_scatter_kernel<uint64_t><<<grid_of((slots + kScatterUnroll - 1) / kScatterUnroll), kBlock, 0, st>>>(
             hop->nbr, hop->eid, hop->ts, hop->dt, k, out->sizes, ws.cnt, out->indptr, out->edge_dst, out->edge_eid,
             out->edge_dt, out->src_nid, out->src_ts);
     return launch_status();
