@@ -7,10 +7,10 @@
 // Every (slot, table) pair is an independent row copy, so the kernel is a
 // plain HBM-bound gather: one wavefront copies kRows rows at a time, lane l
 // moving 16-byte words l, l + 64, ... of each row.  The row keys are
-// wavefront-uniform (scalar loads); the loads of all kRows rows are issued
-// before any store, so a wavefront keeps kRows x 1 KB in flight per pass;
-// outputs are written with nontemporal stores (they are consumed by the next
-// stage, not re-read here).
+// wavefront-uniform (one load by kRows lanes, then broadcast); the loads of
+// all kRows rows are issued before any store, so a wavefront keeps kRows x
+// 1 KB in flight per pass; outputs are written with nontemporal stores (they
+// are consumed by the next stage, not re-read here).
 #include "tgl_internal.hpp"
 
 namespace tgl {
@@ -55,13 +55,23 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(const GatherArgs a) {
         const GatherTable T = a.t[ti];
         const int W = T.words;
         for (int64_t r0 = wave * kRows; r0 < n; r0 += waves * kRows) {
+            // one load brings the kRows keys (lane u holds row r0 + u's), each
+            // then broadcast from its lane: loaded one by one, every key would
+            // wait for the one before
+            int64_t kl = -1;
+            if (lane < kRows) {
+                const int64_t row = r0 + lane;
+                if (row < n) {
+                    const int64_t k = T.key == TGL_KEY_NODE ? static_cast<int64_t>(a.nbr[row]) : a.eid[row];
+                    kl = k >= 0 && k < T.num_rows ? k : -1;
+                }
+            }
             int64_t key[kRows];
 #pragma unroll
             for (int u = 0; u < kRows; u++) {
-                const int64_t row = r0 + u;
-                int64_t k = -1;
-                if (row < n) k = T.key == TGL_KEY_NODE ? static_cast<int64_t>(a.nbr[row]) : a.eid[row];
-                key[u] = k >= 0 && k < T.num_rows ? k : -1;
+                const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(kl), u));
+                const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(kl >> 32), u));
+                key[u] = static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
             }
             for (int w0 = 0; w0 < W; w0 += kWave) {
                 const int w = w0 + lane;
