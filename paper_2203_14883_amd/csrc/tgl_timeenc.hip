@@ -28,6 +28,8 @@
 // Padded slots (dt < 0) have no time difference: their rows are zeros, and a
 // row's dt is the same for the whole wavefront, so those rows branch to plain
 // stores.
+#include <atomic>
+
 #include "tgl_internal.hpp"
 
 namespace tgl {
@@ -135,9 +137,7 @@ __global__ __launch_bounds__(kBlock) void timeenc_kernel(const float *__restrict
 
 // Rows whose byte size is a multiple of 16: lane l of a wavefront owns the
 // 16-byte word w0 + l of the flattened output (EPW elements: 4 float32 or 8
-// bfloat16), so one store instruction writes 1 KB of contiguous output.  The
-// word's row and column come from one 32-bit division by the uniform number
-// of words per row.
+// bfloat16), so one store instruction writes 1 KB of contiguous output.
 template <int OUT, bool PRE>
 __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__restrict__ dt, int64_t n,
                                                              const int64_t *__restrict__ count, int64_t per,
@@ -214,6 +214,44 @@ __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__rest
     }
 }
 
+// Both kernels stride over their rows, so a grid of the blocks the device
+// holds at once does all the work and loads each block's factor table once:
+// with one block per 256 words (capped at 64 Ki blocks) a block lived for
+// about a dozen words and its factor load and barrier were a tenth of its
+// time.  Found once per device and kernel (CUs x resident blocks per CU).
+constexpr int kMaxDevices = 64;
+constexpr int kVariants = 8;                                       // row/word kernel x output x factor table
+std::atomic<int> g_resident[kMaxDevices][kVariants];
+
+template <typename K>
+unsigned resident_grid(K kernel, int variant, int64_t want) {
+    int dev = 0;
+    int r = 0;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < kMaxDevices) {
+        r = g_resident[dev][variant].load(std::memory_order_relaxed);
+        if (r == 0) {
+            int cus = 0, per_cu = 0;
+            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kBlock, 0) == hipSuccess && cus > 0 &&
+                per_cu > 0) {
+                r = cus * per_cu;
+                g_resident[dev][variant].store(r, std::memory_order_relaxed);
+            }
+        }
+    }
+    (void)hipGetLastError();
+    if (r <= 0) r = 1 << 16;
+    return static_cast<unsigned>(want < r ? want : r);
+}
+
+template <typename K>
+void launch_resident(K kernel, int variant, int64_t want, hipStream_t st, const float *dt, int64_t n,
+                     const int64_t *count, int64_t per, const float *omega, const float *phi, int dim, void *out) {
+    const unsigned nb = resident_grid(kernel, variant, want);
+    ScopedTimer tm(TGL_TIMER_TIMEENC, st);
+    kernel<<<nb, kBlock, 0, st>>>(dt, n, count, per, omega, phi, dim, out);
+}
+
 }  // namespace
 }  // namespace tgl
 
@@ -238,32 +276,24 @@ tgl_status tgl_time_encode(const float *dt, int64_t n, const int64_t *count, int
     const bool vec = (static_cast<int64_t>(dim) * esize) % 16 == 0 && (reinterpret_cast<uintptr_t>(out) & 15u) == 0;
     if (vec) {
         const int64_t words = n * (static_cast<int64_t>(dim) * esize / 16);
-        int64_t blocks = (words + kBlock - 1) / kBlock;
-        if (blocks > (1 << 16)) blocks = 1 << 16;
-        ScopedTimer tm(TGL_TIMER_TIMEENC, st);
-        const unsigned nb = static_cast<unsigned>(blocks);
+        const int64_t want = (words + kBlock - 1) / kBlock;
         if (out_type == TGL_OUT_F32) {
-            if (pre) timeenc_vec_kernel<TGL_OUT_F32, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
-            else timeenc_vec_kernel<TGL_OUT_F32, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+            if (pre) launch_resident(timeenc_vec_kernel<TGL_OUT_F32, true>, 4, want, st, dt, n, count, per_count, omega, phi, dim, out);
+            else launch_resident(timeenc_vec_kernel<TGL_OUT_F32, false>, 5, want, st, dt, n, count, per_count, omega, phi, dim, out);
         } else {
-            if (pre) timeenc_vec_kernel<TGL_OUT_BF16, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
-            else timeenc_vec_kernel<TGL_OUT_BF16, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
+            if (pre) launch_resident(timeenc_vec_kernel<TGL_OUT_BF16, true>, 6, want, st, dt, n, count, per_count, omega, phi, dim, out);
+            else launch_resident(timeenc_vec_kernel<TGL_OUT_BF16, false>, 7, want, st, dt, n, count, per_count, omega, phi, dim, out);
         }
         return launch_status();
     }
     constexpr int64_t rows_per_block = static_cast<int64_t>(kBlock / kWave) * kRows;
-    int64_t blocks = (n + rows_per_block - 1) / rows_per_block;
-    if (blocks > (1 << 16)) blocks = 1 << 16;
-    {
-        ScopedTimer tm(TGL_TIMER_TIMEENC, st);
-        const unsigned nb = static_cast<unsigned>(blocks);
-        if (out_type == TGL_OUT_F32) {
-            if (pre) timeenc_kernel<TGL_OUT_F32, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
-            else timeenc_kernel<TGL_OUT_F32, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
-        } else {
-            if (pre) timeenc_kernel<TGL_OUT_BF16, true><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
-            else timeenc_kernel<TGL_OUT_BF16, false><<<nb, kBlock, 0, st>>>(dt, n, count, per_count, omega, phi, dim, out);
-        }
+    const int64_t want = (n + rows_per_block - 1) / rows_per_block;
+    if (out_type == TGL_OUT_F32) {
+        if (pre) launch_resident(timeenc_kernel<TGL_OUT_F32, true>, 0, want, st, dt, n, count, per_count, omega, phi, dim, out);
+        else launch_resident(timeenc_kernel<TGL_OUT_F32, false>, 1, want, st, dt, n, count, per_count, omega, phi, dim, out);
+    } else {
+        if (pre) launch_resident(timeenc_kernel<TGL_OUT_BF16, true>, 2, want, st, dt, n, count, per_count, omega, phi, dim, out);
+        else launch_resident(timeenc_kernel<TGL_OUT_BF16, false>, 3, want, st, dt, n, count, per_count, omega, phi, dim, out);
     }
     return launch_status();
 }
