@@ -50,12 +50,8 @@ constexpr float kC6 = 7.903536371318469f;
 
 // cos(omega dt + phi) from wp = omega / 2 pi and pp = phi / 2 pi; omega[j] and
 // phi[j] are read only for the double-precision fallback.
-__device__ __forceinline__ float encode(double wp, double pp, float dt, const float *__restrict__ omega,
-                                        const float *__restrict__ phi, int j) {
-    const double t = fma(wp, static_cast<double>(dt), pp);        // the argument in turns
-    if (!(fabs(t) < kTurnLimit))                                   // huge, infinite or NaN
-        return static_cast<float>(cos(fma(static_cast<double>(omega[j]), static_cast<double>(dt),
-                                          static_cast<double>(phi[j]))));
+// cos(2 pi t) for an argument t in turns with |t| < kTurnLimit
+__device__ __forceinline__ float cos_turns(double t) {
     const double f = t - rint(t);                                  // exact, in [-1/2, 1/2]
     const double a = fabs(f);
     const bool flip = a > 0.25;                                    // cos(2 pi a) = -cos(2 pi (1/2 - a))
@@ -68,6 +64,15 @@ __device__ __forceinline__ float encode(double wp, double pp, float dt, const fl
     c = __builtin_fmaf(y, c, kC1);
     c = __builtin_fmaf(y, c, 1.0f);
     return flip ? -c : c;
+}
+
+__device__ __forceinline__ float encode(double wp, double pp, float dt, const float *__restrict__ omega,
+                                        const float *__restrict__ phi, int j) {
+    const double t = fma(wp, static_cast<double>(dt), pp);        // the argument in turns
+    if (!(fabs(t) < kTurnLimit))                                   // huge, infinite or NaN
+        return static_cast<float>(cos(fma(static_cast<double>(omega[j]), static_cast<double>(dt),
+                                          static_cast<double>(phi[j]))));
+    return cos_turns(t);
 }
 
 // the per-column factors (omega / 2 pi, phi / 2 pi) of columns [0, dim), into
@@ -138,12 +143,17 @@ __global__ __launch_bounds__(kBlock) void timeenc_kernel(const float *__restrict
 // Rows whose byte size is a multiple of 16: lane l of a wavefront owns the
 // 16-byte word w0 + l of the flattened output (EPW elements: 4 float32 or 8
 // bfloat16), so one store instruction writes 1 KB of contiguous output.
+// With float32 output and the factors in LDS, a lane reads its word's four
+// factor pairs together and checks the four arguments once, so the elements
+// are evaluated side by side rather than each behind its own LDS wait and
+// branch; that kernel is held to 64 VGPRs, i.e. 8 wavefronts per SIMD (at 7
+// it is slower than the element-by-element form).  The other forms keep the
+// element-by-element evaluation, which needs fewer registers.
 template <int OUT, bool PRE>
-__global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__restrict__ dt, int64_t n,
-                                                             const int64_t *__restrict__ count, int64_t per,
-                                                             const float *__restrict__ omega,
-                                                             const float *__restrict__ phi, int dim,
-                                                             void *__restrict__ out) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(OUT == TGL_OUT_F32 && PRE ? 8 : 1)))
+void timeenc_vec_kernel(const float *__restrict__ dt, int64_t n, const int64_t *__restrict__ count, int64_t per,
+                        const float *__restrict__ omega, const float *__restrict__ phi, int dim,
+                        void *__restrict__ out) {
     constexpr int EPW = OUT == TGL_OUT_F32 ? 4 : 8;                 // elements per 16-byte word
     __shared__ double2 fac[PRE ? kMaxPre : 1];
     if constexpr (PRE) load_factors(fac, omega, phi, dim);
@@ -180,7 +190,35 @@ __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__rest
             const int col = static_cast<int>(r - dr * wpr) * EPW;
             const float d = dt[row];
             float v[EPW];
-            if (d >= 0.0f) {
+            if (d < 0.0f) {
+#pragma unroll
+                for (int e = 0; e < EPW; e++) v[e] = 0.0f;
+            } else if constexpr (OUT == TGL_OUT_F32 && PRE) {
+                // the factors as the general form reads them: with a plain
+                // fac[col + e] hipcc combines the four range checks through
+                // 16-bit vector ops instead of lane masks, and runs slower
+                double2 fj[EPW];
+#pragma unroll
+                for (int e = 0; e < EPW; e++)
+                    fj[e] = PRE ? fac[col + e]
+                                : make_double2(static_cast<double>(omega[col + e]) * kInvTwoPi,
+                                               static_cast<double>(phi[col + e]) * kInvTwoPi);
+                const double dd = static_cast<double>(d);
+                double t[EPW];
+                bool ok = true;
+#pragma unroll
+                for (int e = 0; e < EPW; e++) {
+                    t[e] = fma(fj[e].x, dd, fj[e].y);
+                    ok = ok && fabs(t[e]) < kTurnLimit;
+                }
+                if (ok) {                           // the arguments encode() reduces itself
+#pragma unroll
+                    for (int e = 0; e < EPW; e++) v[e] = cos_turns(t[e]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < EPW; e++) v[e] = encode(fj[e].x, fj[e].y, d, omega, phi, col + e);
+                }
+            } else {
 #pragma unroll
                 for (int e = 0; e < EPW; e++) {
                     const double2 fj = PRE ? fac[col + e]
@@ -188,9 +226,6 @@ __global__ __launch_bounds__(kBlock) void timeenc_vec_kernel(const float *__rest
                                                           static_cast<double>(phi[col + e]) * kInvTwoPi);
                     v[e] = encode(fj.x, fj.y, d, omega, phi, col + e);
                 }
-            } else {
-#pragma unroll
-                for (int e = 0; e < EPW; e++) v[e] = 0.0f;
             }
             int4 word;
             if constexpr (OUT == TGL_OUT_F32) {
