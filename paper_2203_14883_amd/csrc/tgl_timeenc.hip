@@ -55,7 +55,7 @@ __device__ __forceinline__ float cos_turns(double t) {
     const double f = t - rint(t);                                  // exact, in [-1/2, 1/2]
     const double a = fabs(f);
     const bool flip = a > 0.25;                                    // cos(2 pi a) = -cos(2 pi (1/2 - a))
-    const float g = static_cast<float>(flip ? 0.5 - a : a);        // 0.5 - a is exact
+    const float g = static_cast<float>(fmin(a, 0.5 - a));         // 0.5 - a is exact; flip picks it
     const float y = g * g;
     float c = __builtin_fmaf(y, kC6, kC5);
     c = __builtin_fmaf(y, c, kC4);
