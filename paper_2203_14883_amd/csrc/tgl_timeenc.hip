@@ -48,8 +48,6 @@ constexpr float kC4 = 60.24464137187666f;
 constexpr float kC5 = -26.426256783374397f;
 constexpr float kC6 = 7.903536371318469f;
 
-// cos(omega dt + phi) from wp = omega / 2 pi and pp = phi / 2 pi; omega[j] and
-// phi[j] are read only for the double-precision fallback.
 // cos(2 pi t) for an argument t in turns with |t| < kTurnLimit
 __device__ __forceinline__ float cos_turns(double t) {
     const double f = t - rint(t);                                  // exact, in [-1/2, 1/2]
@@ -66,6 +64,8 @@ __device__ __forceinline__ float cos_turns(double t) {
     return flip ? -c : c;
 }
 
+// cos(omega dt + phi) from wp = omega / 2 pi and pp = phi / 2 pi; omega[j] and
+// phi[j] are read only for the double-precision fallback.
 __device__ __forceinline__ float encode(double wp, double pp, float dt, const float *__restrict__ omega,
                                         const float *__restrict__ phi, int j) {
     const double t = fma(wp, static_cast<double>(dt), pp);        // the argument in turns
