@@ -35,8 +35,8 @@ namespace tgl {
 namespace {
 
 constexpr uint64_t kGolden = 0x9E3779B97F4A7C15ull;
-constexpr int kMaxGrid = 1 << 16;
-constexpr int kMultiEdges = 9;       // window edges per root held in LDS by hop_multi_kernel (S <= 8)     // cap on blocks of the grid-stride hop kernels
+constexpr int kMaxGrid = 1 << 16;      // cap on blocks of the grid-stride hop kernels
+constexpr int kMultiEdges = 9;       // window edges per root held in LDS by hop_multi_kernel (S <= 8)
 constexpr int kWavesPerBlock = kBlock / kWave;
 
 __host__ __device__ __forceinline__ uint64_t mix64(uint64_t z) {
@@ -1226,7 +1226,11 @@ __global__ __launch_bounds__(kBlock) void group_scan_kernel(int32_t *__restrict_
 }
 
 struct SampleWs {
-    int32_t *cnt = nullptr;          // valid slots per group of the current hop, then their offsets in the tile
+    // valid slots per group of hop h, then their offsets in the scan tile:
+    // hop h writes cnt[h & 1] while it reads hop h - 1's offsets from
+    // cnt[(h - 1) & 1] (a single buffer would let a later chunk read a count
+    // that an earlier chunk of the same launch has just written)
+    int32_t *cnt[2] = {nullptr, nullptr};
     int64_t *tile_off = nullptr;     // per scan tile: total, then exclusive offset
     int32_t *s[2] = {nullptr, nullptr};       // window per root (hops 2..L-1)
     uint64_t *path[2] = {nullptr, nullptr};   // path per root (hops 2..L-1)
@@ -1235,10 +1239,11 @@ struct SampleWs {
     size_t bytes = 0;
 };
 
-// Workspace: per-group counts, offsets and scan partials for the largest hop
-// h < L; window, path and hop-1 ancestor time of the roots of hops 2..L-1
-// (two alternating buffers); the neighbour-first hint of the slots of hops
-// 1..L-1 (hop h writes buffer h & 1, hop h + 1 reads it).
+// Workspace: per-group counts and offsets for the largest hop h < L (two
+// alternating buffers when L >= 3: hop h writes buffer h & 1, hop h + 1 reads
+// it) and scan partials; window, path and hop-1 ancestor time of the roots of
+// hops 2..L-1 (two alternating buffers); the neighbour-first hint of the
+// slots of hops 1..L-1 (hop h writes buffer h & 1, hop h + 1 reads it).
 SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S) {
     SampleWs w;
     Carver cv(base);
@@ -1249,7 +1254,8 @@ SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S
         for (int i = 0; i < nfirst; i++) w.first[(1 + i) & 1] = cv.take<uint8_t>(static_cast<size_t>(max_slots));
         int64_t max_groups = cap[0] * S;      // hop-1 groups
         for (int h = 2; h < hops; h++) max_groups = cap[h - 1] > max_groups ? cap[h - 1] : max_groups;
-        w.cnt = cv.take<int32_t>(static_cast<size_t>(max_groups));
+        const int ncnt = hops >= 3 ? 2 : 1;
+        for (int i = 0; i < ncnt; i++) w.cnt[(1 + i) & 1] = cv.take<int32_t>(static_cast<size_t>(max_groups));
         w.tile_off = cv.take<int64_t>(static_cast<size_t>(scan_tiles(max_groups) + 1));
         if (hops >= 3) {
             int64_t max_mid = 0;               // roots of hops 2..L-1
@@ -1362,7 +1368,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         a.o_ts = o.ts;
         a.o_dt = o.dt;
         a.o_parent = h >= 2 ? o.parent : nullptr;
-        a.o_cnt = last ? nullptr : ws.cnt;
+        a.o_cnt = last ? nullptr : ws.cnt[h & 1];
         // window and path of this hop's roots are kept for hop h + 1 (hop-1
         // children derive them from their slot index instead)
         const bool keep = h >= 2 && h < hops;
@@ -1376,7 +1382,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
             const tgl_hop_out &po = outs[h - 2];
             a.p_nbr = po.nbr;
             a.p_ts = po.ts;
-            a.p_local = ws.cnt;
+            a.p_local = ws.cnt[(h - 1) & 1];
             a.p_tile = ws.tile_off;
             a.p_k = fanouts[h - 2];
             a.p_s = h >= 3 ? ws.s[(h - 1) & 1] : nullptr;
@@ -1400,7 +1406,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         const int64_t *groups_dyn = h == 1 ? nullptr : counts + (h - 1);
         const int64_t tiles = scan_tiles(groups_cap) > 0 ? scan_tiles(groups_cap) : 1;
         ScopedTimer tm(TGL_TIMER_COMPACT, st);
-        group_scan_kernel<<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(ws.cnt, groups_cap, groups_dyn,
+        group_scan_kernel<<<static_cast<unsigned>(tiles), kBlock, 0, st>>>(ws.cnt[h & 1], groups_cap, groups_dyn,
                                                                           ws.tile_off);
         launch_scan_partials(ws.tile_off, tiles, counts + h, st);
         if (launch_status() != TGL_OK) return TGL_EDEVICE;

@@ -1,15 +1,18 @@
 """GPU path against the oracle at the full preset sizes, in the launch
 configuration bench.py times.
 
-* c4 (121.7M nodes, 1.3B edges, 2.6B T-CSR entries): one whole benchmark
-  step (64 batches, 768,000 roots, 2 hops) is compared slot for slot with the
-  oracle, which builds the full runs of every node the step reaches.
-* c3 (191M edges, runs up to ~4.6e7 entries) and c5 (200M entries built from a
-  shuffled COO, 2 hops inside 3 snapshots): the whole step runs on the GPU and
-  a sample of its roots -- including roots on the hottest nodes -- is compared
-  root by root (hop-1 slots and the hop-2 slots of that root's children).
-* For all three, the GPU T-CSR is checked in full on the device (indptr,
-  degrees, sortedness of every run, the timestamp array) and the runs of the
+* c4 (121.7M nodes, 1.3B edges, 2.6B T-CSR entries): two whole benchmark
+  steps (64 batches, 768,000 roots, 2 hops) are compared slot for slot with
+  the oracle, which builds the full runs of every node the step reaches.
+* c3 (191M edges, runs up to ~4.6e7 entries; 1 hop in 3 snapshots) and c5
+  (200M entries built from a shuffled COO; 2 hops inside 3 snapshots): the
+  whole GPU T-CSR is compared byte for byte with the oracle's build of the
+  same COO (indptr, nbr, eid, ts; node records, search index and
+  neighbour-first hints against their definitions), and two whole
+  benchmark steps each (c3: 64 batches = 768,000 roots; c5: one batch =
+  180,000 roots) slot for slot with the oracle on that T-CSR.
+* For c4 the GPU T-CSR is checked in full on the device (indptr, degrees,
+  sortedness of every run, the timestamp array, the hints) and the runs of
   sampled nodes bit for bit against the oracle's.
 """
 import gc
@@ -110,29 +113,6 @@ def gpu_step(torch, g, w, b0, B):
     return roots, rts, base, hops_to_numpy(smp.hops())
 
 
-def per_root(out, r, S, fan):
-    """Slots of root r in a GPU step: its hop-1 slots and the hop-2 slots of its
-    children (found through the parent indices)."""
-    k1 = fan[0]
-    lo, hi = r * S * k1, (r + 1) * S * k1
-    res = [{f: out[0][f][lo:hi] for f in ("nbr", "eid", "ts", "dt")}]
-    if len(fan) > 1:
-        par = out[1]["parent"]
-        q = np.nonzero((par >= lo) & (par < hi))[0]
-        k2 = fan[1]
-        idx = (q[:, None] * k2 + np.arange(k2)[None, :]).reshape(-1)
-        res.append({f: out[1][f][idx] for f in ("nbr", "eid", "ts", "dt")})
-        res[1]["parent"] = par[q] - lo
-    return res
-
-
-def oracle_per_root(og, roots, rts, r, w, base):
-    o = oracle.sample(og, roots[r:r + 1], rts[r:r + 1], w.fanouts, w.mode, w.snapshots,
-                      w.snapshot_len, w.sample_seed, base + r)
-    res = [dict(nbr=h.nbr, eid=h.eid, ts=h.ts, dt=h.dt, parent=h.parent) for h in o]
-    return res
-
-
 def test_c4_full_step(torch):
     announce("c4 full size: generate")
     w = W.make_c4()
@@ -156,51 +136,33 @@ def test_c4_full_step(torch):
     torch.cuda.empty_cache()
 
 
-def _hot_and_random_roots(w, roots, n_random, n_hot, seed):
-    deg = np.bincount(np.concatenate([w.src, w.dst]), minlength=w.num_nodes)
-    hot = np.argsort(deg)[::-1][:n_hot]
-    pick = []
-    for x in hot:
-        where = np.nonzero(roots == x)[0]
-        if len(where):
-            pick.append(int(where[len(where) // 2]))
-    rng = np.random.default_rng(seed)
-    # random roots among the negatives (uniform nodes) keep the oracle's work
-    # bounded; every batch contributes [src; dst; neg] blocks of E roots each
-    E = w.batch_edges
-    blocks = len(roots) // (3 * E)
-    neg = (np.arange(blocks)[:, None] * 3 * E + 2 * E + np.arange(E)[None, :]).reshape(-1)
-    pick += [int(i) for i in rng.choice(neg, n_random, replace=False)]
-    return sorted(set(pick)), hot
-
-
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["c3", "c5"])
-def test_hot_runs_full_size(torch, name):
+def test_full_size_whole_steps(torch, name):
+    from gpu_util import tcsr_to_host
+    from test_gpu_parity import assert_tcsr_equal
     announce("%s full size: generate" % name)
     w = W.make(name)
     announce("%s full size: GPU build of %d edges" % (name, w.num_edges))
     g = build_on_gpu(torch, w)
-    B = 64 if name == "c3" else 1
-    b0 = w.num_batches() // 2
-    announce("%s step at batch %d: GPU sample" % (name, b0))
-    roots, rts, base, got = gpu_step(torch, g, w, b0, B)
-    picks, hot = _hot_and_random_roots(w, roots, 24, 2, seed=7)
-    announce("%s: oracle for %d roots (%d on the hottest nodes)" % (name, len(picks), len(picks) - 24))
+    announce("%s full size: oracle build of the same COO" % name)
     src, dst, ts, eid = w.build_input()
-    reach = np.unique(roots[picks])
-    og = subgraph.owned_tcsr(src, dst, ts, eid, w.num_nodes, reach)
-    if len(w.fanouts) > 1:
-        kids = []
-        for r in picks:
-            o = oracle.sample(og, roots[r:r + 1], rts[r:r + 1], w.fanouts[:1], w.mode, w.snapshots,
-                              w.snapshot_len, w.sample_seed, base + r)
-            kids.append(o[0].nbr[o[0].nbr >= 0])
-        reach = np.unique(np.concatenate([reach] + kids))
-        og = subgraph.owned_tcsr(src, dst, ts, eid, w.num_nodes, reach)
-    for r in picks:
-        assert_hops_equal(per_root(got, r, w.snapshots, w.fanouts),
-                          oracle_per_root(og, roots, rts, r, w, base), "%s root %d" % (name, r))
-    check_runs(g, og, np.unique(roots[picks]))
+    og = oracle.build_tcsr(src, dst, ts, eid, w.num_nodes, w.undirected)
+    del src, dst, ts, eid
+    gc.collect()
+    announce("%s full size: T-CSR byte for byte" % name)
+    assert_tcsr_equal(tcsr_to_host(g), og, "%s full size" % name)
+    gc.collect()
+    B = 64 if name == "c3" else 1
+    for b0 in (w.num_batches() // 2, w.num_batches() - B):
+        announce("%s step at batch %d (%d batches): GPU sample" % (name, b0, B))
+        roots, rts, base, got = gpu_step(torch, g, w, b0, B)
+        announce("%s step at batch %d: oracle" % (name, b0))
+        want = oracle.sample(og, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
+                             w.sample_seed, base)
+        assert_hops_equal(got, want, "%s step at batch %d" % (name, b0))
+        for h in range(len(w.fanouts)):
+            assert got[h]["num_roots"] == want[h].num_roots
     del g
     gc.collect()
     torch.cuda.empty_cache()

@@ -325,3 +325,44 @@ def test_anchor_root_invariants_and_special_case():
             assert np.all(tsv[ok] >= t0[ok] - (s1[ok] + 1) * D)
             assert np.all(tsv[ok] < np.minimum(t0[ok] - s1[ok] * D, par_t[ok]))
             par_t = tsv
+
+
+def _deep_case(rng, trial):
+    """Dense tiny graph and roots with non-empty histories, so that deep hops
+    and wide fanouts still carry valid slots."""
+    N = int(rng.integers(2, 12))
+    m0 = int(rng.integers(40, 250))
+    src = rng.integers(0, N, m0).astype(np.int32)
+    dst = rng.integers(0, N, m0).astype(np.int32)
+    ts = rng.integers(0, 40, m0).astype(np.float32)
+    und = bool(rng.integers(0, 4))                 # mostly undirected
+    eid = None if rng.integers(0, 2) else rng.integers(0, 10**9, m0).astype(np.int64)
+    R = int(rng.integers(1, 5))
+    roots = rng.integers(0, N, R).astype(np.int32)
+    rts = rng.integers(20, 42, R).astype(np.float32)
+    mode = ["recent", "uniform"][trial % 4 // 2]
+    if trial % 2 == 0:
+        fan = [int(rng.choice([1, 2])) for _ in range(int(rng.integers(5, 9)))]
+        S, delta = [(1, math.inf), (2, 15.0), (3, 6.0)][int(rng.integers(0, 3))]
+    else:
+        fan = [int(rng.choice([71, 128, 513, 1024]))] + [int(rng.choice([1, 2, 3])) for _ in range(int(rng.integers(0, 2)))]
+        S, delta = [(1, math.inf), (2, 9.0)][int(rng.integers(0, 2))]
+    return N, src, dst, ts, eid, und, roots, rts, fan, mode, S, delta, int(rng.integers(0, 2**63)), int(rng.integers(0, 2**62))
+
+
+def test_deep_hops_and_wide_fanouts_match_brute_force():
+    """The whole accepted range of the sampler's arguments: 5-8 hops (the
+    alternating per-hop buffers of paths and windows wrap several times) and
+    fanouts from 71 up to the maximum of 1024, against the brute force, on
+    dense graphs whose windows are mostly non-empty."""
+    rng = np.random.default_rng(58)
+    deep = wide = 0
+    for trial in range(32):
+        N, src, dst, ts, eid, und, roots, rts, fan, mode, S, delta, seed, base = _deep_case(rng, trial)
+        g = oracle.build_tcsr(src, dst, ts, eid, N, und)
+        got = oracle.sample(g, roots, rts, fan, mode, S, delta, seed, base)
+        want = brute.sample(src, dst, ts, eid, N, und, roots, rts, fan, mode, S, delta, seed, base)
+        assert_hops_equal(got, want, "trial %d fan %s" % (trial, fan))
+        deep += len(fan) >= 5 and int((got[-1].nbr >= 0).sum()) > 0
+        wide += fan[0] > 70 and int((got[0].nbr >= 0).sum()) > 70
+    assert deep >= 8 and wide >= 8, (deep, wide)
