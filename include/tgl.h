@@ -94,6 +94,23 @@ typedef struct tgl_node {
 } tgl_node;
 
 /*
+ * The neighbour's history before an entry: for entry p = (owner u, neighbour
+ * v, time t), the positions [lo, hi) of v's own run whose timestamps are
+ * below t, i.e. lo = indptr[v] and hi = lo + #{entries of v with ts < t}
+ * ({0, 0} for a neighbour id outside [0, num_nodes)).  A root of a later hop
+ * made from this entry is (v, t), and without snapshots its candidates are
+ * exactly these entries: the search Algorithm 1 runs for layers > 0, done
+ * once per entry when the T-CSR is built.  With it, the sampler gathers an
+ * entry's span together with the entry and serves the next hop's root
+ * without reading its node record or searching its run.  hi == lo is the
+ * TGL_NBR_FIRST hint.
+ */
+typedef struct tgl_span {
+    uint32_t lo;
+    uint32_t hi;
+} tgl_span;
+
+/*
  * Non-owning view of a T-CSR (Section 3.1): node x owns entries
  * [indptr[x], indptr[x+1]) of `entries`, sorted by ts ascending (ties in any
  * fixed order; tgl_tcsr_build uses input order).  Timestamps must not be NaN.
@@ -112,6 +129,11 @@ typedef struct tgl_node {
  *                     timestamps, small enough to stay in cache), then reads
  *                     at most TGL_INDEX_STRIDE - 1 timestamps of the run.
  *                     Results are the same with or without it.
+ *   hist     [device] tgl_span[num_entries], 8-byte aligned, or NULL: the
+ *                     neighbour's history before each entry (see tgl_span).
+ *                     Read by calls with one snapshot of infinite length and
+ *                     more than one hop; results are the same with or
+ *                     without it.
  * num_entries must be at most 2^32 - 1.  The sampler clamps every indptr
  * value into [0, num_entries], so a malformed view yields wrong samples but
  * never an out-of-bounds access.
@@ -124,6 +146,7 @@ typedef struct tgl_tcsr {
     const float *ts;
     const tgl_node *nodes;
     const float *ts_index;
+    const tgl_span *hist;
 } tgl_tcsr;
 
 /*
@@ -178,6 +201,8 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  *   nodes_out  [device] tgl_node[num_nodes]   output, 128-byte aligned
  *   ts_index_out [device] float[tgl_index_len(M)] output, 16-byte aligned, or
  *                                             NULL (no search index)
+ *   hist_out   [device] tgl_span[M]           output, 8-byte aligned, or NULL
+ *                                             (no neighbour histories)
  *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
  * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
  * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
@@ -189,7 +214,7 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          tgl_node *nodes_out, float *ts_index_out, void *workspace,
+                          tgl_node *nodes_out, float *ts_index_out, tgl_span *hist_out, void *workspace,
                           size_t workspace_bytes, void *stream);
 
 /* Length of the search index of a T-CSR with num_entries entries:
@@ -197,9 +222,10 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
 int64_t tgl_index_len(int64_t num_entries);
 
 /*
- * Writes the per-node summaries, the search index (if ts_index is not NULL)
- * and the TGL_NBR_FIRST hints (if entries is not NULL) of a T-CSR given by its
- * indptr and timestamp arrays (for a T-CSR built elsewhere and uploaded).
+ * Writes the per-node summaries, the search index (if ts_index is not NULL),
+ * the TGL_NBR_FIRST hints (if entries is not NULL) and the neighbour
+ * histories (if hist is not NULL) of a T-CSR given by its indptr, timestamp
+ * and entry arrays (for a T-CSR built elsewhere and uploaded).
  *   indptr     [device] int64[num_nodes + 1]
  *   ts         [device] float[num_entries]
  *   num_nodes  in [1, 2^31 - 1];  num_entries in [0, 2^32 - 1]
@@ -211,11 +237,13 @@ int64_t tgl_index_len(int64_t num_entries);
  *              neighbour's run has no timestamp below the entry's ts; clear
  *              for a neighbour id outside [0, num_nodes)), the other fields
  *              are left alone
+ *   hist       [device] tgl_span[num_entries], 8-byte aligned, output, or
+ *              NULL; requires entries
  * indptr values are clamped into [0, num_entries].  Never synchronises.
  */
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
                           int64_t num_entries, tgl_node *nodes, float *ts_index,
-                          tgl_entry *entries, void *stream);
+                          tgl_entry *entries, tgl_span *hist, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */

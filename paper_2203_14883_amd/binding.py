@@ -54,7 +54,7 @@ class TglError(RuntimeError):
 class c_tcsr(C.Structure):
     _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
                 ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p),
-                ("nodes", C.c_void_p), ("ts_index", C.c_void_p)]
+                ("nodes", C.c_void_p), ("ts_index", C.c_void_p), ("hist", C.c_void_p)]
 
 
 class c_table(C.Structure):
@@ -100,11 +100,11 @@ def lib() -> C.CDLL:
     L.tgl_tcsr_build_workspace.restype = C.c_size_t
     L.tgl_tcsr_build_workspace.argtypes = [i64, i64, u32]
     L.tgl_tcsr_build.restype = i32
-    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, P, C.c_size_t, P]
+    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, P, P, C.c_size_t, P]
     L.tgl_index_len.restype = i64
     L.tgl_index_len.argtypes = [i64]
     L.tgl_tcsr_nodes.restype = i32
-    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P, P]
+    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P, P, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -176,13 +176,15 @@ class TCSR:
     128-byte records (uint32 start, uint32 end, float32 first ts, float32 last
     ts, then float32 ts of the run's first 28 entries, +inf beyond);
     ts_index float32[ceil(M / 32)], every 32nd timestamp (the search index), or
-    None."""
+    None; hist int32[M, 2], per entry the positions [lo, hi) of the neighbour's
+    entries older than it (the neighbour's history), or None."""
     indptr: torch.Tensor
     entries: torch.Tensor
     ts: torch.Tensor
     nodes: torch.Tensor
     num_nodes: int
     ts_index: Optional[torch.Tensor] = None
+    hist: Optional[torch.Tensor] = None
 
     @property
     def num_entries(self) -> int:
@@ -211,7 +213,8 @@ class TCSR:
         return c_tcsr(self.num_nodes, m, self.indptr.data_ptr(),
                       self.entries.data_ptr() if m else None, self.ts.data_ptr() if m else None,
                       self.nodes.data_ptr(),
-                      self.ts_index.data_ptr() if m and self.ts_index is not None else None)
+                      self.ts_index.data_ptr() if m and self.ts_index is not None else None,
+                      self.hist.data_ptr() if m and self.hist is not None else None)
 
 
 def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray:
@@ -228,10 +231,12 @@ def index_len(num_entries: int) -> int:
     return int(lib().tgl_index_len(int(num_entries)))
 
 
-def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hints: bool = True) -> TCSR:
+def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hints: bool = True,
+                   hist: bool = True) -> TCSR:
     """Uploads a T-CSR given as host arrays (e.g. one built elsewhere) and
-    computes its node summaries, if `index` its search index, and if `hints`
-    the neighbour-first hint bits (else they stay clear)."""
+    computes its node summaries, if `index` its search index, if `hints` the
+    neighbour-first hint bits (else they stay clear) and if `hist` the
+    neighbour histories."""
     rec = pack_entries(nbr, ts, eid)
     ent = torch.from_numpy(rec).to(device)
     tsa = torch.from_numpy(np.ascontiguousarray(np.asarray(ts, np.float32))).to(device)
@@ -243,10 +248,13 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hint
     nodes = torch.empty((n, NODE_WORDS), dtype=torch.int32, device=device)
     m = int(ent.shape[0])
     tsx = torch.empty(index_len(m), dtype=torch.float32, device=device) if index else None
+    hs = torch.empty((m, 2), dtype=torch.int32, device=device) if hist else None
     _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if m else None, n, m, _p(nodes),
-                                _p(tsx) if index and m else None, _p(ent) if hints and m else None,
-                                _stream()), "tgl_tcsr_nodes")
-    return TCSR(ip, ent, tsa, nodes, n, tsx)
+                                _p(tsx) if index and m else None, _p(ent) if (hints or hist) and m else None,
+                                _p(hs) if hist and m else None, _stream()), "tgl_tcsr_nodes")
+    if hist and not hints and m:
+        ent.view(torch.int32)[:, 0] &= NBR_MASK     # histories need the entries; keep the hint bits clear
+    return TCSR(ip, ent, tsa, nodes, n, tsx, hs)
 
 
 def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:
@@ -256,9 +264,11 @@ def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True
 
 def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
                eid: Optional[torch.Tensor], num_nodes: int, undirected: bool = True,
-               workspace: Optional[torch.Tensor] = None, stream=None, index: bool = True) -> TCSR:
+               workspace: Optional[torch.Tensor] = None, stream=None, index: bool = True,
+               hist: bool = True) -> TCSR:
     """Builds the T-CSR of a device COO (int32 src/dst, float32 ts, int64 eid or
-    None), with its search index if `index`."""
+    None), with its search index if `index` and its neighbour histories if
+    `hist`."""
     L = lib()
     m0 = int(src.shape[0])
     flags = BUILD_UNDIRECTED if undirected else 0
@@ -274,6 +284,7 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     tsa = torch.empty(M, dtype=torch.float32, device=dev)
     nodes = torch.empty((num_nodes, NODE_WORDS), dtype=torch.int32, device=dev)
     tsx = torch.empty(index_len(M), dtype=torch.float32, device=dev) if index else None
+    hs = torch.empty((M, 2), dtype=torch.int32, device=dev) if hist else None
     need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
     if need == 0:
         raise TglError(EINVAL, "tgl_tcsr_build_workspace")
@@ -282,12 +293,12 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     s = L.tgl_tcsr_build(_p(src), _p(dst), _p(ts), _p(eid), m0, num_nodes, flags, _p(indptr),
                          _p(entries) if M else None, _p(tsa) if M else None, _p(nodes),
-                         _p(tsx) if index and M else None, _p(workspace), workspace.numel(),
-                         _stream(stream))
+                         _p(tsx) if index and M else None, _p(hs) if hist and M else None, _p(workspace),
+                         workspace.numel(), _stream(stream))
     if own_ws:
         del workspace
     _check(s, "tgl_tcsr_build")
-    return TCSR(indptr, entries, tsa, nodes, num_nodes, tsx)
+    return TCSR(indptr, entries, tsa, nodes, num_nodes, tsx, hs)
 
 
 # --------------------------------------------------------------------------

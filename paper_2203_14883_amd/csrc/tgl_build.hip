@@ -580,6 +580,63 @@ __global__ __launch_bounds__(kBlock) void first_hint_kernel(int4 *__restrict__ e
     }
 }
 
+// Neighbour histories (tgl_span): entry p with neighbour v and time t gets
+// hist[p] = {lo, hi}, lo the start of v's run and hi = lo + #{entries of v
+// with ts < t} -- where a root (v, t) of a later hop finds its candidates
+// when windows are unbounded below.  v's node record answers alone when t is
+// at or below its first timestamp, above its last, or inside the first
+// TGL_NODE_INLINE timestamps (held in the record); otherwise a binary search
+// of the rest of the run, which then holds an entry at or above t (the last
+// one).  A neighbour id outside [0, N) gets {0, 0}.
+__global__ __launch_bounds__(kBlock) void hist_kernel(const int4 *__restrict__ ent, const float *__restrict__ ts,
+                                                      int64_t M, const int4 *__restrict__ nodes, int64_t N,
+                                                      uint2 *__restrict__ hist) {
+    const int2 *const head = reinterpret_cast<const int2 *>(ent);  // (nbr, ts) of each 16-byte entry
+    const int64_t gstride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += gstride) {
+        const int2 e = head[2 * p];
+        const uint32_t x = static_cast<uint32_t>(e.x) & TGL_NBR_MASK;
+        const float t = __int_as_float(e.y);
+        uint32_t lo = 0, hi = 0;
+        if (static_cast<int64_t>(x) < N) {
+            const int4 *const rec = nodes + static_cast<int64_t>(x) * 8;
+            const int4 h = rec[0];
+            const uint32_t um = static_cast<uint32_t>(M);
+            uint32_t a = static_cast<uint32_t>(h.x), b = static_cast<uint32_t>(h.y);
+            a = a > um ? um : a;
+            b = b < a ? a : (b > um ? um : b);
+            lo = a;
+            if (!(__int_as_float(h.z) < t)) {
+                hi = a;                                   // nothing below t (or t is NaN)
+            } else if (__int_as_float(h.w) < t) {
+                hi = b;                                   // the whole run
+            } else {
+                uint32_t c = 0;                           // inline timestamps below t (+inf past the run)
+#pragma unroll
+                for (int q = 1; q <= TGL_NODE_INLINE / 4; q++) {
+                    const int4 w = rec[q];
+                    c += (__int_as_float(w.x) < t) + (__int_as_float(w.y) < t) + (__int_as_float(w.z) < t) +
+                         (__int_as_float(w.w) < t);
+                }
+                if (c < TGL_NODE_INLINE || b - a <= TGL_NODE_INLINE) {
+                    hi = a + c;
+                } else {
+                    // the first position of [a + TGL_NODE_INLINE, b) with ts >= t;
+                    // ts[b - 1] (the last timestamp) is one
+                    uint32_t l = a + TGL_NODE_INLINE, r = b - 1;
+                    while (l < r) {
+                        const uint32_t m = l + (r - l) / 2;
+                        if (ts[m] < t) l = m + 1;
+                        else r = m;
+                    }
+                    hi = l;
+                }
+            }
+        }
+        hist[p] = make_uint2(lo, hi);
+    }
+}
+
 // Search index: every TGL_INDEX_STRIDE-th timestamp.
 __global__ __launch_bounds__(kBlock) void index_kernel(const float *__restrict__ ts, int64_t L,
                                                        float *__restrict__ idx) {
@@ -689,13 +746,14 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          tgl_node *nodes_out, float *ts_index_out, void *workspace,
+                          tgl_node *nodes_out, float *ts_index_out, tgl_span *hist_out, void *workspace,
                           size_t workspace_bytes, void *stream) {
     if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
     if (num_edges > 0 && (!src || !dst || !ts || !entries || !ts_out)) return TGL_EINVAL;
     if (!indptr || !nodes_out) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(nodes_out) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_index_out) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(hist_out) & 7u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_out) & 15u) != 0) return TGL_EINVAL;
     const int64_t m0 = num_edges;
@@ -808,6 +866,10 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         const int64_t L = tgl_index_len(M);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts_out, L, ts_index_out);
     }
+    if (hist_out)
+        hist_kernel<<<grid_for(M), kBlock, 0, st>>>(reinterpret_cast<const int4 *>(entries), ts_out, M,
+                                                    reinterpret_cast<const int4 *>(nodes_out), num_nodes,
+                                                    reinterpret_cast<uint2 *>(hist_out));
     return launch_status();
 }
 
@@ -818,13 +880,15 @@ int64_t tgl_index_len(int64_t num_entries) {
 
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
                           int64_t num_entries, tgl_node *nodes, float *ts_index, tgl_entry *entries,
-                          void *stream) {
+                          tgl_span *hist, void *stream) {
     if (num_nodes < 1 || num_nodes > INT32_MAX) return TGL_EINVAL;
     if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
     if (!indptr || !nodes || (num_entries > 0 && !ts)) return TGL_EINVAL;
+    if (hist && num_entries > 0 && !entries) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(nodes) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_index) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(hist) & 7u) != 0) return TGL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
@@ -837,6 +901,10 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
         const int64_t L = tgl_index_len(num_entries);
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts, L, ts_index);
     }
+    if (hist && num_entries > 0)
+        hist_kernel<<<grid_for(num_entries), kBlock, 0, st>>>(reinterpret_cast<const int4 *>(entries), ts, num_entries,
+                                                              reinterpret_cast<const int4 *>(nodes), num_nodes,
+                                                              reinterpret_cast<uint2 *>(hist));
     return launch_status();
 }
 

@@ -54,6 +54,7 @@ struct HopArgs {
     uint32_t nx;                // its length
     const int4 *nodes;          // tgl_node per node (8 x 16 bytes): run start, end, first ts,
                                 // last ts, then the run's first timestamps
+    const uint2 *hist;          // tgl_span per entry: the neighbour's entries older than it
     int64_t num_nodes;
     int64_t num_entries;
     // hop 1: dense roots
@@ -72,6 +73,7 @@ struct HopArgs {
     int64_t p_groups_static;    // previous hop's groups (hop 1 groups: R*S) ...
     const int64_t *p_groups_dyn; // ... or read on the device (roots of hop >= 2)
     const uint8_t *p_first;     // TGL_NBR_FIRST hint of each previous-hop slot, or null
+    const uint2 *p_win;         // window of each previous-hop slot's root (hist of its entry)
     // parameters
     uint64_t root_base;
     int32_t S;                  // snapshots
@@ -94,6 +96,7 @@ struct HopArgs {
     float *o_t0;                // hop-1 ancestor time of each root, for a later hop (anchor A, or null)
     uint64_t *o_path;           // path of each root, for a later hop (or null)
     uint8_t *o_first;           // TGL_NBR_FIRST hint of each slot, for the next hop (or null)
+    uint2 *o_win;               // hist of each valid slot's entry, for the next hop (WIN kernels)
     int64_t *count0_out;        // hop 1 stores its root count here
 };
 
@@ -530,6 +533,53 @@ __device__ __forceinline__ void emit_slot(const HopArgs &p, int64_t o, bool vali
     }
 }
 
+// Output arrays of one chunk, offset to its first slot: a slot is then
+// addressed by a 32-bit offset from a wavefront-uniform base.
+struct OutRow {
+    int32_t *nbr;
+    int64_t *eid;
+    float *ts;
+    float *dt;
+    uint8_t *first;             // TGL_NBR_FIRST hint per slot, or null
+    uint2 *win;                 // next hop's window per valid slot, or null
+};
+
+// emit_slot for slot e of the chunk whose outputs start at o.
+template <bool LAST>
+__device__ __forceinline__ void emit_at(const OutRow &o, uint32_t e, bool valid, int4 v, float t) {
+    int32_t nbr = -1;
+    int64_t eid = -1;
+    float ts = -1.0f, dt = -1.0f;
+    if constexpr (!LAST) {
+        if (o.first) o.first[e] = valid && v.x < 0 ? 1 : 0;
+    }
+    if (valid) {
+        nbr = static_cast<int32_t>(static_cast<uint32_t>(v.x) & TGL_NBR_MASK);
+        ts = __int_as_float(v.y);
+        eid = static_cast<int64_t>(static_cast<uint32_t>(v.z)) | (static_cast<int64_t>(v.w) << 32);
+        dt = static_cast<float>(static_cast<double>(t) - static_cast<double>(ts));
+    }
+    if constexpr (LAST) {
+        __builtin_nontemporal_store(nbr, o.nbr + e);
+        __builtin_nontemporal_store(eid, o.eid + e);
+        __builtin_nontemporal_store(ts, o.ts + e);
+        __builtin_nontemporal_store(dt, o.dt + e);
+    } else {
+        o.nbr[e] = nbr;
+        o.eid[e] = eid;
+        o.ts[e] = ts;
+        o.dt[e] = dt;
+    }
+}
+
+// A 64-bit value that is the same in every active lane, moved to scalar
+// registers.
+__device__ __forceinline__ int64_t uniform64(int64_t v) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+    const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(static_cast<uint64_t>(v) >> 32));
+    return static_cast<int64_t>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 // The T-CSR records of U picks (UINT32_MAX: no pick), with all U loads in
 // flight together.  A lane without a pick reads entry 0 and its caller
 // ignores the record: predicating the loads instead would put each behind a
@@ -544,6 +594,28 @@ __device__ __forceinline__ void gather_records(const int4 *__restrict__ ent, uin
     }
 #pragma unroll
     for (int u = 0; u < U; u++) rec[u] = ent[pick[u] != UINT32_MAX ? pick[u] : 0u];
+}
+
+// gather_records plus each pick's neighbour history, all loads in flight
+// together (a lane without a pick reads entry 0).
+template <int U>
+__device__ __forceinline__ void gather_records_hist(const int4 *__restrict__ ent, const uint2 *__restrict__ hist,
+                                                    uint32_t M, const uint32_t (&pick)[U], int4 (&rec)[U],
+                                                    uint2 (&hv)[U]) {
+    if (M == 0) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            rec[u] = make_int4(-1, -1, -1, -1);
+            hv[u] = make_uint2(0u, 0u);
+        }
+        return;
+    }
+#pragma unroll
+    for (int u = 0; u < U; u++) {
+        const uint32_t q = pick[u] != UINT32_MAX ? pick[u] : 0u;
+        rec[u] = ent[q];
+        hv[u] = hist[q];
+    }
 }
 
 __device__ __forceinline__ void wave_sync_lds() {
@@ -742,6 +814,15 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     if (p.count0_out && blockIdx.x == 0 && threadIdx.x == 0) *p.count0_out = nv;
     const int64_t nchunks = (nv + kWave - 1) / kWave;
     const uint64_t hop_key = static_cast<uint64_t>(p.hop) << 40;
+    // phase 3 serves slot e = lane + 64 n of a chunk in round n: its root
+    // i = e / (W k), window s and rank j (e % (W k) = s k + j) start at those
+    // of e = lane and advance by the mixed-radix digits of 64 per round
+    const int dj = kWave % k;
+    const int ds = (kWave / k) % W;
+    const int di = (kWave / k) / W;
+    const int li0 = lane / nslots;
+    const int ls0 = (lane - li0 * nslots) / k;
+    const int lj0 = lane - li0 * nslots - ls0 * k;
 
     for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w; c < nchunks;
          c += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
@@ -830,16 +911,31 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
         // ---- phase 3: one lane per slot ----
         const int total = nvalid * nslots;
         const int64_t obase = c * kWave * static_cast<int64_t>(nslots);
+        OutRow orow{p.o_nbr + obase, p.o_eid + obase, p.o_ts + obase, p.o_dt + obase, nullptr};
+        if constexpr (!LAST) orow.first = p.o_first ? p.o_first + obase : nullptr;
+        int ci = li0, cs = ls0, cj = lj0;           // (i, s, j) of this lane's slot in the round
         for (int e0 = 0; e0 < total; e0 += U * kWave) {
             uint32_t pick[U];                       // UINT32_MAX: PAD slot
+            int iu[U];
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
                 const bool act = e < total;
-                const int i = act ? e / nslots : 0;
-                const int r = e - i * nslots;
-                const int s = act ? r / k : 0;
-                const int j = r - s * k;
+                const int i = act ? ci : 0;
+                const int s = act ? cs : 0;
+                const int j = cj;
+                iu[u] = i;
+                cj += dj;
+                cs += ds;
+                ci += di;
+                if (cj >= k) {
+                    cj -= k;
+                    cs += 1;
+                }
+                if (cs >= W) {
+                    cs -= W;
+                    ci += 1;
+                }
                 const uint32_t whi = r_e[w][i * kMultiEdges + s];
                 uint32_t wlo = r_e[w][i * kMultiEdges + s + 1];
                 if (wlo > whi) wlo = whi;
@@ -858,7 +954,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
-                if (e < total) emit_slot<LAST>(p, obase + e, pick[u] != UINT32_MAX, rec[u], r_t[w][e / nslots]);
+                if (e < total) emit_at<LAST>(orow, static_cast<uint32_t>(e), pick[u] != UINT32_MAX, rec[u], r_t[w][iu[u]]);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows
@@ -912,9 +1008,15 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
 //   phase 3, one lane per slot: selection, gather and emit.  The packed roots
 //     have consecutive indices, so the slots of a chunk are one contiguous
 //     range of the output and the stores coalesce.
-template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 ? 7 : 6))) void hop_single_kernel(const HopArgs p) {
+// WIN (one window unbounded below, a T-CSR with neighbour histories): the
+// window of a root of hop >= 2 is the history of the entry it came from,
+// which the previous hop gathered with the entry; phase 1 takes it from
+// there, and reads no node record and leaves nothing to search.  A hop that
+// is not the last gathers the histories of its picks for the next hop.
+template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR, bool WIN>
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !FIRST ? 8 : (NB == 1 ? 7 : 6)))) void hop_single_kernel(const HopArgs p) {
     static_assert(FIRST || !PTR, "saved window edges are kept for hop 1 only");
+    static_assert(!WIN || NB == 1, "histories give windows unbounded below");
     constexpr int GPW = kWave / G;            // roots located per wavefront round
     constexpr int U = 4;                      // slots per lane whose loads are in flight together
     const int lane = lane_id();
@@ -925,10 +1027,11 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
     __shared__ uint32_t r_n[kWavesPerBlock][kWave];    // run end, then window size
     __shared__ float r_f[kWavesPerBlock][kWave];       // first and last timestamp of the run
     __shared__ float r_l[kWavesPerBlock][kWave];
-    __shared__ int64_t r_q[kWavesPerBlock][kWave];
-    __shared__ uint64_t r_hp[kWavesPerBlock][kWave];   // uniform: mix64(seedmix ^ path)
+    __shared__ int64_t r_q0[kWavesPerBlock];           // index of the first packed root
+    // uniform: mix64(seedmix ^ path) ^ (hop << 40 | s << 24), so that the
+    // draw of rank j hashes it ^ j (the key fields do not overlap)
+    __shared__ uint64_t r_hp[kWavesPerBlock][kWave];
     __shared__ float r_t[kWavesPerBlock][kWave];
-    __shared__ int32_t r_s[kWavesPerBlock][kWave];
     __shared__ int32_t r_x[kWavesPerBlock][kWave];     // node of each packed root
     __shared__ float r_vh[kWavesPerBlock][kWave];      // window thresholds: vl <= ts < vh
     __shared__ float r_vl[kWavesPerBlock][NB == 2 ? kWave : 1];
@@ -948,6 +1051,13 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
     const uint64_t path1 = p.root_base * S * static_cast<uint64_t>(pk);   // hop-1 children: + v
     const int k = p.k;
     const uint64_t hop_key = static_cast<uint64_t>(p.hop) << 40;
+    // phase 3 serves slot e = lane + 64 n of a chunk in round n: its root
+    // e / k and rank e % k start at (lane / k, lane % k) and advance by
+    // (64 / k, 64 % k) per round, with a carry
+    const int di = kWave / k;
+    const int dj = kWave - di * k;
+    const int li0 = lane / k;
+    const int lj0 = lane - li0 * k;
 
     for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + w; c < nchunks;
          c += static_cast<int64_t>(gridDim.x) * kWavesPerBlock) {
@@ -997,22 +1107,37 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                 }
             }
         }
-        // a root whose entry carried the hint has an empty window: its node
-        // record is not read
-        bool known_empty = false;
-        if constexpr (!FIRST) known_empty = valid && p.p_first && p.p_first[v] != 0;
-        const NodeRun run = node_run(p, x, valid && !known_empty);
-        // window thresholds; with the root anchor the window also ends below t
-        float vh = bound_value(ta, s, p.delta);
-        if (p.anchor == TGL_ANCHOR_ROOT && t < vh) vh = t;
-        const float vl = NB == 2 ? bound_value(ta, s + 1, p.delta) : 0.0f;
-        // window edges the run's first and last timestamps decide
-        uint32_t lo = run.a, hi = run.a;
+        NodeRun run{0u, 0u, 0.0f, 0.0f};
+        float vh = 0.0f, vl = 0.0f;
+        uint32_t lo = 0, hi = 0;
         bool need = false;
-        if (valid) {
-            need = !edge_from_summary(run.a, run.b, run.first, run.last, vh, hi);
-            if constexpr (NB == 2) need |= !edge_from_summary(run.a, run.b, run.first, run.last, vl, lo);
-            if (lo > hi) lo = hi;
+        if constexpr (WIN && !FIRST) {
+            // the window is the history of the entry this root came from,
+            // clamped into the entries
+            if (valid) {
+                const uint2 wv = p.p_win[v];
+                const uint32_t M = static_cast<uint32_t>(p.num_entries);
+                hi = wv.y < M ? wv.y : M;
+                lo = wv.x < hi ? wv.x : hi;
+            }
+        } else {
+            // a root whose entry carried the hint has an empty window: its node
+            // record is not read
+            bool known_empty = false;
+            if constexpr (!FIRST) known_empty = valid && p.p_first && p.p_first[v] != 0;
+            run = node_run(p, x, valid && !known_empty);
+            // window thresholds; with the root anchor the window also ends below t
+            vh = bound_value(ta, s, p.delta);
+            if (p.anchor == TGL_ANCHOR_ROOT && t < vh) vh = t;
+            if constexpr (NB == 2) vl = bound_value(ta, s + 1, p.delta);
+            // window edges the run's first and last timestamps decide
+            lo = run.a;
+            hi = run.a;
+            if (valid) {
+                need = !edge_from_summary(run.a, run.b, run.first, run.last, vh, hi);
+                if constexpr (NB == 2) need |= !edge_from_summary(run.a, run.b, run.first, run.last, vl, lo);
+                if (lo > hi) lo = hi;
+            }
         }
         const uint64_t mask = __ballot(valid);
         const uint64_t need_mask = __ballot(valid && need);
@@ -1020,16 +1145,19 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
             const int r = rank_below(mask);
             r_lo[w][r] = need ? run.a : lo;
             r_n[w][r] = need ? run.b : hi - lo;
-            r_f[w][r] = run.first;
-            r_l[w][r] = run.last;
-            r_q[w][r] = q;
-            r_hp[w][r] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ path) : 0;
+            if (r == 0) r_q0[w] = q;             // packed roots are q0, q0 + 1, ...
+            r_hp[w][r] = MODE == TGL_UNIFORM
+                             ? mix64(p.seedmix ^ path) ^ hop_key ^ (static_cast<uint64_t>(static_cast<uint32_t>(s)) << 24)
+                             : 0;
             r_t[w][r] = t;
-            r_s[w][r] = s;
-            r_x[w][r] = x;
-            r_vh[w][r] = vh;
-            if constexpr (NB == 2) r_vl[w][r] = vl;
-            if (need) r_need[w][rank_below(need_mask)] = static_cast<uint8_t>(r);
+            if constexpr (!(WIN && !FIRST)) {
+                r_f[w][r] = run.first;
+                r_l[w][r] = run.last;
+                r_x[w][r] = x;
+                r_vh[w][r] = vh;
+                if constexpr (NB == 2) r_vl[w][r] = vl;
+                if (need) r_need[w][rank_below(need_mask)] = static_cast<uint8_t>(r);
+            }
             if (!need && p.o_cnt) {
                 const uint32_t n = hi - lo;
                 p.o_cnt[q] = MODE == TGL_MOST_RECENT ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
@@ -1041,7 +1169,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
         const int nneed = __popcll(need_mask);
 
         // ---- phase 2: G lanes per root search the windows phase 1 left open ----
-        for (int base = 0; base < nneed; base += GPW) {
+        for (int base = 0; base < (WIN && !FIRST ? 0 : nneed); base += GPW) {
             if (base + gw < nneed) {                // group-uniform
                 const int i = r_need[w][base + gw];
                 uint32_t wlo, whi;
@@ -1052,7 +1180,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
                     r_n[w][i] = whi - wlo;
                     if (p.o_cnt) {
                         const uint32_t n = whi - wlo;
-                        p.o_cnt[r_q[w][i]] = MODE == TGL_MOST_RECENT
+                        p.o_cnt[r_q0[w] + i] = MODE == TGL_MOST_RECENT
                                                  ? static_cast<int32_t>(n < static_cast<uint32_t>(k) ? n : k)
                                                  : (n > 0 ? k : 0);
                     }
@@ -1062,36 +1190,57 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
         wave_sync_lds();
 
         // ---- phase 3: one lane per slot ----
+        // slot e of the chunk (root i = e / k, rank j = e % k) is output
+        // q0 * k + e, packed roots having consecutive indices
         const int total = nvalid * k;
+        const int64_t obase = total > 0 ? uniform64(r_q0[w]) * k : 0;
+        OutRow orow{p.o_nbr + obase, p.o_eid + obase, p.o_ts + obase, p.o_dt + obase, nullptr, nullptr};
+        if constexpr (!LAST && !WIN) orow.first = p.o_first ? p.o_first + obase : nullptr;
+        if constexpr (!LAST && WIN) orow.win = p.o_win + obase;
+        int ci = li0, cj = lj0;                     // (i, j) of this lane's slot in the round
         for (int e0 = 0; e0 < total; e0 += U * kWave) {
             uint32_t pick[U];                       // UINT32_MAX: PAD slot
+            int iu[U];
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
                 const bool act = e < total;
-                const int i = act ? e / k : 0;
-                const int j = e - i * k;
+                const int i = act ? ci : 0;
+                const int j = cj;
+                iu[u] = i;
+                cj += dj;
+                ci += di;
+                if (cj >= k) {
+                    cj -= k;
+                    ci += 1;
+                }
                 const uint32_t lo = r_lo[w][i];
                 const uint32_t n = r_n[w][i];
                 if constexpr (MODE == TGL_MOST_RECENT) {
                     pick[u] = act && static_cast<uint32_t>(j) < n ? lo + n - 1 - static_cast<uint32_t>(j) : UINT32_MAX;
                 } else {
-                    const uint64_t key = hop_key | (static_cast<uint64_t>(r_s[w][i]) << 24) | static_cast<uint64_t>(j);
                     pick[u] = act && n > 0
-                                  ? lo + static_cast<uint32_t>(__umul64hi(mix64(r_hp[w][i] ^ key), static_cast<uint64_t>(n)))
+                                  ? lo + static_cast<uint32_t>(__umul64hi(mix64(r_hp[w][i] ^ static_cast<uint64_t>(j)),
+                                                                          static_cast<uint64_t>(n)))
                                   : UINT32_MAX;
                 }
             }
             int4 rec[U];
-            gather_records<U>(p.ent, static_cast<uint32_t>(p.num_entries), pick, rec);
+            if constexpr (WIN && !LAST) {
+                uint2 hv[U];
+                gather_records_hist<U>(p.ent, p.hist, static_cast<uint32_t>(p.num_entries), pick, rec, hv);
+#pragma unroll
+                for (int u = 0; u < U; u++) {
+                    const int e = e0 + u * kWave + lane;
+                    if (e < total && pick[u] != UINT32_MAX) orow.win[e] = hv[u];
+                }
+            } else {
+                gather_records<U>(p.ent, static_cast<uint32_t>(p.num_entries), pick, rec);
+            }
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
-                if (e < total) {
-                    const int i = e / k;
-                    const int j = e - i * k;
-                    emit_slot<LAST>(p, r_q[w][i] * k + j, pick[u] != UINT32_MAX, rec[u], r_t[w][i]);
-                }
+                if (e < total) emit_at<LAST>(orow, static_cast<uint32_t>(e), pick[u] != UINT32_MAX, rec[u], r_t[w][iu[u]]);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows
@@ -1099,7 +1248,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(NB == 1 
 }
 
 template <int MODE, bool LAST>
-void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t work, hipStream_t st) {
+void launch_mode_last(int G, bool first, bool multi, bool win, const HopArgs &a, int64_t work, hipStream_t st) {
     // `work` candidate roots (hop 1: roots; later hops: previous slots), 64 per wavefront
     int64_t blocks = (work + kBlock - 1) / kBlock;
     if (blocks < 1) blocks = 1;
@@ -1124,26 +1273,30 @@ void launch_mode_last(int G, bool first, bool multi, const HopArgs &a, int64_t w
         // the window search uses 8 lanes per root whatever the fanout; one
         // window edge when windows are unbounded below, else two
         const bool ptr = first && a.ptr;
-        if (a.delta_inf) {
-            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true><<<nb, kBlock, 0, st>>>(a);
-            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 1, false><<<nb, kBlock, 0, st>>>(a);
+        if (win) {                            // windows unbounded below, neighbour histories kept
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true, true><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false, true><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 1, false, true><<<nb, kBlock, 0, st>>>(a);
+        } else if (a.delta_inf) {
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true, false><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false, false><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 1, false, false><<<nb, kBlock, 0, st>>>(a);
         } else {
-            if (ptr) hop_single_kernel<8, MODE, LAST, true, 2, true><<<nb, kBlock, 0, st>>>(a);
-            else if (first) hop_single_kernel<8, MODE, LAST, true, 2, false><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 2, false><<<nb, kBlock, 0, st>>>(a);
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 2, true, false><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 2, false, false><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 2, false, false><<<nb, kBlock, 0, st>>>(a);
         }
     }
 }
 
-void launch_hop(int G, int mode, bool first, bool multi, bool last, const HopArgs &a, int64_t work,
+void launch_hop(int G, int mode, bool first, bool multi, bool last, bool win, const HopArgs &a, int64_t work,
                 hipStream_t st) {
     if (mode == TGL_MOST_RECENT) {
-        last ? launch_mode_last<TGL_MOST_RECENT, true>(G, first, multi, a, work, st)
-             : launch_mode_last<TGL_MOST_RECENT, false>(G, first, multi, a, work, st);
+        last ? launch_mode_last<TGL_MOST_RECENT, true>(G, first, multi, win, a, work, st)
+             : launch_mode_last<TGL_MOST_RECENT, false>(G, first, multi, win, a, work, st);
     } else {
-        last ? launch_mode_last<TGL_UNIFORM, true>(G, first, multi, a, work, st)
-             : launch_mode_last<TGL_UNIFORM, false>(G, first, multi, a, work, st);
+        last ? launch_mode_last<TGL_UNIFORM, true>(G, first, multi, win, a, work, st)
+             : launch_mode_last<TGL_UNIFORM, false>(G, first, multi, win, a, work, st);
     }
 }
 
@@ -1235,15 +1388,17 @@ struct SampleWs {
     int32_t *s[2] = {nullptr, nullptr};       // window per root (hops 2..L-1)
     uint64_t *path[2] = {nullptr, nullptr};   // path per root (hops 2..L-1)
     float *t0[2] = {nullptr, nullptr};        // hop-1 ancestor time per root (hops 2..L-1, root anchor)
-    uint8_t *first[2] = {nullptr, nullptr};   // TGL_NBR_FIRST hint per slot (hops 1..L-1)
+    uint8_t *first[2] = {nullptr, nullptr};   // TGL_NBR_FIRST hint per slot (hops 1..L-1) ...
+    uint2 *win[2] = {nullptr, nullptr};       // ... or, in the same memory, the next hop's windows
     size_t bytes = 0;
 };
 
 // Workspace: per-group counts and offsets for the largest hop h < L (two
 // alternating buffers when L >= 3: hop h writes buffer h & 1, hop h + 1 reads
 // it) and scan partials; window, path and hop-1 ancestor time of the roots of
-// hops 2..L-1 (two alternating buffers); the neighbour-first hint of the
-// slots of hops 1..L-1 (hop h writes buffer h & 1, hop h + 1 reads it).
+// hops 2..L-1 (two alternating buffers); per slot of hops 1..L-1 the
+// neighbour-first hint, or with one snapshot room for the history span of the
+// slot's entry (hop h writes buffer h & 1, hop h + 1 reads it).
 SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S) {
     SampleWs w;
     Carver cv(base);
@@ -1251,7 +1406,14 @@ SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S
         int64_t max_slots = 0;                 // slots of hops 1..L-1
         for (int h = 1; h < hops; h++) max_slots = cap[h] > max_slots ? cap[h] : max_slots;
         const int nfirst = hops >= 3 ? 2 : 1;
-        for (int i = 0; i < nfirst; i++) w.first[(1 + i) & 1] = cv.take<uint8_t>(static_cast<size_t>(max_slots));
+        // a slot carries a hint byte, or with one snapshot the history span of
+        // its entry (when the T-CSR has them)
+        const size_t per_slot = S == 1 ? sizeof(uint2) : 1;
+        for (int i = 0; i < nfirst; i++) {
+            uint8_t *b = cv.take<uint8_t>(static_cast<size_t>(max_slots) * per_slot);
+            w.first[(1 + i) & 1] = b;
+            w.win[(1 + i) & 1] = reinterpret_cast<uint2 *>(b);
+        }
         int64_t max_groups = cap[0] * S;      // hop-1 groups
         for (int h = 2; h < hops; h++) max_groups = cap[h - 1] > max_groups ? cap[h - 1] : max_groups;
         const int ncnt = hops >= 3 ? 2 : 1;
@@ -1320,6 +1482,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
     if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts_index) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->hist) & 7u) != 0) return TGL_EINVAL;
     if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
     int64_t cap[TGL_MAX_HOPS + 1];
     if (!capacities(num_roots, hops, fanouts, num_snapshots, cap)) return TGL_EINVAL;
@@ -1342,6 +1505,11 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
     a.tsx = g->num_entries > 0 ? g->ts_index : nullptr;
     a.nx = static_cast<uint32_t>(tgl_index_len(g->num_entries));
     a.nodes = reinterpret_cast<const int4 *>(g->nodes);
+    // windows of hops >= 2 from the histories of the previous hop's entries:
+    // one snapshot unbounded below (either anchor then places the window of
+    // a root below its own time)
+    const bool win = g->hist && g->num_entries > 0 && num_snapshots == 1 && dinf && hops >= 2;
+    a.hist = win ? reinterpret_cast<const uint2 *>(g->hist) : nullptr;
     a.num_nodes = g->num_nodes;
     a.num_entries = g->num_entries;
     a.rx = roots;
@@ -1375,8 +1543,10 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         a.o_s = keep ? ws.s[h & 1] : nullptr;
         a.o_path = keep ? ws.path[h & 1] : nullptr;
         a.o_t0 = keep && anchor == TGL_ANCHOR_ROOT ? ws.t0[h & 1] : nullptr;
-        a.o_first = last ? nullptr : ws.first[h & 1];
-        a.p_first = h >= 2 ? ws.first[(h - 1) & 1] : nullptr;
+        a.o_first = last || win ? nullptr : ws.first[h & 1];
+        a.p_first = h >= 2 && !win ? ws.first[(h - 1) & 1] : nullptr;
+        a.o_win = !last && win ? ws.win[h & 1] : nullptr;
+        a.p_win = h >= 2 && win ? ws.win[(h - 1) & 1] : nullptr;
         a.count0_out = h == 1 ? counts : nullptr;
         if (h >= 2) {
             const tgl_hop_out &po = outs[h - 2];
@@ -1396,7 +1566,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
         const int64_t work = h == 1 ? num_roots : cap[h - 1];
         {
             ScopedTimer tm(h == 1 ? TGL_TIMER_HOP1 : TGL_TIMER_HOPN, st);
-            launch_hop(G, mode, h == 1, multi, last, a, work, st);
+            launch_hop(G, mode, h == 1, multi, last, win, a, work, st);
         }
         if (launch_status() != TGL_OK) return TGL_EDEVICE;
         if (last) break;

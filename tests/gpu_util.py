@@ -50,7 +50,65 @@ def first_hints(indptr, nbr, ts):
     return h
 
 
-def tcsr_to_host(g, hints=True):
+def _ordered_bits(ts):
+    """float32 -> int64 keys in [0, 2^32) with the order of the floats (no NaN)."""
+    b = np.asarray(ts, np.float32).view(np.int32).astype(np.int64)
+    return np.where(b >= 0, b | 0x80000000, (~b) & 0xFFFFFFFF)
+
+
+def hist_of(indptr, nbr, ts):
+    """The neighbour history of every entry, from its definition: positions
+    [lo, hi) of the neighbour's run whose timestamps are below the entry's
+    (lo = the run's start); (0, 0) for a neighbour outside the node range.
+    Runs are sorted by time, so lo + #{run timestamps below t} is the lower
+    bound of (neighbour, t) in the (owner, ts) order of all entries."""
+    indptr = np.asarray(indptr, np.int64)
+    nbr = np.asarray(nbr, np.int64)
+    ts = np.asarray(ts, np.float32)
+    n = len(indptr) - 1
+    ok = (nbr >= 0) & (nbr < n)
+    lo = np.zeros(len(nbr), np.int64)
+    hi = np.zeros(len(nbr), np.int64)
+    lo[ok] = indptr[nbr[ok]]
+    owner = np.repeat(np.arange(n, dtype=np.int64), np.diff(indptr))
+    key = (owner << 32) | _ordered_bits(ts)
+    q = (nbr[ok] << 32) | _ordered_bits(ts[ok])
+    order = np.argsort(q, kind="stable")      # sorted queries keep the search in cache
+    pos = np.empty(len(q), np.int64)
+    pos[order] = np.searchsorted(key, q[order], side="left")
+    hi[ok] = pos
+    return lo, hi
+
+
+def check_hist_device(g, chunk=1 << 27):
+    """Neighbour histories of a device T-CSR against their definition,
+    computed on the device in chunks (for T-CSRs too large for the host)."""
+    import torch
+    M, n = g.num_entries, g.num_nodes
+    ip = g.indptr
+
+    def ordered(bits):
+        bits = bits.long()
+        return torch.where(bits >= 0, bits | 0x80000000, (~bits) & 0xFFFFFFFF)
+
+    key = torch.repeat_interleave(torch.arange(n, device=ip.device, dtype=torch.int64), ip[1:] - ip[:-1],
+                                  output_size=M) << 32
+    for c0 in range(0, M, chunk):
+        key[c0:c0 + chunk] |= ordered(g.ts[c0:c0 + chunk].view(torch.int32))
+    words = g.entries.view(torch.int32)
+    hs = g.hist
+    for c0 in range(0, M, chunk):
+        v = (words[c0:c0 + chunk, 0] & 0x7FFFFFFF).long()
+        t = ordered(g.ts[c0:c0 + chunk].view(torch.int32))
+        hi = torch.searchsorted(key, (v << 32) | t)
+        got = hs[c0:c0 + chunk].long() & 0xFFFFFFFF
+        assert torch.equal(got[:, 0], ip[v]), "neighbour history start differs in entries %d.." % c0
+        assert torch.equal(got[:, 1], hi), "neighbour history end differs in entries %d.." % c0
+    del key
+    torch.cuda.empty_cache()
+
+
+def tcsr_to_host(g, hints=True, hist_on_host=True):
     """Host copy of a device T-CSR; checks that the separate timestamp array
     equals the records' timestamps bit for bit, and that the neighbour-first
     hint bits follow their definition (or, with hints=False, are all clear)."""
@@ -81,6 +139,11 @@ def tcsr_to_host(g, hints=True):
     if g.ts_index is not None:
         tsx = g.ts_index.cpu().numpy()
         assert np.array_equal(tsx.view(np.uint32), ts[::32].view(np.uint32)), "search index"
+    if g.hist is not None and hist_on_host:
+        hs = g.hist.cpu().numpy().view(np.uint32).astype(np.int64)
+        lo, hi = hist_of(ip, nbr, ts)
+        assert np.array_equal(hs[:, 0], lo), "neighbour history start: %d differ" % int((hs[:, 0] != lo).sum())
+        assert np.array_equal(hs[:, 1], hi), "neighbour history end: %d differ" % int((hs[:, 1] != hi).sum())
     return oracle.TCSR(g.indptr.cpu().numpy(), nbr.copy(), ent[:, 1].copy(),
                        w[:, 1].copy().view(np.float32))
 

@@ -31,9 +31,9 @@ def assert_tcsr_equal(got, want, what=""):
     assert same_bits(got.ts, want.ts), what + " ts: " + str(first_diff(got.ts, want.ts))
 
 
-def gpu_build(src, dst, ts, eid, n, undirected):
+def gpu_build(src, dst, ts, eid, n, undirected, hist=True):
     return P.tcsr_build(upload(src, np.int32), upload(dst, np.int32), upload(ts, np.float32),
-                        None if eid is None else upload(eid, np.int64), n, undirected)
+                        None if eid is None else upload(eid, np.int64), n, undirected, hist=hist)
 
 
 def gpu_sample(g, roots, rts, fan, mode, S, D, seed, base, anchor="own"):
@@ -74,9 +74,11 @@ def test_random_small_graphs(torch):
     rng = np.random.default_rng(2024)
     for trial in range(160):
         N, src, dst, ts, eid, und, roots, rts, fan, mode, S, D, seed, base = _rand_case(rng)
-        announce("random trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s" % (trial, N, len(src), len(roots), fan, mode, S, D))
+        hist = trial % 3 != 2              # with and without neighbour histories
+        announce("random trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s hist=%s"
+                 % (trial, N, len(src), len(roots), fan, mode, S, D, hist))
         want_g = oracle.build_tcsr(src, dst, ts, eid, N, und)
-        g = gpu_build(src, dst, ts, eid, N, und)
+        g = gpu_build(src, dst, ts, eid, N, und, hist)
         assert_tcsr_equal(tcsr_to_host(g), want_g, "trial %d" % trial)
         want = oracle.sample(want_g, roots, rts, fan, mode, S, D, seed, base)
         got = gpu_sample(g, roots, rts, fan, mode, S, D, seed, base)
@@ -359,11 +361,14 @@ def test_snapshot_anchor_root(torch):
 
 def test_neighbour_first_hints(torch):
     """The neighbour-first hint (bit 31 of a T-CSR entry's nbr) lets a later
-    hop skip the node record of a root with an empty window.  Samples must be
-    the oracle's with the hints set exactly (GPU build, upload), with the hints
-    clear everywhere, and with either snapshot anchor, on random graphs of 2-4
-    hops (directed and undirected, with finite and infinite windows) and on a
-    reduced c4, where about half of the hop-2 roots carry the hint."""
+    hop skip the node record of a root with an empty window, and the
+    neighbour history (per entry, its neighbour's entries older than it)
+    gives a later hop's window outright when windows are unbounded below.
+    Samples must be the oracle's with the hints set exactly or clear
+    everywhere, with and without histories, and with either snapshot anchor,
+    on random graphs of 2-4 hops (directed and undirected, with finite and
+    infinite windows) and on a reduced c4, where about half of the hop-2
+    roots carry the hint."""
     rng = np.random.default_rng(31)
     trial = 0
     while trial < 40:
@@ -376,11 +381,12 @@ def test_neighbour_first_hints(torch):
                  % (trial, N, len(src), len(roots), fan, mode, S, D, anchor))
         og = oracle.build_tcsr(src, dst, ts, eid, N, und)
         want = oracle.sample(og, roots, rts, fan, mode, S, D, seed, base, anchor=anchor)
-        for hints in (True, False):
-            g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints)
-            assert_tcsr_equal(tcsr_to_host(g, hints=hints), og, "hint trial %d (hints=%s)" % (trial, hints))
+        for hints, hist in ((True, True), (True, False), (False, False), (False, True)):
+            g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints, hist=hist)
+            what = "hint trial %d (hints=%s, hist=%s)" % (trial, hints, hist)
+            assert_tcsr_equal(tcsr_to_host(g, hints=hints), og, what)
             got = gpu_sample(g, roots, rts, fan, mode, S, D, seed, base, anchor=anchor)
-            assert_hops_equal(got, want, "hint trial %d (hints=%s)" % (trial, hints))
+            assert_hops_equal(got, want, what)
     w = W.make_c4(num_nodes=1_000_000, num_edges=10_700_000)
     og = oracle.build_tcsr(w.src, w.dst, w.ts, None, w.num_nodes, True)
     roots, rts, base = w.batches(2000, 2008)
@@ -392,11 +398,11 @@ def test_neighbour_first_hints(torch):
     v = want[0].nbr >= 0
     hinted = ~(first[want[0].nbr[v]] < want[0].ts[v])
     assert hinted.mean() > 0.3, "reduced c4: only %.2f of the hop-2 roots are hinted" % hinted.mean()
-    for hints in (True, False):
-        announce("hints=%s on reduced c4" % hints)
-        g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints)
+    for hints, hist in ((True, True), (True, False), (False, False), (False, True)):
+        announce("hints=%s hist=%s on reduced c4" % (hints, hist))
+        g = P.tcsr_from_host(og.indptr, og.nbr, og.ts, og.eid, hints=hints, hist=hist)
         got = gpu_sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
-        assert_hops_equal(got, want, "reduced c4 (hints=%s)" % hints)
+        assert_hops_equal(got, want, "reduced c4 (hints=%s, hist=%s)" % (hints, hist))
 
 
 def test_many_windows(torch):
