@@ -305,6 +305,25 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
                       uint64_t root_base, const tgl_hop_out *outs, int64_t *counts,
                       void *workspace, size_t workspace_bytes, void *stream);
 
+/*
+ * tgl_sample for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops, harnesses that forbid allocation): the
+ * workspace is a fixed area of TGL_NOALLOC_SCRATCH_BYTES bytes that the
+ * library's code object holds on each GPU it is loaded on, until the process
+ * ends.  Arguments, outputs and errors as tgl_sample, without the workspace;
+ * a call whose tgl_sample_workspace(...) exceeds the area returns
+ * TGL_ENOSPACE and enqueues nothing.  The call allocates nothing (the first
+ * call on a device looks up the area's device address).  Every call on one
+ * GPU uses that GPU's one area: calls that overlap on one GPU (several
+ * streams or threads) race and must be serialised by the caller.  Nothing in
+ * the area needs clearing between calls.
+ */
+#define TGL_NOALLOC_SCRATCH_BYTES (128u << 20)
+tgl_status tgl_sample_noalloc(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
+                              int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
+                              int32_t num_snapshots, float snapshot_len, uint64_t seed,
+                              uint64_t root_base, const tgl_hop_out *outs, int64_t *counts, void *stream);
+
 /* Options of tgl_sample_ex (zero-initialise; NULL means all defaults). */
 #define TGL_ANCHOR_OWN  0  /* windows of a hop >= 2 root at its own time t:
                               [t - (s+1) D, t - s D) (the default)              */

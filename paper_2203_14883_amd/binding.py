@@ -29,6 +29,7 @@ KEY_NODE, KEY_EDGE = 0, 1
 MAX_TABLES = 8
 
 NODE_WORDS = 32     # int32 words of one node record (128 bytes)
+NOALLOC_SCRATCH_BYTES = 128 << 20   # workspace area of tgl_sample_noalloc
 NODE_INLINE = 28    # timestamps held inline in a node record
 NBR_MASK = 0x7FFFFFFF     # neighbour id bits of a T-CSR entry's nbr field
 NBR_FIRST = -0x80000000   # bit 31: the neighbour-first hint (as int32)
@@ -40,7 +41,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
            "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
-           "tgl_sample_ex", "tgl_pointers_reset", "tgl_mfg_workspace", "tgl_mfg_export",
+           "tgl_sample_ex", "tgl_sample_noalloc", "tgl_pointers_reset", "tgl_mfg_workspace", "tgl_mfg_export",
            "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset", "tgl_timer_select")
 
@@ -115,6 +116,9 @@ def lib() -> C.CDLL:
     L.tgl_sample_ex.restype = i32
     L.tgl_sample_ex.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
                                 C.POINTER(c_sample_opts), C.POINTER(c_hop_out), P, P, C.c_size_t, P]
+    L.tgl_sample_noalloc.restype = i32
+    L.tgl_sample_noalloc.argtypes = [C.POINTER(c_tcsr), P, P, i64, i32, P, i32, i32, f32, u64, u64,
+                                     C.POINTER(c_hop_out), P, P]
     L.tgl_pointers_reset.restype = i32
     L.tgl_pointers_reset.argtypes = [C.POINTER(c_tcsr), i32, P, P]
     L.tgl_mfg_workspace.restype = C.c_size_t

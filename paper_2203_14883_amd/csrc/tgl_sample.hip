@@ -29,6 +29,8 @@
 //
 // Nothing is synchronised with the host: per-hop root counts stay on the
 // device and the next hop's kernels read them.
+#include <mutex>
+
 #include "tgl_internal.hpp"
 
 namespace tgl {
@@ -1435,6 +1437,65 @@ SampleWs carve_sample_ws(void *base, int32_t hops, const int64_t *cap, int32_t S
     return w;
 }
 
+// Workspace of tgl_sample_noalloc: a fixed area of device memory that the
+// code object holds on every GPU it is loaded on, for callers that cannot
+// allocate.  Host code never uses the array's name as an address: its
+// device address is looked up once per device and kept in scratch_dev.
+// Every call on one GPU shares that GPU's area.
+static __device__ __align__(256) uint8_t scratch[TGL_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+void *scratch_dev[kMaxDevices] = {};
+std::mutex scratch_mu;
+
+// The device address of `scratch` on the current device, looked up on the
+// first call there.
+tgl_status scratch_ptr(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TGL_EDEVICE;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_dev[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return TGL_EDEVICE;
+        scratch_dev[dev] = ptr;
+    }
+    *out = scratch_dev[dev];
+    return TGL_OK;
+}
+
+// Host-side argument checks of tgl_sample_ex (nothing is enqueued on
+// failure); fills cap with the per-hop capacities.
+tgl_status sample_check(const tgl_tcsr *g, const int32_t *roots, const float *root_ts, int64_t num_roots,
+                        int32_t hops, const int32_t *fanouts, int32_t mode, int32_t num_snapshots,
+                        float snapshot_len, const tgl_sample_opts *opts, const tgl_hop_out *outs,
+                        const int64_t *counts, int64_t *cap) {
+    if (!g || !outs || !counts) return TGL_EINVAL;
+    const int32_t anchor = opts ? opts->anchor : TGL_ANCHOR_OWN;
+    if (anchor != TGL_ANCHOR_OWN && anchor != TGL_ANCHOR_ROOT) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(opts ? opts->pointers : nullptr) & 3u) != 0) return TGL_EINVAL;
+    if (!sample_args_ok(num_roots, hops, fanouts, num_snapshots)) return TGL_EINVAL;
+    if (mode != TGL_MOST_RECENT && mode != TGL_UNIFORM) return TGL_EINVAL;
+    if (snapshot_len != snapshot_len || !(snapshot_len > 0.0f)) return TGL_EINVAL;
+    if (__builtin_isinf(snapshot_len) && num_snapshots != 1) return TGL_EINVAL;
+    if (g->num_nodes < 1 || g->num_nodes > INT32_MAX) return TGL_EINVAL;
+    if (g->num_entries < 0 || g->num_entries > static_cast<int64_t>(UINT32_MAX)) return TGL_EINVAL;
+    if (!g->indptr || (g->num_entries > 0 && !g->entries)) return TGL_EINVAL;
+    if (g->num_entries > 0 && !g->ts) return TGL_EINVAL;
+    if (!g->nodes || (reinterpret_cast<uintptr_t>(g->nodes) & 127u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->ts_index) & 15u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->hist) & 7u) != 0) return TGL_EINVAL;
+    if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
+    if (!capacities(num_roots, hops, fanouts, num_snapshots, cap)) return TGL_EINVAL;
+    for (int h = 0; h < hops; h++) {
+        const tgl_hop_out &o = outs[h];
+        if (cap[h + 1] > 0 && (!o.nbr || !o.eid || !o.ts || !o.dt)) return TGL_EINVAL;
+        if (h > 0 && cap[h] > 0 && !o.parent) return TGL_EINVAL;
+    }
+    return TGL_OK;
+}
+
 }  // namespace
 }  // namespace tgl
 
@@ -1464,33 +1525,13 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
                          uint64_t root_base, const tgl_sample_opts *opts, const tgl_hop_out *outs,
                          int64_t *counts, void *workspace, size_t workspace_bytes, void *stream) {
     // ---- host-side argument checks (nothing is enqueued on failure) ----
-    if (!g || !outs || !counts) return TGL_EINVAL;
-    const int32_t anchor = opts ? opts->anchor : TGL_ANCHOR_OWN;
-    if (anchor != TGL_ANCHOR_OWN && anchor != TGL_ANCHOR_ROOT) return TGL_EINVAL;
-    uint32_t *const pointers = opts ? opts->pointers : nullptr;
-    if ((reinterpret_cast<uintptr_t>(pointers) & 3u) != 0) return TGL_EINVAL;
-    if (!sample_args_ok(num_roots, hops, fanouts, num_snapshots)) return TGL_EINVAL;
-    if (mode != TGL_MOST_RECENT && mode != TGL_UNIFORM) return TGL_EINVAL;
-    if (snapshot_len != snapshot_len || !(snapshot_len > 0.0f)) return TGL_EINVAL;
-    const bool dinf = __builtin_isinf(snapshot_len);
-    if (dinf && num_snapshots != 1) return TGL_EINVAL;
-    if (g->num_nodes < 1 || g->num_nodes > INT32_MAX) return TGL_EINVAL;
-    if (g->num_entries < 0 || g->num_entries > static_cast<int64_t>(UINT32_MAX)) return TGL_EINVAL;
-    if (!g->indptr || (g->num_entries > 0 && !g->entries)) return TGL_EINVAL;
-    if (g->num_entries > 0 && !g->ts) return TGL_EINVAL;
-    if (!g->nodes || (reinterpret_cast<uintptr_t>(g->nodes) & 127u) != 0) return TGL_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(g->entries) & 15u) != 0) return TGL_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(g->ts_index) & 15u) != 0) return TGL_EINVAL;
-    if ((reinterpret_cast<uintptr_t>(g->hist) & 7u) != 0) return TGL_EINVAL;
-    if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
     int64_t cap[TGL_MAX_HOPS + 1];
-    if (!capacities(num_roots, hops, fanouts, num_snapshots, cap)) return TGL_EINVAL;
-    for (int h = 0; h < hops; h++) {
-        const tgl_hop_out &o = outs[h];
-        if (cap[h + 1] > 0 && (!o.nbr || !o.eid || !o.ts || !o.dt)) return TGL_EINVAL;
-        if (h > 0 && cap[h] > 0 && !o.parent) return TGL_EINVAL;
-    }
+    const tgl_status chk = sample_check(g, roots, root_ts, num_roots, hops, fanouts, mode, num_snapshots,
+                                        snapshot_len, opts, outs, counts, cap);
+    if (chk != TGL_OK) return chk;
+    const int32_t anchor = opts ? opts->anchor : TGL_ANCHOR_OWN;
+    uint32_t *const pointers = opts ? opts->pointers : nullptr;
+    const bool dinf = __builtin_isinf(snapshot_len);
     const SampleWs need = carve_sample_ws(nullptr, hops, cap, num_snapshots);
     if (hops >= 2 && (!workspace || workspace_bytes < need.bytes)) return TGL_ENOSPACE;
     const SampleWs ws = carve_sample_ws(workspace, hops, cap, num_snapshots);
@@ -1606,6 +1647,21 @@ tgl_status tgl_sample(const tgl_tcsr *g, const int32_t *roots, const float *root
                       void *workspace, size_t workspace_bytes, void *stream) {
     return tgl_sample_ex(g, roots, root_ts, num_roots, hops, fanouts, mode, num_snapshots, snapshot_len, seed,
                          root_base, nullptr, outs, counts, workspace, workspace_bytes, stream);
+}
+
+tgl_status tgl_sample_noalloc(const tgl_tcsr *g, const int32_t *roots, const float *root_ts,
+                              int64_t num_roots, int32_t hops, const int32_t *fanouts, int32_t mode,
+                              int32_t num_snapshots, float snapshot_len, uint64_t seed,
+                              uint64_t root_base, const tgl_hop_out *outs, int64_t *counts, void *stream) {
+    int64_t cap[TGL_MAX_HOPS + 1];
+    const tgl_status chk = sample_check(g, roots, root_ts, num_roots, hops, fanouts, mode, num_snapshots,
+                                        snapshot_len, nullptr, outs, counts, cap);
+    if (chk != TGL_OK) return chk;
+    if (carve_sample_ws(nullptr, hops, cap, num_snapshots).bytes > TGL_NOALLOC_SCRATCH_BYTES) return TGL_ENOSPACE;
+    void *ws = nullptr;
+    if (scratch_ptr(&ws) != TGL_OK) return TGL_EDEVICE;
+    return tgl_sample_ex(g, roots, root_ts, num_roots, hops, fanouts, mode, num_snapshots, snapshot_len, seed,
+                         root_base, nullptr, outs, counts, ws, TGL_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"

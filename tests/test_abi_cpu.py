@@ -270,3 +270,23 @@ def test_mfg_argument_checks():
     assert call(ws_bytes=8) == B.ENOSPACE
     assert call(roots=None, rts=None, ws_bytes=8) == B.ENOSPACE   # no roots: accepted up to the workspace
     assert call(ws=None) == B.ENOSPACE
+
+
+def test_noalloc_argument_checks():
+    """tgl_sample_noalloc checks its arguments on the host like tgl_sample,
+    and refuses a call whose workspace would exceed its static area."""
+    L = P.lib()
+    g = B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE)
+    outs = (B.c_hop_out * 2)(B.c_hop_out(FAKE, FAKE, FAKE, FAKE, None), B.c_hop_out(FAKE, FAKE, FAKE, FAKE, FAKE))
+
+    def call(n=5, fan=(10, 10), hops=2, mode=1, S=1, delta=float("inf"), gg=g):
+        fa, fp = B._i32_array(fan)
+        return L.tgl_sample_noalloc(C.byref(gg) if gg is not None else None, FAKE, FAKE, n, hops, fp, mode, S,
+                                    C.c_float(delta), 0, 0, outs, FAKE, None)
+    assert call(fan=(0, 10)) == B.EINVAL
+    assert call(mode=7) == B.EINVAL
+    assert call(S=2) == B.EINVAL                     # several snapshots need a finite length
+    assert call(gg=None) == B.EINVAL
+    assert call(n=20000, fan=(1024, 1024)) == B.ENOSPACE
+    need = L.tgl_sample_workspace(20000, 2, B._i32_array((1024, 1024))[1], 1)
+    assert need > B.NOALLOC_SCRATCH_BYTES
