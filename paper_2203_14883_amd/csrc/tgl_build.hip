@@ -587,53 +587,75 @@ __global__ __launch_bounds__(kBlock) void first_hint_kernel(int4 *__restrict__ e
 // at or below its first timestamp, above its last, or inside the first
 // TGL_NODE_INLINE timestamps (held in the record); otherwise a binary search
 // of the rest of the run, which then holds an entry at or above t (the last
-// one).  A neighbour id outside [0, N) gets {0, 0}.
-__global__ __launch_bounds__(kBlock) void hist_kernel(const int4 *__restrict__ ent, const float *__restrict__ ts,
+// one).  A neighbour id outside [0, N) gets {0, 0}.  With set_hint, the
+// entry's TGL_NBR_FIRST bit is written from the span (hi == lo: no entry of
+// v below t) over a clear bit.  Wavefront-tiled like emit_kernel, so that
+// each lane's record loads for its kEmitPerLane entries are in flight
+// together.
+__global__ __launch_bounds__(kBlock) void hist_kernel(int4 *__restrict__ ent, const float *__restrict__ ts,
                                                       int64_t M, const int4 *__restrict__ nodes, int64_t N,
-                                                      uint2 *__restrict__ hist) {
-    const int2 *const head = reinterpret_cast<const int2 *>(ent);  // (nbr, ts) of each 16-byte entry
-    const int64_t gstride = static_cast<int64_t>(gridDim.x) * kBlock;
-    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += gstride) {
-        const int2 e = head[2 * p];
-        const uint32_t x = static_cast<uint32_t>(e.x) & TGL_NBR_MASK;
-        const float t = __int_as_float(e.y);
-        uint32_t lo = 0, hi = 0;
-        if (static_cast<int64_t>(x) < N) {
-            const int4 *const rec = nodes + static_cast<int64_t>(x) * 8;
-            const int4 h = rec[0];
-            const uint32_t um = static_cast<uint32_t>(M);
-            uint32_t a = static_cast<uint32_t>(h.x), b = static_cast<uint32_t>(h.y);
-            a = a > um ? um : a;
-            b = b < a ? a : (b > um ? um : b);
-            lo = a;
-            if (!(__int_as_float(h.z) < t)) {
-                hi = a;                                   // nothing below t (or t is NaN)
-            } else if (__int_as_float(h.w) < t) {
-                hi = b;                                   // the whole run
-            } else {
-                uint32_t c = 0;                           // inline timestamps below t (+inf past the run)
+                                                      uint2 *__restrict__ hist, bool set_hint) {
+    int2 *const head = reinterpret_cast<int2 *>(ent);        // (nbr, ts) of each 16-byte entry
+    const uint32_t um = static_cast<uint32_t>(M);
+    const int lane = lane_id();
+    const int64_t wave = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) / kWave;
+    const int64_t waves = static_cast<int64_t>(gridDim.x) * (kBlock / kWave);
+    for (int64_t base = wave * kEmitSpan; base < M; base += waves * kEmitSpan) {
+        int2 e[kEmitPerLane];
 #pragma unroll
-                for (int q = 1; q <= TGL_NODE_INLINE / 4; q++) {
-                    const int4 w = rec[q];
-                    c += (__int_as_float(w.x) < t) + (__int_as_float(w.y) < t) + (__int_as_float(w.z) < t) +
-                         (__int_as_float(w.w) < t);
-                }
-                if (c < TGL_NODE_INLINE || b - a <= TGL_NODE_INLINE) {
-                    hi = a + c;
-                } else {
-                    // the first position of [a + TGL_NODE_INLINE, b) with ts >= t;
-                    // ts[b - 1] (the last timestamp) is one
-                    uint32_t l = a + TGL_NODE_INLINE, r = b - 1;
-                    while (l < r) {
-                        const uint32_t m = l + (r - l) / 2;
-                        if (ts[m] < t) l = m + 1;
-                        else r = m;
-                    }
-                    hi = l;
-                }
-            }
+        for (int j = 0; j < kEmitPerLane; j++) {
+            const int64_t p = base + j * kWave + lane;
+            e[j] = head[2 * (p < M ? p : M - 1)];
         }
-        hist[p] = make_uint2(lo, hi);
+        int4 h[kEmitPerLane];
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++) {
+            const uint32_t x = static_cast<uint32_t>(e[j].x) & TGL_NBR_MASK;
+            h[j] = nodes[static_cast<int64_t>(static_cast<int64_t>(x) < N ? x : 0u) * 8];   // record 0 stands in
+        }
+#pragma unroll
+        for (int j = 0; j < kEmitPerLane; j++) {
+            const int64_t p = base + j * kWave + lane;
+            if (p >= M) continue;
+            const uint32_t x = static_cast<uint32_t>(e[j].x) & TGL_NBR_MASK;
+            const float t = __int_as_float(e[j].y);
+            uint32_t lo = 0, hi = 0;
+            if (static_cast<int64_t>(x) < N) {
+                uint32_t a = static_cast<uint32_t>(h[j].x), b = static_cast<uint32_t>(h[j].y);
+                a = a > um ? um : a;
+                b = b < a ? a : (b > um ? um : b);
+                lo = a;
+                if (!(__int_as_float(h[j].z) < t)) {
+                    hi = a;                               // nothing below t (or t is NaN)
+                } else if (__int_as_float(h[j].w) < t) {
+                    hi = b;                               // the whole run
+                } else {
+                    const int4 *const rec = nodes + static_cast<int64_t>(x) * 8;
+                    uint32_t c = 0;                       // inline timestamps below t (+inf past the run)
+#pragma unroll
+                    for (int q = 1; q <= TGL_NODE_INLINE / 4; q++) {
+                        const int4 w = rec[q];
+                        c += (__int_as_float(w.x) < t) + (__int_as_float(w.y) < t) + (__int_as_float(w.z) < t) +
+                             (__int_as_float(w.w) < t);
+                    }
+                    if (c < TGL_NODE_INLINE || b - a <= TGL_NODE_INLINE) {
+                        hi = a + c;
+                    } else {
+                        // the first position of [a + TGL_NODE_INLINE, b) with ts >= t;
+                        // ts[b - 1] (the last timestamp) is one
+                        uint32_t l = a + TGL_NODE_INLINE, r = b - 1;
+                        while (l < r) {
+                            const uint32_t m = l + (r - l) / 2;
+                            if (ts[m] < t) l = m + 1;
+                            else r = m;
+                        }
+                        hi = l;
+                    }
+                }
+                if (set_hint && hi == lo) head[2 * p].x = static_cast<int>(x | TGL_NBR_FIRST);
+            }
+            hist[p] = make_uint2(lo, hi);
+        }
     }
 }
 
@@ -831,8 +853,10 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     // set afterwards from the node records.
     // A packed timestamp field of at most 16 bits stands in for the float, so
     // that the neighbours' values are gathered from a smaller array.
+    // With neighbour histories the hints come from them instead (an empty
+    // history is the hint), and no first timestamps are needed.
     const int fbytes = L.packed && L.ts_bits <= 8 ? 1 : (L.packed && L.ts_bits <= 16 ? 2 : 4);
-    void *const first = num_nodes * fbytes <= 8 * M ? static_cast<void *>(w.keys[cur ^ 1]) : nullptr;
+    void *const first = !hist_out && num_nodes * fbytes <= 8 * M ? static_cast<void *>(w.keys[cur ^ 1]) : nullptr;
     const unsigned gm = grid_for(M), gn = grid_for(num_nodes);
     int4 *const ent = reinterpret_cast<int4 *>(entries);
     if (first && fbytes == 1) {
@@ -858,7 +882,7 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
     }
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts_out, num_nodes, M,
                                                              reinterpret_cast<int4 *>(nodes_out), nullptr);
-    if (!first)
+    if (!first && !hist_out)
         first_hint_kernel<<<grid_for(M), kBlock, 0, st>>>(reinterpret_cast<int4 *>(entries), ts_out, M,
                                                           reinterpret_cast<const float *>(nodes_out) + 2, 32,
                                                           num_nodes);
@@ -867,9 +891,9 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts_out, L, ts_index_out);
     }
     if (hist_out)
-        hist_kernel<<<grid_for(M), kBlock, 0, st>>>(reinterpret_cast<const int4 *>(entries), ts_out, M,
-                                                    reinterpret_cast<const int4 *>(nodes_out), num_nodes,
-                                                    reinterpret_cast<uint2 *>(hist_out));
+        hist_kernel<<<grid_for((M + kEmitPerLane - 1) / kEmitPerLane), kBlock, 0, st>>>(
+            reinterpret_cast<int4 *>(entries), ts_out, M, reinterpret_cast<const int4 *>(nodes_out), num_nodes,
+            reinterpret_cast<uint2 *>(hist_out), true);
     return launch_status();
 }
 
@@ -902,9 +926,9 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
         index_kernel<<<grid_for(L), kBlock, 0, st>>>(ts, L, ts_index);
     }
     if (hist && num_entries > 0)
-        hist_kernel<<<grid_for(num_entries), kBlock, 0, st>>>(reinterpret_cast<const int4 *>(entries), ts, num_entries,
-                                                              reinterpret_cast<const int4 *>(nodes), num_nodes,
-                                                              reinterpret_cast<uint2 *>(hist));
+        hist_kernel<<<grid_for((num_entries + kEmitPerLane - 1) / kEmitPerLane), kBlock, 0, st>>>(
+            reinterpret_cast<int4 *>(entries), ts, num_entries, reinterpret_cast<const int4 *>(nodes), num_nodes,
+            reinterpret_cast<uint2 *>(hist), false);
     return launch_status();
 }
 
