@@ -66,6 +66,11 @@ def parse():
                     help="hop 1 from saved window edges (Sec. 3.1 pointers), reset before warm-up; implies --consecutive")
     ap.add_argument("--chunk", type=int, default=None,
                     help="f1, f2: slots per launch (default 2^20 for f1, 2^23 for f2)")
+    ap.add_argument("--epoch", action="store_true",
+                    help="time every super-batch of the epoch in order (a full-epoch sweep; --steps is ignored)")
+    ap.add_argument("--cpu-threads", type=int, default=None,
+                    help="threads of the all-core oracle timing (default: the CPUs this process may use, "
+                         "at most OMP_NUM_THREADS)")
     return ap.parse_args()
 
 
@@ -104,10 +109,13 @@ def kernel_source_hash(files=("tgl_internal.hpp", "tgl_sample.hip")):
     return h.hexdigest()[:16]
 
 
-def read_traffic(kernel_hash, workload, prefix="hop_kernel"):
-    """HBM bytes per launch of the dominant kernel from the committed counter
-    summary, if it was taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", "%s_%s_pmc.md" % (prefix, workload))
+def read_profile(kernel_hash, workload, prefix="hop_kernel"):
+    """Figures of the committed counter summary of the dominant kernel
+    (``profiles/<prefix>_<workload>_pmc.md``), if it was taken on the current
+    kernel source: HBM bytes per launch and the launch duration measured in
+    those same counter runs.  None otherwise."""
+    name = "%s_%s_pmc.md" % (prefix, workload)
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     vals = {}
@@ -118,9 +126,38 @@ def read_traffic(kernel_hash, workload, prefix="hop_kernel"):
     if vals.get("kernel_source_hash") != kernel_hash:
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        out = {"bytes": float(vals["hbm_bytes_per_launch"]), "source": "profiles/" + name}
     except (KeyError, ValueError):
         return None
+    for key, conv in (("avg_duration_us_under_counters", float), ("slots_per_launch", float)):
+        try:
+            out[key] = conv(vals[key])
+        except (KeyError, ValueError):
+            pass
+    return out
+
+
+def read_traffic(kernel_hash, workload, prefix="hop_kernel"):
+    """HBM bytes per launch of a kernel from its committed counter summary
+    (None unless taken on the current kernel source)."""
+    prof = read_profile(kernel_hash, workload, prefix)
+    return prof["bytes"] if prof else None
+
+
+def traffic_fields(prof):
+    """The byte counters' view of the dominant kernel, all from the counter
+    runs themselves (bytes and duration of the same dispatches), never mixed
+    with this run's timing."""
+    if not prof:
+        return {"traffic": None}
+    f = {"traffic": prof["bytes"], "traffic_source": prof["source"]}
+    us = prof.get("avg_duration_us_under_counters")
+    if us:
+        f["traffic_gbs_in_counter_run"] = prof["bytes"] / (us * 1e-6) / 1e9
+        f["traffic_frac_in_counter_run"] = f["traffic_gbs_in_counter_run"] / PEAK_HBM_GBS
+    if prof.get("slots_per_launch"):
+        f["traffic_bytes_per_slot"] = prof["bytes"] / prof["slots_per_launch"]
+    return f
 
 
 def make_workload(name, small):
@@ -151,12 +188,32 @@ def cpu_model():
     return "unknown CPU"
 
 
-def cpu_baseline(w, nbatches):
-    """The oracle, single-threaded, on a bounded sample: the roots of
-    ``nbatches`` consecutive batches from the middle of the epoch (eight GPU
-    steps at the default size), over an oracle T-CSR that holds the full runs
-    of every node the sample reaches.  Only the oracle's sampling call is
-    timed."""
+def cpu_threads(requested=None):
+    """Threads for the all-core oracle timing: the CPUs this process may run
+    on, at most OMP_NUM_THREADS when that is set."""
+    if requested:
+        return requested
+    try:
+        n = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        n = os.cpu_count() or 1
+    cap = os.environ.get("OMP_NUM_THREADS")
+    if cap and cap.isdigit() and int(cap) > 0:
+        n = min(n, int(cap))
+    return max(1, n)
+
+
+def cpu_baseline(w, nbatches, threads):
+    """The oracle as it stands (single-threaded C), on a bounded sample: the
+    roots of ``nbatches`` consecutive batches from the middle of the epoch,
+    over an oracle T-CSR that holds the full runs of every node the sample
+    reaches.  Timed twice on the same roots: one call on one core, then the
+    sample split by batches over ``threads`` host threads, each calling the
+    unchanged oracle on its own batch range with its own root_base (the
+    sampler's output does not depend on how roots are batched; the ctypes
+    call releases the interpreter lock).  Only sampling calls are timed."""
+    from concurrent.futures import ThreadPoolExecutor
+
     import oracle
     from oracle import subgraph
     nbatches = min(nbatches, w.num_batches())
@@ -168,17 +225,47 @@ def cpu_baseline(w, nbatches):
                             w.mode, w.snapshots, w.snapshot_len, w.sample_seed, base)
     build_s = time.perf_counter() - t
     log("CPU oracle: sub-graph of %d entries built in %.1f s" % (len(g.nbr), build_s))
+
+    def valid(out):
+        return int(sum(int((h.nbr >= 0).sum()) for h in out))
+
     t = time.perf_counter()
     out = oracle.sample(g, roots, rts, w.fanouts, w.mode, w.snapshots, w.snapshot_len,
                         w.sample_seed, base)
-    dt = time.perf_counter() - t
-    nbrs = int(sum(int((h.nbr >= 0).sum()) for h in out))
-    return dict(value=nbrs / dt, unit="neighbours/s", cores=1, kind="oracle",
-                sample="%d roots (%d consecutive batches from batch %d) of %s, %d hops, %d neighbours, "
-                       "%.2f s single-threaded on %s (sampling call only; T-CSR of the reached sub-graph, "
-                       "%d entries, built beforehand in %.1f s)"
-                       % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, dt, cpu_model(),
-                          len(g.nbr), build_s))
+    dt1 = time.perf_counter() - t
+    nbrs = valid(out)
+    del out
+    log("CPU oracle, 1 thread: %d neighbours in %.2f s" % (nbrs, dt1))
+
+    # batch ranges per thread (at least one batch each)
+    nt = max(1, min(threads, nbatches))
+    edges = [round(i * nbatches / nt) for i in range(nt + 1)]
+    per_batch = len(roots) // nbatches if nbatches else 0
+    ranges = [(edges[i] * per_batch, edges[i + 1] * per_batch) for i in range(nt)]
+    ranges[-1] = (ranges[-1][0], len(roots))
+
+    def work(rg):
+        r0, r1 = rg
+        return valid(oracle.sample(g, roots[r0:r1], rts[r0:r1], w.fanouts, w.mode, w.snapshots,
+                                   w.snapshot_len, w.sample_seed, base + r0))
+
+    t = time.perf_counter()
+    with ThreadPoolExecutor(nt) as ex:
+        counts = list(ex.map(work, ranges))
+    dtn = time.perf_counter() - t
+    if sum(counts) != nbrs:
+        raise SystemExit("CPU oracle: %d threads found %d neighbours, one thread %d" % (nt, sum(counts), nbrs))
+    log("CPU oracle, %d threads: %.2f s" % (nt, dtn))
+    model = cpu_model()
+    what = ("%d roots (%d consecutive batches from batch %d) of %s, %d hops, %d neighbours; T-CSR of the reached "
+            "sub-graph (%d entries) built beforehand in %.1f s; sampling calls only; %s, %d logical CPUs on the host"
+            % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, len(g.nbr), build_s, model,
+               os.cpu_count() or 0))
+    return dict(value=nbrs / dtn, unit="neighbours/s", cores=nt, kind="oracle",
+                sample="%s; %d threads, each the unchanged single-threaded oracle on its own batch range: %.2f s"
+                       % (what, nt, dtn),
+                cpu_model=model, host_logical_cpus=os.cpu_count(),
+                single_core=dict(value=nbrs / dt1, unit="neighbours/s", cores=1, seconds=dt1))
 
 
 GATHER_DIM = 768             # MAG node features (Table 3), bfloat16
@@ -614,23 +701,32 @@ def main():
 
     ws = torch.empty(P.tcsr_build_workspace(w.num_edges, w.num_nodes, w.undirected),
                      dtype=torch.uint8, device=dev)
+    # neighbour histories serve the hops >= 2 of a sampler with one window
+    # unbounded below; other samplers never read them
+    hist = len(w.fanouts) > 1 and w.snapshots == 1 and math.isinf(w.snapshot_len)
     P.timer_enable(1 << 14)
-    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws)  # warm-up
+    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist)  # warm-up
     del g
     torch.cuda.synchronize()
     P.timer_reset()
     t = time.perf_counter()
-    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws)
+    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist)
     torch.cuda.synchronize()
     build_wall = time.perf_counter() - t
     build_ms, _ = P.timer_read(P.binding.TIMER_BUILD)
     del ws, d_src, d_dst, d_ts, d_eid
     torch.cuda.empty_cache()
-    log("T-CSR built: %d entries, %.1f ms (events), %.1f ms wall" % (g.num_entries, build_ms, build_wall * 1e3))
+    log("T-CSR built: %d entries%s, %.1f ms (events), %.1f ms wall"
+        % (g.num_entries, " with neighbour histories" if hist else "", build_ms, build_wall * 1e3))
 
     B = args.batches_per_step or {"c2": w.num_batches(), "c3": 64, "c4": 64, "c5": 1}[args.workload]
     B = min(B, w.num_batches())
-    if args.consecutive or args.pointers:
+    if args.epoch:
+        # every super-batch of the epoch, in order; warm-up on the first ones
+        timed_pos = list(range(0, w.num_batches(), B))
+        warm_pos = timed_pos[:args.warmup]
+        args.steps = len(timed_pos)
+    elif args.consecutive or args.pointers:
         # consecutive super-batches in chronological order, warm-up steps right before them
         nsteps = args.warmup + args.steps
         b0 = max(0, min(w.num_batches() // 2 - (nsteps * B) // 2, w.num_batches() - nsteps * B))
@@ -645,7 +741,7 @@ def main():
         warm_pos = [(p + max(span // (2 * max(args.steps, 1)), 1)) % span for p in timed_pos[:args.warmup]]
     inputs = {}
     for b in sorted(set(timed_pos + warm_pos)):
-        r, t_, base = w.batches(b, b + B)
+        r, t_, base = w.batches(b, min(b + B, w.num_batches()))
         inputs[b] = (torch.from_numpy(r).to(dev), torch.from_numpy(t_).to(dev), base, len(r))
     max_roots = max(v[3] for v in inputs.values())
     smp = P.Sampler(max_roots, w.fanouts, w.snapshots, device=dev)
@@ -687,17 +783,29 @@ def main():
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
     dom_ms, dom_n = P.timer_read(dominant)
-    hopn_ms, hopn_n = (dom_ms, dom_n) if dominant == P.binding.TIMER_HOPN else (0.0, 0)
     P.timer_select()
     P.timer_reset()
 
     # untimed pass over the same steps: valid slots (neighbours), the
-    # algorithmic bytes of the hop >= 2 kernel, and the other kernels' times
+    # algorithmic bytes of the dominant kernel (every hop >= 2; hop 1 of a
+    # one-hop sampler), and the other kernels' times
     indptr = g.indptr
     nbrs_total = 0
     slots_total = 0
-    hopn_bytes = 0.0
-    hopn_slots = 0
+    dom_bytes = 0.0
+    dom_slots = 0
+    dom_roots = 0
+    bounds_h1 = 1 if math.isinf(w.snapshot_len) else w.snapshots + 1
+    bounds_hn = 1 if math.isinf(w.snapshot_len) else 2
+
+    def search_bytes(x, nb):
+        """4 bytes per probe of a binary search over each root's run, nb
+        window edges per root (nodes outside the graph search nothing)."""
+        ok = (x >= 0) & (x < w.num_nodes)
+        xs = x[ok]
+        deg = (indptr[xs + 1] - indptr[xs]).double()
+        return float((torch.ceil(torch.log2(deg + 1.0)) * 4.0 * nb).sum())
+
     for b in timed_pos:
         run(b)
         hs = smp.hops()
@@ -707,14 +815,21 @@ def main():
             nbrs_total += nv
             slots_total += hop.nbr.numel()
             if h >= 1:
-                hopn_slots += hop.nbr.numel()
+                dom_slots += hop.nbr.numel()
+                dom_roots += hop.num_roots
                 roots2 = hs[h - 1].nbr[hs[h - 1].nbr >= 0].long()
-                deg = (indptr[roots2 + 1] - indptr[roots2]).double()
-                bounds = 1 if math.isinf(w.snapshot_len) else 2
-                search = float((torch.ceil(torch.log2(deg + 1.0)) * 4.0 * bounds).sum())
                 # per root: node + time read, run bounds read, parent index written;
                 # per slot: 16-byte entry read when valid, 20 bytes written
-                hopn_bytes += (hop.num_roots * (8 + 16 + 8) + search + nv * 16 + hop.nbr.numel() * 20)
+                dom_bytes += (hop.num_roots * (8 + 16 + 8) + search_bytes(roots2, bounds_hn) + nv * 16
+                              + hop.nbr.numel() * 20)
+            elif dominant == P.binding.TIMER_HOP1:
+                r, _, _, n = inputs[b]
+                dom_slots += hop.nbr.numel()
+                dom_roots += n
+                # per root: node + time read, run bounds read; S + 1 window
+                # edges searched (one when windows are unbounded below); per
+                # slot as above
+                dom_bytes += n * (8 + 16) + search_bytes(r[:n].long(), bounds_h1) + nv * 16 + hop.nbr.numel() * 20
     hop1_ms, hop1_n = P.timer_read(P.binding.TIMER_HOP1)
     comp_ms, comp_n = P.timer_read(P.binding.TIMER_COMPACT)
     if dominant == P.binding.TIMER_HOP1:
@@ -722,21 +837,28 @@ def main():
     log("timed %d steps: %.2f ms total (timed region: %s %.2f ms; recount pass: hop1 %.2f, compaction %.2f ms)"
         % (args.steps, total_ms, "hopN" if dominant == P.binding.TIMER_HOPN else "hop1", dom_ms,
            hop1_ms, comp_ms))
-    hopn_bytes_per_launch = hopn_bytes / max(len(timed_pos), 1)
-    hopn_slots_per_launch = hopn_slots / max(len(timed_pos), 1)
-    avg_hopn_ms = hopn_ms / max(hopn_n, 1)
-    achieved = hopn_bytes_per_launch / (avg_hopn_ms * 1e-3) / 1e9 if avg_hopn_ms > 0 else 0.0
+    dom_bytes_per_launch = dom_bytes / max(dom_n, 1)
+    dom_slots_per_launch = dom_slots / max(dom_n, 1)
+    avg_dom_ms = dom_ms / max(dom_n, 1)
+    achieved = dom_bytes_per_launch / (avg_dom_ms * 1e-3) / 1e9 if avg_dom_ms > 0 else 0.0
     value = nbrs_total / (total_ms * 1e-3)
     khash = kernel_source_hash()
-    traffic = read_traffic(khash, args.workload) if not args.small else None
-    log("neighbours %d over %d slots; %.3g neighbours/s; hopN %.1f GB/s algorithmic"
-        % (nbrs_total, slots_total, value, achieved))
+    prof = read_profile(khash, args.workload) if not (args.small or args.epoch) else None
+    if len(w.fanouts) > 1:
+        kernel = "hop_single_kernel (hops >= 2)"
+    elif w.snapshots > 1:
+        kernel = "hop_multi_kernel (hop 1)" if w.snapshots <= 8 else "hop_multi_wide_kernel (hop 1)"
+    else:
+        kernel = "hop_single_kernel (hop 1)"
+    log("neighbours %d over %d slots; %.3g neighbours/s; %s %.1f GB/s algorithmic"
+        % (nbrs_total, slots_total, value, kernel, achieved))
 
     cpu = None
     if not args.no_cpu_baseline:
         log("CPU oracle baseline")
-        cpu = cpu_baseline(w, args.cpu_batches or 8 * B)
-        log("CPU oracle: %.3g neighbours/s (%s)" % (cpu["value"], cpu["sample"]))
+        cpu = cpu_baseline(w, args.cpu_batches or min(8 * B, 512), cpu_threads(args.cpu_threads))
+        log("CPU oracle: %.3g neighbours/s on %d threads, %.3g on one (%s)"
+            % (cpu["value"], cpu["cores"], cpu["single_core"]["value"], cpu["sample"]))
 
     line = {
         "metric": METRIC,
@@ -752,37 +874,39 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": "%s%s: %d nodes, %d edges, undirected T-CSR of %d entries; %d-hop %s %s, %d snapshot(s)%s; %d batches of %d edges x 3 roots per step"
+            "workload": "%s%s: %d nodes, %d edges, undirected T-CSR of %d entries; %d-hop %s %s, %d snapshot(s)%s; %d batches of %d edges x 3 roots per step%s"
                         % (w.name, " (reduced)" if args.small else "", w.num_nodes, w.num_edges,
                            g.num_entries, len(w.fanouts), w.mode, "x".join(map(str, w.fanouts)),
                            w.snapshots, "" if math.isinf(w.snapshot_len) else " of %g" % w.snapshot_len,
-                           B, w.batch_edges),
+                           B, w.batch_edges,
+                           "; full epoch (%d batches)" % w.num_batches() if args.epoch else ""),
             "roots_per_step": max_roots,
-            "step_order": "consecutive" if (args.consecutive or args.pointers) else "spread over the epoch",
+            "step_order": ("the whole epoch in order" if args.epoch else
+                           "consecutive" if (args.consecutive or args.pointers) else "spread over the epoch"),
             "hop1_pointers": bool(args.pointers),
             "neighbours_per_step": nbrs_total / args.steps,
             "slots_per_step": slots_total / args.steps,
             "tcsr_build_ms": build_ms,
-            "kernel_ms_per_step": {"hop1": hop1_ms / args.steps, "hopN": hopn_ms / args.steps,
+            "tcsr_neighbour_histories": bool(hist),
+            "kernel_ms_per_step": {"hop1": hop1_ms / args.steps, "hopN": (dom_ms if dominant == P.binding.TIMER_HOPN
+                                                                          else 0.0) / args.steps,
                                    "compaction": comp_ms / args.steps,
                                    "timed_in_region": "hopN" if dominant == P.binding.TIMER_HOPN else "hop1"},
         },
         "roofline": {
-            "kernel": "hop_single_kernel (hops >= 2)",
+            "kernel": kernel,
             "bound": "hbm",
             "achieved": achieved,
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": achieved / PEAK_HBM_GBS,
-            "traffic": traffic,
-            # DRAM-level view of the same launches: counted bytes / kernel time, and both
-            # byte counts per output slot (traffic / algorithmic = the overfetch ratio)
-            "traffic_gbs": traffic / (avg_hopn_ms * 1e-3) / 1e9 if traffic and avg_hopn_ms > 0 else None,
-            "traffic_frac": traffic / (avg_hopn_ms * 1e-3) / 1e9 / PEAK_HBM_GBS if traffic and avg_hopn_ms > 0 else None,
-            "traffic_bytes_per_slot": traffic / hopn_slots_per_launch if traffic and hopn_slots_per_launch else None,
-            "algorithmic_bytes_per_slot": hopn_bytes_per_launch / hopn_slots_per_launch if hopn_slots_per_launch else None,
-            "algorithmic_bytes_per_launch": hopn_bytes_per_launch,
-            "avg_launch_ms": avg_hopn_ms,
+            **traffic_fields(prof),
+            "algorithmic_bytes_per_slot": dom_bytes_per_launch / dom_slots_per_launch if dom_slots_per_launch else None,
+            "algorithmic_bytes_per_launch": dom_bytes_per_launch,
+            "roots_per_launch": dom_roots / max(dom_n, 1),
+            "slots_per_launch": dom_slots_per_launch,
+            "avg_launch_ms": avg_dom_ms,
+            "launches": dom_n,
             "kernel_source_hash": khash,
         },
         "cpu_baseline": cpu,
