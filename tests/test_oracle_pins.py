@@ -366,3 +366,31 @@ def test_deep_hops_and_wide_fanouts_match_brute_force():
         deep += len(fan) >= 5 and int((got[-1].nbr >= 0).sum()) > 0
         wide += fan[0] > 70 and int((got[0].nbr >= 0).sum()) > 70
     assert deep >= 8 and wide >= 8, (deep, wide)
+
+
+def test_history_definition_matches_brute_force():
+    """The test-side definition of an entry's neighbour history (used to check
+    the GPU's histories at every size) against a loop over the neighbour's run:
+    [start of the neighbour's run, start + #{its timestamps below the entry's}),
+    (0, 0) for a neighbour outside the node range; timestamps with ties, signed
+    zeros folded, infinities and denormals."""
+    from gpu_util import hist_of
+    rng = np.random.default_rng(17)
+    vals = np.array([-np.inf, -2.5, -1e-40, 0.0, 1e-40, 3.0, 3.5, 7.0, np.inf], np.float32)
+    for trial in range(300):
+        n = int(rng.integers(1, 9))
+        m = int(rng.integers(0, 50))
+        owner = rng.integers(0, n, m)
+        ts = rng.choice(vals, m)
+        order = np.lexsort((ts, owner))
+        owner, ts = owner[order], ts[order]
+        ip = np.concatenate([[0], np.cumsum(np.bincount(owner, minlength=n))])
+        nbr = rng.integers(-2, n + 2, m)
+        lo, hi = hist_of(ip, nbr, ts)
+        for p in range(m):
+            v = int(nbr[p])
+            if 0 <= v < n:
+                run = ts[ip[v]:ip[v + 1]]
+                assert (lo[p], hi[p]) == (ip[v], ip[v] + int((run < ts[p]).sum())), (trial, p)
+            else:
+                assert (lo[p], hi[p]) == (0, 0), (trial, p)
