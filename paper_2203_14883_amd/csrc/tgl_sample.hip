@@ -598,28 +598,6 @@ __device__ __forceinline__ void gather_records(const int4 *__restrict__ ent, uin
     for (int u = 0; u < U; u++) rec[u] = ent[pick[u] != UINT32_MAX ? pick[u] : 0u];
 }
 
-// gather_records plus each pick's neighbour history, all loads in flight
-// together (a lane without a pick reads entry 0).
-template <int U>
-__device__ __forceinline__ void gather_records_hist(const int4 *__restrict__ ent, const uint2 *__restrict__ hist,
-                                                    uint32_t M, const uint32_t (&pick)[U], int4 (&rec)[U],
-                                                    uint2 (&hv)[U]) {
-    if (M == 0) {
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            rec[u] = make_int4(-1, -1, -1, -1);
-            hv[u] = make_uint2(0u, 0u);
-        }
-        return;
-    }
-#pragma unroll
-    for (int u = 0; u < U; u++) {
-        const uint32_t q = pick[u] != UINT32_MAX ? pick[u] : 0u;
-        rec[u] = ent[q];
-        hv[u] = hist[q];
-    }
-}
-
 __device__ __forceinline__ void wave_sync_lds() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
@@ -1229,12 +1207,18 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !
             }
             int4 rec[U];
             if constexpr (WIN && !LAST) {
+                // the histories are loaded once the entries are in: a pick whose
+                // entry carries the neighbour-first hint has an empty history,
+                // and reads entry 0's (one cached line) instead of its own
+                gather_records<U>(p.ent, static_cast<uint32_t>(p.num_entries), pick, rec);
                 uint2 hv[U];
-                gather_records_hist<U>(p.ent, p.hist, static_cast<uint32_t>(p.num_entries), pick, rec, hv);
+#pragma unroll
+                for (int u = 0; u < U; u++)
+                    hv[u] = p.hist[pick[u] != UINT32_MAX && rec[u].x >= 0 ? pick[u] : 0u];
 #pragma unroll
                 for (int u = 0; u < U; u++) {
                     const int e = e0 + u * kWave + lane;
-                    if (e < total && pick[u] != UINT32_MAX) orow.win[e] = hv[u];
+                    if (e < total && pick[u] != UINT32_MAX) orow.win[e] = rec[u].x >= 0 ? hv[u] : make_uint2(0u, 0u);
                 }
             } else {
                 gather_records<U>(p.ent, static_cast<uint32_t>(p.num_entries), pick, rec);
