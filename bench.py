@@ -208,10 +208,11 @@ def cpu_baseline(w, nbatches, threads):
     roots of ``nbatches`` consecutive batches from the middle of the epoch,
     over an oracle T-CSR that holds the full runs of every node the sample
     reaches.  Timed twice on the same roots: one call on one core, then the
-    sample split by batches over ``threads`` host threads, each calling the
-    unchanged oracle on its own batch range with its own root_base (the
-    sampler's output does not depend on how roots are batched; the ctypes
-    call releases the interpreter lock).  Only sampling calls are timed."""
+    sample split into ``threads`` contiguous root ranges, one host thread
+    each calling the unchanged oracle on its range with its own root_base
+    (the sampler's output does not depend on how roots are batched; the
+    ctypes call releases the interpreter lock).  Only sampling calls are
+    timed."""
     from concurrent.futures import ThreadPoolExecutor
 
     import oracle
@@ -237,12 +238,10 @@ def cpu_baseline(w, nbatches, threads):
     del out
     log("CPU oracle, 1 thread: %d neighbours in %.2f s" % (nbrs, dt1))
 
-    # batch ranges per thread (at least one batch each)
-    nt = max(1, min(threads, nbatches))
-    edges = [round(i * nbatches / nt) for i in range(nt + 1)]
-    per_batch = len(roots) // nbatches if nbatches else 0
-    ranges = [(edges[i] * per_batch, edges[i + 1] * per_batch) for i in range(nt)]
-    ranges[-1] = (ranges[-1][0], len(roots))
+    # one contiguous range of roots per thread
+    nt = max(1, min(threads, len(roots)))
+    edges = [round(i * len(roots) / nt) for i in range(nt + 1)]
+    ranges = [(edges[i], edges[i + 1]) for i in range(nt)]
 
     def work(rg):
         r0, r1 = rg
@@ -262,7 +261,7 @@ def cpu_baseline(w, nbatches, threads):
             % (len(roots), nbatches, b0, w.name, len(w.fanouts), nbrs, len(g.nbr), build_s, model,
                os.cpu_count() or 0))
     return dict(value=nbrs / dtn, unit="neighbours/s", cores=nt, kind="oracle",
-                sample="%s; %d threads, each the unchanged single-threaded oracle on its own batch range: %.2f s"
+                sample="%s; %d threads, each the unchanged single-threaded oracle on its own range of roots: %.2f s"
                        % (what, nt, dtn),
                 cpu_model=model, host_logical_cpus=os.cpu_count(),
                 single_core=dict(value=nbrs / dt1, unit="neighbours/s", cores=1, seconds=dt1))
@@ -702,8 +701,11 @@ def main():
     ws = torch.empty(P.tcsr_build_workspace(w.num_edges, w.num_nodes, w.undirected),
                      dtype=torch.uint8, device=dev)
     # neighbour histories serve the hops >= 2 of a sampler with one window
-    # unbounded below; other samplers never read them
-    hist = len(w.fanouts) > 1 and w.snapshots == 1 and math.isinf(w.snapshot_len)
+    # unbounded below; other samplers never read them, and the rows after the
+    # sampler (f1, f2, f4) only need its slots (f1's feature table needs the
+    # memory)
+    hist = (args.row == "sample" and len(w.fanouts) > 1 and w.snapshots == 1
+            and math.isinf(w.snapshot_len))
     P.timer_enable(1 << 14)
     g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist)  # warm-up
     del g
