@@ -71,6 +71,8 @@ def parse():
     ap.add_argument("--cpu-threads", type=int, default=None,
                     help="threads of the all-core oracle timing (default: the CPUs this process may use, "
                          "at most OMP_NUM_THREADS)")
+    ap.add_argument("--no-dir", action="store_true",
+                    help="build the T-CSR without its time directories (window searches use the index alone)")
     return ap.parse_args()
 
 
@@ -98,7 +100,7 @@ def strip_comments(src):
     return "\n".join(l.rstrip() for l in "".join(out).splitlines() if l.strip())
 
 
-def kernel_source_hash(files=("tgl_internal.hpp", "tgl_sample.hip")):
+def kernel_source_hash(files=("tgl_internal.hpp", "tgl_cells.hpp", "tgl_sample.hip")):
     """Hash of the code (comments left out) of the sources that define the
     measured kernels, to tell whether committed counters still apply."""
     h = hashlib.sha256()
@@ -706,13 +708,16 @@ def main():
     # memory)
     hist = (args.row == "sample" and len(w.fanouts) > 1 and w.snapshots == 1
             and math.isinf(w.snapshot_len))
+    # time directories serve the window searches of long runs
+    tdir = args.row == "sample" and not args.no_dir
     P.timer_enable(1 << 14)
-    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist)  # warm-up
+    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist,
+                     dir=tdir)  # warm-up
     del g
     torch.cuda.synchronize()
     P.timer_reset()
     t = time.perf_counter()
-    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist)
+    g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist, dir=tdir)
     torch.cuda.synchronize()
     build_wall = time.perf_counter() - t
     build_ms, _ = P.timer_read(P.binding.TIMER_BUILD)
@@ -890,6 +895,7 @@ def main():
             "slots_per_step": slots_total / args.steps,
             "tcsr_build_ms": build_ms,
             "tcsr_neighbour_histories": bool(hist),
+            "tcsr_time_directory": bool(tdir),
             "kernel_ms_per_step": {"hop1": hop1_ms / args.steps, "hopN": (dom_ms if dominant == P.binding.TIMER_HOPN
                                                                           else 0.0) / args.steps,
                                    "compaction": comp_ms / args.steps,

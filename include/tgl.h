@@ -111,6 +111,29 @@ typedef struct tgl_span {
 } tgl_span;
 
 /*
+ * One cell of a run's time directory.  Section 3.1 finds a window edge by a
+ * binary search of the node's time-sorted run; the directory replaces most
+ * of that search by one lookup.  The run [a, b) of a node (first and last
+ * timestamps f, l) owns the search-index slots j with j * TGL_INDEX_STRIDE
+ * in [a, b): K = ceil(b / S) - ceil(a / S) of them (S = TGL_INDEX_STRIDE),
+ * and slot ceil(a / S) + k holds its cell k.  The cells split [f, l] evenly:
+ * with sc = K / (l - f) when l - f is positive and finite (sc = 0 otherwise),
+ *   cell(t) = 0 if t <= f;  K - 1 if t >= l;
+ *             min(K - 1, floor((t - f) * sc)) otherwise,
+ * every operation a float32 one rounded to nearest.  cell is non-decreasing
+ * in t, so each cell's entries are one stretch of the run, and cell k holds
+ *   pos = a + #{entries of the run whose timestamp's cell is below k}
+ *   ts  = the timestamp of entry pos (+inf if pos = b).
+ * For a threshold v with cell(v) = k, the count of the run's timestamps
+ * below v lies between pos and the next cell's pos (b after the last cell),
+ * and equals pos when v <= ts.
+ */
+typedef struct tgl_cell {
+    uint32_t pos;
+    float ts;
+} tgl_cell;
+
+/*
  * Non-owning view of a T-CSR (Section 3.1): node x owns entries
  * [indptr[x], indptr[x+1]) of `entries`, sorted by ts ascending (ties in any
  * fixed order; tgl_tcsr_build uses input order).  Timestamps must not be NaN.
@@ -134,6 +157,12 @@ typedef struct tgl_span {
  *                     Read by calls with one snapshot of infinite length and
  *                     more than one hop; results are the same with or
  *                     without it.
+ *   dir      [device] tgl_cell[tgl_index_len(num_entries)], 8-byte aligned,
+ *                     or NULL: the time directory of every run (see
+ *                     tgl_cell), written by tgl_tcsr_build or tgl_tcsr_nodes
+ *                     from the same arrays.  The window search of a run
+ *                     longer than a few cache lines starts from it; results
+ *                     are the same with or without it.
  * num_entries must be at most 2^32 - 1.  The sampler clamps every indptr
  * value into [0, num_entries], so a malformed view yields wrong samples but
  * never an out-of-bounds access.
@@ -147,6 +176,7 @@ typedef struct tgl_tcsr {
     const tgl_node *nodes;
     const float *ts_index;
     const tgl_span *hist;
+    const tgl_cell *dir;
 } tgl_tcsr;
 
 /*
@@ -203,6 +233,8 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
  *                                             NULL (no search index)
  *   hist_out   [device] tgl_span[M]           output, 8-byte aligned, or NULL
  *                                             (no neighbour histories)
+ *   dir_out    [device] tgl_cell[tgl_index_len(M)] output, 8-byte aligned,
+ *                                             or NULL (no time directory)
  *   workspace  [device] at least tgl_tcsr_build_workspace(...) bytes
  * Entry i < num_edges is (owner src[i], nbr dst[i], ts[i], eid[i]); with
  * TGL_BUILD_UNDIRECTED entry num_edges + i is the reversed edge (owner
@@ -214,8 +246,8 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          tgl_node *nodes_out, float *ts_index_out, tgl_span *hist_out, void *workspace,
-                          size_t workspace_bytes, void *stream);
+                          tgl_node *nodes_out, float *ts_index_out, tgl_span *hist_out,
+                          tgl_cell *dir_out, void *workspace, size_t workspace_bytes, void *stream);
 
 /* Length of the search index of a T-CSR with num_entries entries:
  * ceil(num_entries / TGL_INDEX_STRIDE), or -1 if num_entries is negative. */
@@ -223,9 +255,10 @@ int64_t tgl_index_len(int64_t num_entries);
 
 /*
  * Writes the per-node summaries, the search index (if ts_index is not NULL),
- * the TGL_NBR_FIRST hints (if entries is not NULL) and the neighbour
- * histories (if hist is not NULL) of a T-CSR given by its indptr, timestamp
- * and entry arrays (for a T-CSR built elsewhere and uploaded).
+ * the TGL_NBR_FIRST hints (if entries is not NULL), the neighbour histories
+ * (if hist is not NULL) and the time directory (if dir is not NULL) of a
+ * T-CSR given by its indptr, timestamp and entry arrays (for a T-CSR built
+ * elsewhere and uploaded).
  *   indptr     [device] int64[num_nodes + 1]
  *   ts         [device] float[num_entries]
  *   num_nodes  in [1, 2^31 - 1];  num_entries in [0, 2^32 - 1]
@@ -239,11 +272,13 @@ int64_t tgl_index_len(int64_t num_entries);
  *              are left alone
  *   hist       [device] tgl_span[num_entries], 8-byte aligned, output, or
  *              NULL; requires entries
+ *   dir        [device] tgl_cell[tgl_index_len(num_entries)], 8-byte
+ *              aligned, output, or NULL
  * indptr values are clamped into [0, num_entries].  Never synchronises.
  */
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
                           int64_t num_entries, tgl_node *nodes, float *ts_index,
-                          tgl_entry *entries, tgl_span *hist, void *stream);
+                          tgl_entry *entries, tgl_span *hist, tgl_cell *dir, void *stream);
 
 /* ------------------------------------------------------------------------ */
 /* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */

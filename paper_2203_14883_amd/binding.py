@@ -55,7 +55,8 @@ class TglError(RuntimeError):
 class c_tcsr(C.Structure):
     _fields_ = [("num_nodes", C.c_int64), ("num_entries", C.c_int64),
                 ("indptr", C.c_void_p), ("entries", C.c_void_p), ("ts", C.c_void_p),
-                ("nodes", C.c_void_p), ("ts_index", C.c_void_p), ("hist", C.c_void_p)]
+                ("nodes", C.c_void_p), ("ts_index", C.c_void_p), ("hist", C.c_void_p),
+                ("dir", C.c_void_p)]
 
 
 class c_table(C.Structure):
@@ -101,11 +102,11 @@ def lib() -> C.CDLL:
     L.tgl_tcsr_build_workspace.restype = C.c_size_t
     L.tgl_tcsr_build_workspace.argtypes = [i64, i64, u32]
     L.tgl_tcsr_build.restype = i32
-    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, P, P, C.c_size_t, P]
+    L.tgl_tcsr_build.argtypes = [P, P, P, P, i64, i64, u32, P, P, P, P, P, P, P, P, C.c_size_t, P]
     L.tgl_index_len.restype = i64
     L.tgl_index_len.argtypes = [i64]
     L.tgl_tcsr_nodes.restype = i32
-    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P, P, P]
+    L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P, P, P, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -181,7 +182,9 @@ class TCSR:
     ts, then float32 ts of the run's first 28 entries, +inf beyond);
     ts_index float32[ceil(M / 32)], every 32nd timestamp (the search index), or
     None; hist int32[M, 2], per entry the positions [lo, hi) of the neighbour's
-    entries older than it (the neighbour's history), or None."""
+    entries older than it (the neighbour's history), or None; dir int32[ceil(M /
+    32), 2], the runs' time directories (per search-index slot, a cell's first
+    position and its timestamp's float32 bits), or None."""
     indptr: torch.Tensor
     entries: torch.Tensor
     ts: torch.Tensor
@@ -189,6 +192,7 @@ class TCSR:
     num_nodes: int
     ts_index: Optional[torch.Tensor] = None
     hist: Optional[torch.Tensor] = None
+    dir: Optional[torch.Tensor] = None
 
     @property
     def num_entries(self) -> int:
@@ -218,7 +222,8 @@ class TCSR:
                       self.entries.data_ptr() if m else None, self.ts.data_ptr() if m else None,
                       self.nodes.data_ptr(),
                       self.ts_index.data_ptr() if m and self.ts_index is not None else None,
-                      self.hist.data_ptr() if m and self.hist is not None else None)
+                      self.hist.data_ptr() if m and self.hist is not None else None,
+                      self.dir.data_ptr() if m and self.dir is not None else None)
 
 
 def pack_entries(nbr: np.ndarray, ts: np.ndarray, eid: np.ndarray) -> np.ndarray:
@@ -236,11 +241,11 @@ def index_len(num_entries: int) -> int:
 
 
 def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hints: bool = True,
-                   hist: bool = True) -> TCSR:
+                   hist: bool = True, dir: bool = True) -> TCSR:
     """Uploads a T-CSR given as host arrays (e.g. one built elsewhere) and
     computes its node summaries, if `index` its search index, if `hints` the
-    neighbour-first hint bits (else they stay clear) and if `hist` the
-    neighbour histories."""
+    neighbour-first hint bits (else they stay clear), if `hist` the
+    neighbour histories and if `dir` the time directories."""
     rec = pack_entries(nbr, ts, eid)
     ent = torch.from_numpy(rec).to(device)
     tsa = torch.from_numpy(np.ascontiguousarray(np.asarray(ts, np.float32))).to(device)
@@ -253,12 +258,14 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hint
     m = int(ent.shape[0])
     tsx = torch.empty(index_len(m), dtype=torch.float32, device=device) if index else None
     hs = torch.empty((m, 2), dtype=torch.int32, device=device) if hist else None
+    td = torch.empty((index_len(m), 2), dtype=torch.int32, device=device) if dir else None
     _check(lib().tgl_tcsr_nodes(_p(ip), _p(tsa) if m else None, n, m, _p(nodes),
                                 _p(tsx) if index and m else None, _p(ent) if (hints or hist) and m else None,
-                                _p(hs) if hist and m else None, _stream()), "tgl_tcsr_nodes")
+                                _p(hs) if hist and m else None, _p(td) if dir and m else None, _stream()),
+           "tgl_tcsr_nodes")
     if hist and not hints and m:
         ent.view(torch.int32)[:, 0] &= NBR_MASK     # histories need the entries; keep the hint bits clear
-    return TCSR(ip, ent, tsa, nodes, n, tsx, hs)
+    return TCSR(ip, ent, tsa, nodes, n, tsx, hs, td)
 
 
 def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:
@@ -269,10 +276,10 @@ def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True
 def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
                eid: Optional[torch.Tensor], num_nodes: int, undirected: bool = True,
                workspace: Optional[torch.Tensor] = None, stream=None, index: bool = True,
-               hist: bool = True) -> TCSR:
+               hist: bool = True, dir: bool = True) -> TCSR:
     """Builds the T-CSR of a device COO (int32 src/dst, float32 ts, int64 eid or
-    None), with its search index if `index` and its neighbour histories if
-    `hist`."""
+    None), with its search index if `index`, its neighbour histories if
+    `hist` and its time directories if `dir`."""
     L = lib()
     m0 = int(src.shape[0])
     flags = BUILD_UNDIRECTED if undirected else 0
@@ -289,6 +296,7 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
     nodes = torch.empty((num_nodes, NODE_WORDS), dtype=torch.int32, device=dev)
     tsx = torch.empty(index_len(M), dtype=torch.float32, device=dev) if index else None
     hs = torch.empty((M, 2), dtype=torch.int32, device=dev) if hist else None
+    td = torch.empty((index_len(M), 2), dtype=torch.int32, device=dev) if dir else None
     need = int(L.tgl_tcsr_build_workspace(m0, num_nodes, flags))
     if need == 0:
         raise TglError(EINVAL, "tgl_tcsr_build_workspace")
@@ -297,12 +305,12 @@ def tcsr_build(src: torch.Tensor, dst: torch.Tensor, ts: torch.Tensor,
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
     s = L.tgl_tcsr_build(_p(src), _p(dst), _p(ts), _p(eid), m0, num_nodes, flags, _p(indptr),
                          _p(entries) if M else None, _p(tsa) if M else None, _p(nodes),
-                         _p(tsx) if index and M else None, _p(hs) if hist and M else None, _p(workspace),
-                         workspace.numel(), _stream(stream))
+                         _p(tsx) if index and M else None, _p(hs) if hist and M else None,
+                         _p(td) if dir and M else None, _p(workspace), workspace.numel(), _stream(stream))
     if own_ws:
         del workspace
     _check(s, "tgl_tcsr_build")
-    return TCSR(indptr, entries, tsa, nodes, num_nodes, tsx, hs)
+    return TCSR(indptr, entries, tsa, nodes, num_nodes, tsx, hs, td)
 
 
 # --------------------------------------------------------------------------

@@ -20,6 +20,7 @@
 //
 // The paper builds the T-CSR once on the host; here the same structure is
 // produced on the device from a COO that may be in any order.
+#include "tgl_cells.hpp"
 #include "tgl_internal.hpp"
 
 namespace tgl {
@@ -667,6 +668,56 @@ __global__ __launch_bounds__(kBlock) void index_kernel(const float *__restrict__
         idx[j] = ts[j * TGL_INDEX_STRIDE];
 }
 
+// Time directory (tgl_cell), one lane per search-index slot j: the node x
+// whose run [a, b) holds entry p = j * TGL_INDEX_STRIDE (the last x with
+// indptr[x] <= p, by a binary search of indptr), then the first position of
+// the run whose timestamp falls in cell k = j - ceil(a / TGL_INDEX_STRIDE)
+// or later, or b if there is none (a binary search of the run on the cells
+// of its timestamps; a run whose timestamps are all equal has every entry
+// in cell 0).  The run bounds and first and last timestamps come from the
+// node records, which the sampler reads too.  A slot whose entry the
+// record's run does not hold (only with a malformed indptr) gets {a, +inf}.
+__global__ __launch_bounds__(kBlock) void dir_kernel(const int64_t *__restrict__ indptr,
+                                                     const float *__restrict__ ts, const int4 *__restrict__ nodes,
+                                                     int64_t N, int64_t M, int64_t L, uint2 *__restrict__ dir) {
+    constexpr uint32_t X = TGL_INDEX_STRIDE;
+    const uint32_t um = static_cast<uint32_t>(M);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < L; j += stride) {
+        const int64_t p = j * X;
+        int64_t lo = 0, hi = N - 1;
+        while (lo < hi) {
+            const int64_t mid = lo + (hi - lo + 1) / 2;
+            if (indptr[mid] <= p) lo = mid;
+            else hi = mid - 1;
+        }
+        const int4 r = nodes[lo * 8];
+        uint32_t a = static_cast<uint32_t>(r.x), b = static_cast<uint32_t>(r.y);
+        a = a > um ? um : a;
+        b = b < a ? a : (b > um ? um : b);
+        uint32_t pos = a;
+        float cts = __builtin_inff();
+        if (p >= a && p < b) {
+            const float f = __int_as_float(r.z), l = __int_as_float(r.w);
+            const uint32_t ja = a / X + (a % X != 0);
+            const uint32_t K = b / X + (b % X != 0) - ja;
+            const uint32_t k = static_cast<uint32_t>(j) - ja;
+            if (k > 0) {
+                const float sc = dir_scale(f, l, K);
+                uint32_t l2 = a, r2 = b;
+                while (l2 < r2) {
+                    const uint32_t m = l2 + (r2 - l2) / 2;
+                    if (dir_cell(ts[m], f, l, sc, K) < k) l2 = m + 1;
+                    else r2 = m;
+                }
+                pos = l2;
+            }
+            if (pos < b) cts = ts[pos];
+        }
+        dir[j] = make_uint2(pos, __float_as_uint(cts));
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void fill_indptr_kernel(int64_t *__restrict__ indptr, int64_t n,
                                                              int64_t value) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
@@ -768,14 +819,15 @@ size_t tgl_tcsr_build_workspace(int64_t num_edges, int64_t num_nodes, uint32_t f
 tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *ts,
                           const int64_t *eid, int64_t num_edges, int64_t num_nodes,
                           uint32_t flags, int64_t *indptr, tgl_entry *entries, float *ts_out,
-                          tgl_node *nodes_out, float *ts_index_out, tgl_span *hist_out, void *workspace,
-                          size_t workspace_bytes, void *stream) {
+                          tgl_node *nodes_out, float *ts_index_out, tgl_span *hist_out,
+                          tgl_cell *dir_out, void *workspace, size_t workspace_bytes, void *stream) {
     if (!build_args_ok(num_edges, num_nodes, flags)) return TGL_EINVAL;
     if (num_edges > 0 && (!src || !dst || !ts || !entries || !ts_out)) return TGL_EINVAL;
     if (!indptr || !nodes_out) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(nodes_out) & 127u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_index_out) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(hist_out) & 7u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(dir_out) & 7u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(ts_out) & 15u) != 0) return TGL_EINVAL;
     const int64_t m0 = num_edges;
@@ -894,6 +946,11 @@ tgl_status tgl_tcsr_build(const int32_t *src, const int32_t *dst, const float *t
         hist_kernel<<<grid_for((M + kEmitPerLane - 1) / kEmitPerLane), kBlock, 0, st>>>(
             reinterpret_cast<int4 *>(entries), ts_out, M, reinterpret_cast<const int4 *>(nodes_out), num_nodes,
             reinterpret_cast<uint2 *>(hist_out), true);
+    if (dir_out) {
+        const int64_t L = tgl_index_len(M);
+        dir_kernel<<<grid_for(L), kBlock, 0, st>>>(indptr, ts_out, reinterpret_cast<const int4 *>(nodes_out),
+                                                   num_nodes, M, L, reinterpret_cast<uint2 *>(dir_out));
+    }
     return launch_status();
 }
 
@@ -904,7 +961,7 @@ int64_t tgl_index_len(int64_t num_entries) {
 
 tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_nodes,
                           int64_t num_entries, tgl_node *nodes, float *ts_index, tgl_entry *entries,
-                          tgl_span *hist, void *stream) {
+                          tgl_span *hist, tgl_cell *dir, void *stream) {
     if (num_nodes < 1 || num_nodes > INT32_MAX) return TGL_EINVAL;
     if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
     if (!indptr || !nodes || (num_entries > 0 && !ts)) return TGL_EINVAL;
@@ -913,6 +970,7 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
     if ((reinterpret_cast<uintptr_t>(ts_index) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(hist) & 7u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(dir) & 7u) != 0) return TGL_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     (void)hipGetLastError();
     nodes_kernel<<<grid_for(num_nodes * 8), kBlock, 0, st>>>(indptr, ts, num_nodes, num_entries,
@@ -929,6 +987,11 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
         hist_kernel<<<grid_for((num_entries + kEmitPerLane - 1) / kEmitPerLane), kBlock, 0, st>>>(
             reinterpret_cast<int4 *>(entries), ts, num_entries, reinterpret_cast<const int4 *>(nodes), num_nodes,
             reinterpret_cast<uint2 *>(hist), false);
+    if (dir && num_entries > 0) {
+        const int64_t L = tgl_index_len(num_entries);
+        dir_kernel<<<grid_for(L), kBlock, 0, st>>>(indptr, ts, reinterpret_cast<const int4 *>(nodes), num_nodes,
+                                                   num_entries, L, reinterpret_cast<uint2 *>(dir));
+    }
     return launch_status();
 }
 

@@ -31,6 +31,7 @@
 // device and the next hop's kernels read them.
 #include <mutex>
 
+#include "tgl_cells.hpp"
 #include "tgl_internal.hpp"
 
 namespace tgl {
@@ -57,6 +58,7 @@ struct HopArgs {
     const int4 *nodes;          // tgl_node per node (8 x 16 bytes): run start, end, first ts,
                                 // last ts, then the run's first timestamps
     const uint2 *hist;          // tgl_span per entry: the neighbour's entries older than it
+    const uint2 *dir;           // tgl_cell per search-index slot: the runs' time directories, or null
     int64_t num_nodes;
     int64_t num_entries;
     // hop 1: dense roots
@@ -136,7 +138,7 @@ __device__ __forceinline__ HeldRun<G> load_run(const float *__restrict__ tsa, ui
 #pragma unroll
     for (int m = 0; m < HeldRun<G>::NV; m++) {
         const uint32_t p4 = r.p0 + 4 * m;
-        r.v[m] = p4 < hi ? load_ts4(tsa, p4, M) : make_float4(inf, inf, inf, inf);
+        r.v[m] = p4 < hi && lo < hi ? load_ts4(tsa, p4, M) : make_float4(inf, inf, inf, inf);
     }
     return r;
 }
@@ -226,6 +228,10 @@ __device__ __forceinline__ void search_n(const float *__restrict__ arr, uint32_t
             }
         }
     }
+    bool open = false;
+#pragma unroll
+    for (int i = 0; i < NE; i++) open |= hi[i] > lo[i];
+    if (!open) return;                              // group-uniform: every answer is known
     HeldRun<G> r[NE];
 #pragma unroll
     for (int i = 0; i < NE; i++) r[i] = load_run<G>(arr, lo[i], hi[i], n_arr, gl);
@@ -292,69 +298,8 @@ __device__ __forceinline__ void guided_round(const float *__restrict__ arr, uint
     }
 }
 
-// Positions below NE thresholds in the time-sorted run [lo0, hi0) of the
-// timestamp array (M entries): out[i] = lo0 + #{p in [lo0, hi0): ts[p] < v[i]}
-// for each i with act[i] (out[i] = lo0 otherwise).  rec, when not null, is the
-// record of a node whose whole run (lo0 onwards) is inline in it: the run is
-// then read from there.  A run of at most one held stretch is loaded once and
-// serves every threshold.  A run long enough to
-// need more than one probe round is first narrowed on the search index tsx
-// (nx samples, tsx[j] = ts[j * TGL_INDEX_STRIDE]) when there is one, starting
-// with a round guided by the run shape rs (the run that holds the stretch,
-// lo0 its start): with r
-// the samples inside the run below v[i], the answer lies after sample r - 1
-// and at or before sample r, fewer than TGL_INDEX_STRIDE timestamps.
-template <int G, int NE>
-__device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uint32_t M,
-                                              const float *__restrict__ tsx, uint32_t nx,
-                                              const int4 *__restrict__ rec, uint32_t lo0, uint32_t hi0,
-                                              const RunShape &rs, const float (&v)[NE], const bool (&act)[NE],
-                                              uint32_t (&out)[NE], int gl) {
-    constexpr uint32_t X = TGL_INDEX_STRIDE;
-    if (rec || hi0 - lo0 <= HeldRun<G>::span) {    // group-uniform: one load serves every bound
-        const HeldRun<G> r = rec ? load_inline<G>(rec, lo0, gl) : load_run<G>(tsa, lo0, hi0, M, gl);
-#pragma unroll
-        for (int i = 0; i < NE; i++) out[i] = act[i] ? count_in<G>(r, lo0, hi0, v[i]) : lo0;
-        return;
-    }
-    uint32_t lo[NE], hi[NE];
-    if (tsx && hi0 - lo0 > HeldRun<G>::span * (G + 1)) {   // group-uniform
-        // samples j in [ja, jb) are the positions j * X inside [lo0, hi0)
-        const uint32_t ja = lo0 / X + (lo0 % X != 0);
-        const uint32_t jb = hi0 / X + (hi0 % X != 0);
-        uint32_t gc[NE], gd[NE];
-#pragma unroll
-        for (int i = 0; i < NE; i++) {
-            lo[i] = ja;
-            hi[i] = act[i] ? jb : ja;
-            uint32_t pos, spread;
-            run_estimate(rs, v[i], pos, spread);
-            gc[i] = pos / X;
-            gd[i] = spread / X > 0 ? spread / X : 1u;
-        }
-        guided_round<G, NE>(tsx, lo, hi, v, gc, gd, gl);
-        search_n<G, NE>(tsx, nx, lo, hi, v, gl);
-#pragma unroll
-        for (int i = 0; i < NE; i++) {
-            const uint32_t r = lo[i];
-            lo[i] = r > ja ? (r - 1) * X + 1 : lo0;  // ts[(r-1) X] < v[i]
-            hi[i] = r < jb ? r * X : hi0;            // ts[r X] >= v[i]
-            if (!act[i]) hi[i] = lo[i];
-        }
-    } else {
-#pragma unroll
-        for (int i = 0; i < NE; i++) {
-            lo[i] = lo0;
-            hi[i] = act[i] ? hi0 : lo0;
-        }
-    }
-    search_n<G, NE>(tsa, M, lo, hi, v, gl);
-#pragma unroll
-    for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0;
-}
-
-// count_below_n with a range per threshold: out[i] = lo0[i] + #{p in
-// [lo0[i], hi0[i]): ts[p] < v[i]} for each i with act[i] (lo0[i] otherwise),
+// Positions below NE thresholds, each in a range of its own: out[i] = lo0[i]
+// + #{p in [lo0[i], hi0[i]): ts[p] < v[i]} for each i with act[i] (lo0[i] otherwise),
 // each range a stretch of one sorted run.  Ranges longer than one probe round
 // are narrowed on the search index first when there is one.
 template <int G, int NE>
@@ -396,6 +341,128 @@ __device__ __forceinline__ void count_below_ranges(const float *__restrict__ tsa
     search_n<G, NE>(tsa, M, lo, hi, v, gl);
 #pragma unroll
     for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0[i];
+}
+
+// Positions below NE thresholds in [lo0, hi0), a range of the run [rs.a,
+// rs.b), from the run's time directory (tgl_cell per search-index slot; the
+// run owns K >= 1 cells), as count_below_n returns them: threshold i falls in cell
+// k = cell(v[i]), whose first position pos and timestamp, and the next
+// cell's pos (rs.b after the last cell), are read with one round of loads.
+// The run's count below v[i] is pos when v[i] <= ts[pos], else it lies in
+// [pos + 1, next pos], a stretch of about TGL_INDEX_STRIDE entries when the
+// run's timestamps are spread evenly, which count_below_ranges searches
+// (with the index when it is long).  Clamping the stretch into [lo0, hi0)
+// gives the count within that range.  Every position read from the
+// directory is clamped into the run.
+template <int G, int NE>
+__device__ __forceinline__ void count_below_dir(const float *__restrict__ tsa, uint32_t M,
+                                                const float *__restrict__ tsx, uint32_t nx,
+                                                const uint2 *__restrict__ dir, uint32_t lo0, uint32_t hi0,
+                                                const RunShape &rs, const float (&v)[NE], const bool (&act)[NE],
+                                                uint32_t (&out)[NE], int gl) {
+    constexpr uint32_t X = TGL_INDEX_STRIDE;
+    const uint32_t ja = rs.a / X + (rs.a % X != 0);
+    const uint32_t K = rs.b / X + (rs.b % X != 0) - ja;
+    const float sc = dir_scale(rs.first, rs.last, K);
+    uint2 c0[NE];
+    uint32_t c1[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        c0[i] = make_uint2(rs.a, 0u);
+        c1[i] = rs.b;
+        if (act[i]) {                               // group-uniform
+            const uint32_t kc = dir_cell(v[i], rs.first, rs.last, sc, K);
+            c0[i] = dir[ja + kc];
+            if (kc + 1 < K) c1[i] = dir[ja + kc + 1].x;
+        }
+    }
+    uint32_t lo[NE], hi[NE];
+    bool open[NE];
+#pragma unroll
+    for (int i = 0; i < NE; i++) {
+        const uint32_t pos = c0[i].x < rs.a ? rs.a : (c0[i].x > rs.b ? rs.b : c0[i].x);
+        const uint32_t nxt = c1[i] < pos ? pos : (c1[i] > rs.b ? rs.b : c1[i]);
+        const bool past = v[i] > __uint_as_float(c0[i].y) && pos < nxt;
+        uint32_t l = past ? pos + 1 : pos;
+        uint32_t h = past ? nxt : l;
+        l = l < lo0 ? lo0 : (l > hi0 ? hi0 : l);
+        h = h < l ? l : (h > hi0 ? hi0 : h);
+        lo[i] = act[i] ? l : lo0;
+        hi[i] = act[i] ? h : lo0;
+        open[i] = act[i] && h > l;
+    }
+    count_below_ranges<G, NE>(tsa, M, tsx, nx, lo, hi, v, open, out, gl);
+}
+
+// Positions below NE thresholds in the time-sorted run [lo0, hi0) of the
+// timestamp array (M entries): out[i] = lo0 + #{p in [lo0, hi0): ts[p] < v[i]}
+// for each i with act[i] (out[i] = lo0 otherwise).  rec, when not null, is the
+// record of a node whose whole run (lo0 onwards) is inline in it: the run is
+// then read from there.  A run of at most one held stretch is loaded once and
+// serves every threshold.  A longer range starts from the time directory dir
+// of its run rs when there is one (count_below_dir).  Otherwise a range long
+// enough to need more than one probe round is first narrowed on the search
+// index tsx (nx samples, tsx[j] = ts[j * TGL_INDEX_STRIDE]) when there is
+// one, starting with a round guided by the run shape rs (the run that holds
+// the stretch, lo0 its start): with r the samples inside the run below v[i],
+// the answer lies after sample r - 1 and at or before sample r, fewer than
+// TGL_INDEX_STRIDE timestamps.
+template <int G, int NE, bool DIR>
+__device__ __forceinline__ void count_below_n(const float *__restrict__ tsa, uint32_t M,
+                                              const float *__restrict__ tsx, uint32_t nx,
+                                              const uint2 *__restrict__ dir,
+                                              const int4 *__restrict__ rec, uint32_t lo0, uint32_t hi0,
+                                              const RunShape &rs, const float (&v)[NE], const bool (&act)[NE],
+                                              uint32_t (&out)[NE], int gl) {
+    constexpr uint32_t X = TGL_INDEX_STRIDE;
+    if (rec || hi0 - lo0 <= HeldRun<G>::span) {    // group-uniform: one load serves every bound
+        const HeldRun<G> r = rec ? load_inline<G>(rec, lo0, gl) : load_run<G>(tsa, lo0, hi0, M, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++) out[i] = act[i] ? count_in<G>(r, lo0, hi0, v[i]) : lo0;
+        return;
+    }
+    if constexpr (DIR) {
+        // the range is longer than one held stretch, so its run owns a cell
+        count_below_dir<G, NE>(tsa, M, tsx, nx, dir, lo0, hi0, rs, v, act, out, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++)
+            if (!act[i]) out[i] = lo0;
+        return;
+    }
+    uint32_t lo[NE], hi[NE];
+    if (tsx && hi0 - lo0 > HeldRun<G>::span * (G + 1)) {   // group-uniform
+        // samples j in [ja, jb) are the positions j * X inside [lo0, hi0)
+        const uint32_t ja = lo0 / X + (lo0 % X != 0);
+        const uint32_t jb = hi0 / X + (hi0 % X != 0);
+        uint32_t gc[NE], gd[NE];
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            lo[i] = ja;
+            hi[i] = act[i] ? jb : ja;
+            uint32_t pos, spread;
+            run_estimate(rs, v[i], pos, spread);
+            gc[i] = pos / X;
+            gd[i] = spread / X > 0 ? spread / X : 1u;
+        }
+        guided_round<G, NE>(tsx, lo, hi, v, gc, gd, gl);
+        search_n<G, NE>(tsx, nx, lo, hi, v, gl);
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            const uint32_t r = lo[i];
+            lo[i] = r > ja ? (r - 1) * X + 1 : lo0;  // ts[(r-1) X] < v[i]
+            hi[i] = r < jb ? r * X : hi0;            // ts[r X] >= v[i]
+            if (!act[i]) hi[i] = lo[i];
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < NE; i++) {
+            lo[i] = lo0;
+            hi[i] = act[i] ? hi0 : lo0;
+        }
+    }
+    search_n<G, NE>(tsa, M, lo, hi, v, gl);
+#pragma unroll
+    for (int i = 0; i < NE; i++) out[i] = act[i] ? lo[i] : lo0;
 }
 
 // Window edges of a long run [a, b) found from saved positions -- the
@@ -608,7 +675,7 @@ __device__ __forceinline__ void wave_sync_lds() {
 // windows: run [a, b) with first and last timestamps, query time t, hash key
 // hp; its slots start at q * S * k.  All G lanes of the group call it
 // together; my_edges is the group's row of LDS.
-template <int G, int MODE, bool LAST, bool PTR>
+template <int G, int MODE, bool LAST, bool PTR, bool DIR>
 __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, int32_t x, uint32_t a, uint32_t b,
                                            float first, float last, float t, uint64_t hp, int gl,
                                            uint32_t *my_edges) {
@@ -638,7 +705,7 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, int32_t 
             for (int u = 0; u < NE; u++) ei[u] = i0 + u;
             from_pointers<G, NE>(p, x, a, b, ei, v, act, cs, gl);
         } else {
-            count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, nullptr, a, top, RunShape{a, b, first, last}, v, act, cs, gl);
+            count_below_n<G, NE, DIR>(p.tsa, M, p.tsx, p.nx, p.dir, nullptr, a, top, RunShape{a, b, first, last}, v, act, cs, gl);
         }
 #pragma unroll
         for (int u = 0; u < NE; u++) {
@@ -698,7 +765,7 @@ __device__ __forceinline__ void multi_root(const HopArgs &p, int64_t q, int32_t 
 //     packed into LDS;
 //   phase 2, G lanes per root, 64 / G roots per round: the S + 1 window
 //     edges, then selection and emission of the root's S * k slots.
-template <int G, int MODE, bool LAST, bool PTR>
+template <int G, int MODE, bool LAST, bool PTR, bool DIR>
 __global__ __launch_bounds__(kBlock) void hop_multi_wide_kernel(const HopArgs p) {
     constexpr int GPW = kWave / G;            // roots served per wavefront round
     constexpr int GPB = kBlock / G;
@@ -748,7 +815,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_wide_kernel(const HopArgs p)
         for (int base = 0; base < nvalid; base += GPW) {
             const int i = base + gw;
             if (i < nvalid) {                       // group-uniform
-                multi_root<G, MODE, LAST, PTR>(p, c * kWave + i, r_x[w][i], r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i],
+                multi_root<G, MODE, LAST, PTR, DIR>(p, c * kWave + i, r_x[w][i], r_a[w][i], r_b[w][i], r_f[w][i], r_l[w][i],
                                           r_t[w][i], r_hp[w][i], gl, my_edges);
             }
         }
@@ -767,7 +834,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_wide_kernel(const HopArgs p)
 //   phase 3, one lane per slot: selection, gather and emission.  Roots are
 //     dense on the first hop, so a chunk's slots are one contiguous range of
 //     the output and the stores coalesce.
-template <int MODE, bool LAST, bool PTR>
+template <int MODE, bool LAST, bool PTR, bool DIR>
 __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     constexpr int G = 8;
     constexpr int GPW = kWave / G;            // roots located per wavefront round
@@ -859,7 +926,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                         for (int u = 0; u < NE; u++) ei[u] = i0 + u;
                         from_pointers<G, NE>(p, xi, a, b, ei, vv, act, cs, gl);
                     } else {
-                        count_below_n<G, NE>(p.tsa, M, p.tsx, p.nx, rec, a, top, RunShape{a, b, first, last}, vv,
+                        count_below_n<G, NE, DIR>(p.tsa, M, p.tsx, p.nx, p.dir, rec, a, top, RunShape{a, b, first, last}, vv,
                                              act, cs, gl);
                     }
 #pragma unroll
@@ -946,7 +1013,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
 // that the run's first and last timestamps decide is not searched.  NB is
 // the number of window edges: 1 when windows are unbounded below (lo = a),
 // else 2.
-template <int G, int NB, bool PTR>
+template <int G, int NB, bool PTR, bool DIR>
 __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint32_t a, uint32_t b, float first,
                                               float last, float vh, float vl, int gl, uint32_t &lo, uint32_t &hi) {
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
@@ -968,7 +1035,7 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
         for (int i = 0; i < NB; i++) ei[i] = i;             // hop 1 with one window: edges t and t - D
         from_pointers<G, NB>(p, x, a, b, ei, v, act, cs, gl);
     } else {
-        count_below_n<G, NB>(p.tsa, M, p.tsx, p.nx, rec, a, b, RunShape{a, b, first, last}, v, act, cs, gl);
+        count_below_n<G, NB, DIR>(p.tsa, M, p.tsx, p.nx, p.dir, rec, a, b, RunShape{a, b, first, last}, v, act, cs, gl);
     }
     hi = act[0] ? cs[0] : c[0];
     lo = NB == 1 ? a : (act[NB - 1] ? cs[NB - 1] : c[NB - 1]);
@@ -993,9 +1060,10 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
 // which the previous hop gathered with the entry; phase 1 takes it from
 // there, and reads no node record and leaves nothing to search.  A hop that
 // is not the last gathers the histories of its picks for the next hop.
-template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR, bool WIN>
+template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR, bool WIN, bool DIR>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !FIRST ? 8 : (NB == 1 ? 7 : 6)))) void hop_single_kernel(const HopArgs p) {
     static_assert(FIRST || !PTR, "saved window edges are kept for hop 1 only");
+    static_assert(!(PTR && DIR), "saved window edges replace the directory");
     static_assert(!WIN || NB == 1, "histories give windows unbounded below");
     constexpr int GPW = kWave / G;            // roots located per wavefront round
     constexpr int U = 4;                      // slots per lane whose loads are in flight together
@@ -1153,7 +1221,7 @@ __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !
             if (base + gw < nneed) {                // group-uniform
                 const int i = r_need[w][base + gw];
                 uint32_t wlo, whi;
-                locate_window<G, NB, PTR>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_vh[w][i],
+                locate_window<G, NB, PTR, DIR>(p, r_x[w][i], r_lo[w][i], r_n[w][i], r_f[w][i], r_l[w][i], r_vh[w][i],
                                           NB == 2 ? r_vl[w][i] : 0.0f, gl, wlo, whi);
                 if (gl == 0) {
                     r_lo[w][i] = wlo;
@@ -1240,37 +1308,52 @@ void launch_mode_last(int G, bool first, bool multi, bool win, const HopArgs &a,
     if (blocks < 1) blocks = 1;
     if (blocks > kMaxGrid) blocks = kMaxGrid;
     const unsigned nb = static_cast<unsigned>(blocks);
+    // kernels that search long runs start from the time directories when the
+    // T-CSR has them; those that keep saved window edges search from those
+    const bool dir = a.dir != nullptr;
     if (multi && a.windows + 1 <= kMultiEdges) {   // first hop only
-        if (a.ptr) hop_multi_kernel<MODE, LAST, true><<<nb, kBlock, 0, st>>>(a);
-        else hop_multi_kernel<MODE, LAST, false><<<nb, kBlock, 0, st>>>(a);
+        if (a.ptr) hop_multi_kernel<MODE, LAST, true, false><<<nb, kBlock, 0, st>>>(a);
+        else if (dir) hop_multi_kernel<MODE, LAST, false, true><<<nb, kBlock, 0, st>>>(a);
+        else hop_multi_kernel<MODE, LAST, false, false><<<nb, kBlock, 0, st>>>(a);
     } else if (multi && a.ptr) {              // first hop only; saved window edges kept
         switch (G) {
-            case 16: hop_multi_wide_kernel<16, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
-            case 32: hop_multi_wide_kernel<32, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
-            default: hop_multi_wide_kernel<64, MODE, LAST, true><<<nb, kBlock, 0, st>>>(a); break;
+            case 16: hop_multi_wide_kernel<16, MODE, LAST, true, false><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_wide_kernel<32, MODE, LAST, true, false><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_wide_kernel<64, MODE, LAST, true, false><<<nb, kBlock, 0, st>>>(a); break;
+        }
+    } else if (multi && dir) {                // first hop only
+        switch (G) {
+            case 16: hop_multi_wide_kernel<16, MODE, LAST, false, true><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_wide_kernel<32, MODE, LAST, false, true><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_wide_kernel<64, MODE, LAST, false, true><<<nb, kBlock, 0, st>>>(a); break;
         }
     } else if (multi) {                       // first hop only
         switch (G) {
-            case 16: hop_multi_wide_kernel<16, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
-            case 32: hop_multi_wide_kernel<32, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
-            default: hop_multi_wide_kernel<64, MODE, LAST, false><<<nb, kBlock, 0, st>>>(a); break;
+            case 16: hop_multi_wide_kernel<16, MODE, LAST, false, false><<<nb, kBlock, 0, st>>>(a); break;
+            case 32: hop_multi_wide_kernel<32, MODE, LAST, false, false><<<nb, kBlock, 0, st>>>(a); break;
+            default: hop_multi_wide_kernel<64, MODE, LAST, false, false><<<nb, kBlock, 0, st>>>(a); break;
         }
     } else {
         // the window search uses 8 lanes per root whatever the fanout; one
         // window edge when windows are unbounded below, else two
         const bool ptr = first && a.ptr;
         if (win) {                            // windows unbounded below, neighbour histories kept
-            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true, true><<<nb, kBlock, 0, st>>>(a);
-            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false, true><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 1, false, true><<<nb, kBlock, 0, st>>>(a);
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true, true, false><<<nb, kBlock, 0, st>>>(a);
+            else if (first && dir) hop_single_kernel<8, MODE, LAST, true, 1, false, true, true><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false, true, false><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 1, false, true, false><<<nb, kBlock, 0, st>>>(a);
         } else if (a.delta_inf) {
-            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true, false><<<nb, kBlock, 0, st>>>(a);
-            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false, false><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 1, false, false><<<nb, kBlock, 0, st>>>(a);
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 1, true, false, false><<<nb, kBlock, 0, st>>>(a);
+            else if (first && dir) hop_single_kernel<8, MODE, LAST, true, 1, false, false, true><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 1, false, false, false><<<nb, kBlock, 0, st>>>(a);
+            else if (dir) hop_single_kernel<8, MODE, LAST, false, 1, false, false, true><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 1, false, false, false><<<nb, kBlock, 0, st>>>(a);
         } else {
-            if (ptr) hop_single_kernel<8, MODE, LAST, true, 2, true, false><<<nb, kBlock, 0, st>>>(a);
-            else if (first) hop_single_kernel<8, MODE, LAST, true, 2, false, false><<<nb, kBlock, 0, st>>>(a);
-            else hop_single_kernel<8, MODE, LAST, false, 2, false, false><<<nb, kBlock, 0, st>>>(a);
+            if (ptr) hop_single_kernel<8, MODE, LAST, true, 2, true, false, false><<<nb, kBlock, 0, st>>>(a);
+            else if (first && dir) hop_single_kernel<8, MODE, LAST, true, 2, false, false, true><<<nb, kBlock, 0, st>>>(a);
+            else if (first) hop_single_kernel<8, MODE, LAST, true, 2, false, false, false><<<nb, kBlock, 0, st>>>(a);
+            else if (dir) hop_single_kernel<8, MODE, LAST, false, 2, false, false, true><<<nb, kBlock, 0, st>>>(a);
+            else hop_single_kernel<8, MODE, LAST, false, 2, false, false, false><<<nb, kBlock, 0, st>>>(a);
         }
     }
 }
@@ -1470,6 +1553,7 @@ tgl_status sample_check(const tgl_tcsr *g, const int32_t *roots, const float *ro
     if ((reinterpret_cast<uintptr_t>(g->ts) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->ts_index) & 15u) != 0) return TGL_EINVAL;
     if ((reinterpret_cast<uintptr_t>(g->hist) & 7u) != 0) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(g->dir) & 7u) != 0) return TGL_EINVAL;
     if (num_roots > 0 && (!roots || !root_ts)) return TGL_EINVAL;
     if (!capacities(num_roots, hops, fanouts, num_snapshots, cap)) return TGL_EINVAL;
     for (int h = 0; h < hops; h++) {
@@ -1530,6 +1614,7 @@ tgl_status tgl_sample_ex(const tgl_tcsr *g, const int32_t *roots, const float *r
     a.tsx = g->num_entries > 0 ? g->ts_index : nullptr;
     a.nx = static_cast<uint32_t>(tgl_index_len(g->num_entries));
     a.nodes = reinterpret_cast<const int4 *>(g->nodes);
+    a.dir = g->num_entries > 0 ? reinterpret_cast<const uint2 *>(g->dir) : nullptr;
     // windows of hops >= 2 from the histories of the previous hop's entries:
     // one snapshot unbounded below (either anchor then places the window of
     // a root below its own time)

@@ -108,7 +108,117 @@ def check_hist_device(g, chunk=1 << 27):
     torch.cuda.empty_cache()
 
 
-def tcsr_to_host(g, hints=True, hist_on_host=True):
+def dir_scale_np(f, l, K):
+    """Cells per unit of time of runs with first and last timestamps f, l and
+    K cells (tgl_cell): K / (l - f) in float32 when l - f is positive and
+    finite, else 0."""
+    f = np.asarray(f, np.float32)
+    l = np.asarray(l, np.float32)
+    with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
+        span = l - f
+        ok = (span > 0) & np.isfinite(span)
+        return np.where(ok, np.asarray(K).astype(np.float32) / np.where(ok, span, np.float32(1)),
+                        np.float32(0)).astype(np.float32)
+
+
+def dir_cell_np(t, f, l, sc, K):
+    """The cell of time t in a run (tgl_cell): 0 for t <= f, K - 1 for t >= l,
+    else min(K - 1, floor((t - f) * sc)), in float32 operations."""
+    t = np.asarray(t, np.float32)
+    f = np.asarray(f, np.float32)
+    l = np.asarray(l, np.float32)
+    sc = np.asarray(sc, np.float32)
+    K = np.asarray(K, np.int64)
+    with np.errstate(invalid="ignore", over="ignore"):
+        x = (t - f) * sc
+        mid = np.where(x < K.astype(np.float32), np.trunc(np.where(np.isfinite(x), x, 0)), K).astype(np.int64)
+    mid = np.minimum(mid, K - 1)
+    return np.where(~(t > f), 0, np.where(t >= l, K - 1, mid)).astype(np.int64)
+
+
+def dir_cells(indptr, ts):
+    """The time directory of every run, from its definition (tgl_cell): for
+    search-index slot j, with a, b the run holding entry 32 j and k = j -
+    ceil(a / 32) its cell, pos = a + #{entries of the run in cells below k} and
+    its timestamp (+inf at b).  Cells grow along a run and runs follow each
+    other, so slot ceil(a / 32) + cell is a non-decreasing key over all
+    entries, and pos is the lower bound of j among the keys."""
+    X = 32
+    indptr = np.asarray(indptr, np.int64)
+    ts = np.asarray(ts, np.float32)
+    M = len(ts)
+    L = -(-M // X)
+    n = len(indptr) - 1
+    a, b = indptr[:-1], indptr[1:]
+    ja, jb = -(-a // X), -(-b // X)
+    K = jb - ja
+    has = b > a
+    f = np.where(has, ts[np.minimum(a, max(M - 1, 0))] if M else np.inf, np.inf).astype(np.float32)
+    l = np.where(has, ts[np.maximum(b - 1, 0)] if M else -np.inf, -np.inf).astype(np.float32)
+    sc = dir_scale_np(f, l, K)
+    owner = np.repeat(np.arange(n, dtype=np.int64), np.diff(indptr))
+    c = dir_cell_np(ts, f[owner], l[owner], sc[owner], K[owner])
+    key = np.where(K[owner] > 0, ja[owner] + c, ja[owner] - 1)
+    assert np.all(np.diff(key) >= 0)
+    j = np.arange(L, dtype=np.int64)
+    pos = np.searchsorted(key, j, side="left")
+    slot_owner = np.searchsorted(indptr, j * X, side="right") - 1
+    end = indptr[slot_owner + 1]
+    cts = np.full(L, np.inf, np.float32)
+    inside = pos < end
+    cts[inside] = ts[pos[inside]]
+    return pos, cts
+
+
+def check_dir_slots(g, chunk=1 << 24):
+    """Time directory of a device T-CSR against its definition, slot by slot:
+    with a, b, f, l the run of the entry 32 j (from the node records) and k
+    its cell, pos must be the position where the run's cells reach k (entry
+    pos - 1 in a lower cell or pos = a; entry pos in cell k or above, or pos
+    = b), and the cell's timestamp that of entry pos (+inf at b).  Positions are gathered on the device;
+    the cells are computed on the host in float32."""
+    import torch
+    M, n = g.num_entries, g.num_nodes
+    L = -(-M // 32)
+    ip = g.indptr
+    rec = g.nodes[:, :4]
+    for j0 in range(0, L, chunk):
+        j = torch.arange(j0, min(L, j0 + chunk), device=ip.device, dtype=torch.int64)
+        x = torch.searchsorted(ip, j * 32, right=True) - 1
+        r = rec[x].cpu().numpy()
+        d = g.dir[j0:j0 + len(j)]
+        pos = d[:, 0].long() & 0xFFFFFFFF
+        prev = ts_at(g.ts, pos - 1)
+        here = ts_at(g.ts, pos)
+        jn = j.cpu().numpy()
+        pos = pos.cpu().numpy()
+        a = r[:, 0].view(np.uint32).astype(np.int64)
+        b = r[:, 1].view(np.uint32).astype(np.int64)
+        f = r[:, 2].view(np.float32)
+        l = r[:, 3].view(np.float32)
+        assert np.all((a <= jn * 32) & (jn * 32 < b)), "node records do not cover the slots from %d" % j0
+        ja = -(-a // 32)
+        K = -(-b // 32) - ja
+        k = jn - ja
+        sc = dir_scale_np(f, l, K)
+        assert np.all((pos >= a) & (pos <= b)), "directory position outside its run from slot %d" % j0
+        cp = dir_cell_np(prev.cpu().numpy(), f, l, sc, K)
+        ch = dir_cell_np(here.cpu().numpy(), f, l, sc, K)
+        inside = pos < b
+        assert np.all((pos == a) | (cp < k)), "directory position too high from slot %d" % j0
+        assert np.all(~inside | (ch >= k)), "directory position too low from slot %d" % j0
+        want = np.where(inside, here.cpu().numpy(), np.float32(np.inf)).astype(np.float32)
+        got = d[:, 1].cpu().numpy().view(np.uint32)
+        assert np.array_equal(got, want.view(np.uint32)), "directory timestamp from slot %d" % j0
+
+
+def ts_at(ts, pos):
+    """ts[pos] on the device, with positions clamped into the array."""
+    import torch
+    return ts[torch.clamp(pos, 0, ts.shape[0] - 1)]
+
+
+def tcsr_to_host(g, hints=True, hist_on_host=True, dir_on_host=True):
     """Host copy of a device T-CSR; checks that the separate timestamp array
     equals the records' timestamps bit for bit, and that the neighbour-first
     hint bits follow their definition (or, with hints=False, are all clear)."""
@@ -139,6 +249,12 @@ def tcsr_to_host(g, hints=True, hist_on_host=True):
     if g.ts_index is not None:
         tsx = g.ts_index.cpu().numpy()
         assert np.array_equal(tsx.view(np.uint32), ts[::32].view(np.uint32)), "search index"
+    if g.dir is not None and dir_on_host and len(ts):
+        pos, cts = dir_cells(ip, ts)
+        d = g.dir.cpu().numpy().view(np.uint32)
+        assert np.array_equal(d[:, 0].astype(np.int64), pos), "time directory positions: %d differ" % int(
+            (d[:, 0] != pos).sum())
+        assert np.array_equal(d[:, 1], cts.view(np.uint32)), "time directory timestamps"
     if g.hist is not None and hist_on_host:
         hs = g.hist.cpu().numpy().view(np.uint32).astype(np.int64)
         lo, hi = hist_of(ip, nbr, ts)

@@ -97,6 +97,7 @@ def _sample_call(**kw):
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE + 64)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE, FAKE + 4)),
     dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE, None, FAKE + 4)),           # misaligned histories
+    dict(g=B.c_tcsr(10, 100, FAKE, FAKE, FAKE, FAKE, None, None, FAKE + 4)),     # misaligned directory
     dict(g=B.c_tcsr(10, 2**32, FAKE, FAKE, FAKE, FAKE)),
     dict(g=B.c_tcsr(2**31, 100, FAKE, FAKE, FAKE, FAKE)), dict(g=None), dict(counts=None),
 ])
@@ -121,11 +122,11 @@ def test_sample_workspace_too_small():
 def _build_call(**kw):
     L = P.lib()
     a = dict(src=FAKE, dst=FAKE, ts=FAKE, eid=None, m=10, n=5, flags=1, indptr=FAKE,
-             ent=FAKE, ts_out=FAKE, nodes=FAKE, tsx=None, hist=None, ws=FAKE, ws_bytes=1 << 30)
+             ent=FAKE, ts_out=FAKE, nodes=FAKE, tsx=None, hist=None, dir=None, ws=FAKE, ws_bytes=1 << 30)
     a.update(kw)
     return L.tgl_tcsr_build(a["src"], a["dst"], a["ts"], a["eid"], a["m"], a["n"], a["flags"],
-                            a["indptr"], a["ent"], a["ts_out"], a["nodes"], a["tsx"], a["hist"], a["ws"],
-                            a["ws_bytes"], None)
+                            a["indptr"], a["ent"], a["ts_out"], a["nodes"], a["tsx"], a["hist"], a["dir"],
+                            a["ws"], a["ws_bytes"], None)
 
 
 @pytest.mark.parametrize("kw,want", [
@@ -135,7 +136,7 @@ def _build_call(**kw):
     (dict(ent=FAKE + 4), B.EINVAL), (dict(m=2**31), B.EINVAL),
     (dict(ts_out=None), B.EINVAL), (dict(ts_out=FAKE + 8), B.EINVAL),
     (dict(nodes=None), B.EINVAL), (dict(nodes=FAKE + 4), B.EINVAL), (dict(nodes=FAKE + 64), B.EINVAL), (dict(tsx=FAKE + 8), B.EINVAL),
-    (dict(hist=FAKE + 4), B.EINVAL),
+    (dict(hist=FAKE + 4), B.EINVAL), (dict(dir=FAKE + 4), B.EINVAL),
     (dict(ws_bytes=8), B.ENOSPACE), (dict(ws=None), B.ENOSPACE),
 ])
 def test_build_rejects_invalid_arguments(kw, want):
@@ -147,11 +148,12 @@ def test_nodes_rejects_invalid_arguments():
     for args in [(FAKE, FAKE, 0, 10, FAKE), (FAKE, FAKE, 2**31, 10, FAKE), (FAKE, FAKE, 5, -1, FAKE),
                  (FAKE, FAKE, 5, 2**32, FAKE), (None, FAKE, 5, 10, FAKE), (FAKE, None, 5, 10, FAKE),
                  (FAKE, FAKE, 5, 10, None), (FAKE, FAKE, 5, 10, FAKE + 4), (FAKE, FAKE, 5, 10, FAKE + 64)]:
-        assert L.tgl_tcsr_nodes(*args, None, None, None, None) == B.EINVAL, args
-    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, FAKE + 4, None, None, None) == B.EINVAL   # misaligned index
-    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, FAKE + 8, None, None) == B.EINVAL   # misaligned entries
-    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, FAKE, FAKE + 4, None) == B.EINVAL   # misaligned histories
-    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, None, FAKE, None) == B.EINVAL   # histories need entries
+        assert L.tgl_tcsr_nodes(*args, None, None, None, None, None) == B.EINVAL, args
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, FAKE + 4, None, None, None, None) == B.EINVAL   # misaligned index
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, FAKE + 8, None, None, None) == B.EINVAL   # misaligned entries
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, FAKE, FAKE + 4, None, None) == B.EINVAL   # misaligned histories
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, None, FAKE, None, None) == B.EINVAL   # histories need entries
+    assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, None, None, FAKE + 4, None) == B.EINVAL   # misaligned directory
 
 
 def test_index_len():

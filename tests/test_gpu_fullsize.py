@@ -17,6 +17,9 @@ configuration bench.py times.
 * Every full-size build's neighbour histories are checked on the device
   against their definition (the lower bound of each entry's time in its
   neighbour's run).  The c4 steps sample through them.
+* Every full-size build's time directory is checked slot by slot: each
+  cell's position is where its run's cells reach that cell, and its
+  timestamp is that entry's.  The c3 and c5 steps search through them.
 """
 import gc
 
@@ -28,7 +31,7 @@ import paper_2203_14883_amd as P
 from oracle import subgraph
 from paper_2203_14883_amd import workloads as W
 from checks import assert_hops_equal, same_bits
-from gpu_util import announce, check_hist_device, hops_to_numpy, require_gpu
+from gpu_util import announce, check_dir_slots, check_hist_device, hops_to_numpy, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -74,6 +77,8 @@ def build_on_gpu(torch, w):
     torch.cuda.empty_cache()
     # neighbour histories of every entry against their definition
     check_hist_device(g)
+    # time directory of every run, slot by slot
+    check_dir_slots(g)
     return g
 
 
@@ -156,7 +161,7 @@ def test_full_size_whole_steps(torch, name):
     del src, dst, ts, eid
     gc.collect()
     announce("%s full size: T-CSR byte for byte" % name)
-    assert_tcsr_equal(tcsr_to_host(g, hist_on_host=False), og, "%s full size" % name)
+    assert_tcsr_equal(tcsr_to_host(g, hist_on_host=False, dir_on_host=False), og, "%s full size" % name)
     gc.collect()
     B = 64 if name == "c3" else 1
     for b0 in (w.num_batches() // 2, w.num_batches() - B):

@@ -31,9 +31,9 @@ def assert_tcsr_equal(got, want, what=""):
     assert same_bits(got.ts, want.ts), what + " ts: " + str(first_diff(got.ts, want.ts))
 
 
-def gpu_build(src, dst, ts, eid, n, undirected, hist=True):
+def gpu_build(src, dst, ts, eid, n, undirected, hist=True, dir=True):
     return P.tcsr_build(upload(src, np.int32), upload(dst, np.int32), upload(ts, np.float32),
-                        None if eid is None else upload(eid, np.int64), n, undirected, hist=hist)
+                        None if eid is None else upload(eid, np.int64), n, undirected, hist=hist, dir=dir)
 
 
 def gpu_sample(g, roots, rts, fan, mode, S, D, seed, base, anchor="own"):
@@ -75,10 +75,11 @@ def test_random_small_graphs(torch):
     for trial in range(160):
         N, src, dst, ts, eid, und, roots, rts, fan, mode, S, D, seed, base = _rand_case(rng)
         hist = trial % 3 != 2              # with and without neighbour histories
-        announce("random trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s hist=%s"
-                 % (trial, N, len(src), len(roots), fan, mode, S, D, hist))
+        tdir = trial % 4 != 3              # with and without time directories
+        announce("random trial %d N=%d m0=%d R=%d fan=%s mode=%s S=%d D=%s hist=%s dir=%s"
+                 % (trial, N, len(src), len(roots), fan, mode, S, D, hist, tdir))
         want_g = oracle.build_tcsr(src, dst, ts, eid, N, und)
-        g = gpu_build(src, dst, ts, eid, N, und, hist)
+        g = gpu_build(src, dst, ts, eid, N, und, hist, tdir)
         assert_tcsr_equal(tcsr_to_host(g), want_g, "trial %d" % trial)
         want = oracle.sample(want_g, roots, rts, fan, mode, S, D, seed, base)
         got = gpu_sample(g, roots, rts, fan, mode, S, D, seed, base)
@@ -251,8 +252,10 @@ def test_long_runs_and_off_grid_window_edges(torch):
     want_g = oracle.build_tcsr(src, dst, ts, None, N, False)
     g = gpu_build(src, dst, ts, None, N, False)
     assert_tcsr_equal(tcsr_to_host(g), want_g, "long runs")
-    assert g.ts_index is not None
-    g_plain = dataclasses.replace(g, ts_index=None)
+    assert g.ts_index is not None and g.dir is not None
+    variants = ((g, "directory and index"), (dataclasses.replace(g, dir=None), "index"),
+                (dataclasses.replace(g, ts_index=None), "directory"),
+                (dataclasses.replace(g, ts_index=None, dir=None), "neither"))
     for S, D, R in [(1, math.inf, 3000), (1, 0.1, 3000), (3, 0.37, 3000), (7, 0.1, 1500), (8, 0.37, 1500),
                     (9, 0.1, 1000), (64, 0.1, 300)]:
         roots = rng.integers(0, N, R).astype(np.int32)
@@ -262,18 +265,19 @@ def test_long_runs_and_off_grid_window_edges(torch):
         for mode in ("recent", "uniform"):
             announce("long runs S=%d D=%s R=%d mode=%s" % (S, D, R, mode))
             want = oracle.sample(want_g, roots, rts, [10, 5], mode, S, D, 11, 3)
-            for gg, what in ((g, "indexed"), (g_plain, "no index")):
+            for gg, what in variants:
                 got = gpu_sample(gg, roots, rts, [10, 5], mode, S, D, 11, 3)
                 assert_hops_equal(got, want, "S=%d D=%s %s %s" % (S, D, mode, what))
 
 
 def test_guided_search_on_skewed_runs(torch):
     """The first round on the search index places its probes by interpolating
-    between a run's first and last timestamps; the window edges must not
-    depend on how good that guess is.  Long runs (indexed search) whose
+    between a run's first and last timestamps, and the time directory splits
+    the same span into even cells; the window edges must not depend on how
+    well either fits the run.  Long runs (indexed search) whose
     timestamps are far from evenly spread -- nearly all at the start, nearly
-    all at the end, geometric, two clusters, one value with two outliers, and
-    an even spread for contrast -- queried at entry timestamps, between them
+    all at the end, geometric, two clusters, one value with two outliers, one
+    value throughout, and an even spread for contrast -- queried at entry timestamps, between them
     and outside the run, with 1-3 snapshots and 1-2 hops."""
     rng = np.random.default_rng(4242)
     L = 60_000
@@ -284,6 +288,7 @@ def test_guided_search_on_skewed_runs(torch):
         np.sort(2.0 ** (rng.random(L) * 40.0)),                                 # geometric over 12 decades
         np.sort(np.concatenate([rng.random(L // 2) * 10.0, 9.9e5 + rng.random(L - L // 2) * 10.0])),  # two clusters
         np.concatenate([[-1e9], np.full(L - 2, 5.0), [1e9]]),                   # one value, two outliers
+        np.full(L, 5.0),                                                        # one value throughout
     ]
     N = len(runs)
     src = np.concatenate([np.full(L, x, np.int32) for x in range(N)])
@@ -302,8 +307,9 @@ def test_guided_search_on_skewed_runs(torch):
         for mode, fan in (("recent", [10]), ("uniform", [10, 3])):
             announce("skewed runs S=%d D=%s mode=%s" % (S, D, mode))
             want = oracle.sample(want_g, roots, rts, fan, mode, S, D, 5, 0)
-            got = gpu_sample(g, roots, rts, fan, mode, S, D, 5, 0)
-            assert_hops_equal(got, want, "skewed runs S=%d D=%s %s" % (S, D, mode))
+            for gg, what in ((g, "directory"), (dataclasses.replace(g, dir=None), "index")):
+                got = gpu_sample(gg, roots, rts, fan, mode, S, D, 5, 0)
+                assert_hops_equal(got, want, "skewed runs S=%d D=%s %s %s" % (S, D, mode, what))
 
 
 def test_chunk_scheduled_batches(torch):

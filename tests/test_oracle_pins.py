@@ -394,3 +394,75 @@ def test_history_definition_matches_brute_force():
                 assert (lo[p], hi[p]) == (ip[v], ip[v] + int((run < ts[p]).sum())), (trial, p)
             else:
                 assert (lo[p], hi[p]) == (0, 0), (trial, p)
+
+
+def _cell_scalar(t, f, l, K):
+    """One timestamp's cell in a run (tgl_cell), written out with float32
+    scalars: cells split [f, l] evenly, every operation rounded to float32."""
+    t, f, l = np.float32(t), np.float32(f), np.float32(l)
+    with np.errstate(invalid="ignore", over="ignore", divide="ignore"):
+        span = np.float32(l - f)
+        sc = np.float32(np.float32(K) / span) if span > 0 and np.isfinite(span) else np.float32(0)
+        if not t > f:
+            return 0
+        if t >= l:
+            return K - 1
+        x = np.float32(np.float32(t - f) * sc)
+    c = int(np.floor(x)) if x < np.float32(K) else K
+    return min(c, K - 1)
+
+
+def test_time_directory_definition_matches_brute_force():
+    """The test-side definition of the runs' time directories (used to check
+    the GPU's at every size) against a loop over each run and cell: cell k of
+    a run [a, b) sits in search-index slot ceil(a / 32) + k and holds a + the
+    number of the run's timestamps in lower cells, and the timestamp there
+    (+inf at b).  Then the property the sampler relies on: a threshold v in
+    cell k has #{ts < v} between the cell's position and the next cell's,
+    equal to the cell's position when v is at or below its timestamp.  Runs
+    with ties, infinities, denormals, runs of one repeated timestamp (all in
+    cell 0), and lengths around multiples of 32."""
+    from gpu_util import dir_cells
+    rng = np.random.default_rng(23)
+    vals = np.array([-np.inf, -2.5, -1e-40, 0.0, 1e-40, 3.0, 3.5, 7.0, 1e30, np.inf], np.float32)
+    for trial in range(120):
+        n = int(rng.integers(1, 6))
+        m = int(rng.integers(1, 400))
+        owner = np.sort(rng.integers(0, n, m))
+        if trial % 4 == 0:
+            ts = rng.choice(vals, m)
+        elif trial % 4 == 1:
+            ts = rng.integers(0, 40, m).astype(np.float32)         # heavy ties
+        elif trial % 4 == 2:
+            ts = (rng.random(m) * 1e3).astype(np.float32)
+        else:
+            ts = np.full(m, rng.choice(vals[1:-1]), np.float32)   # every run one timestamp
+        order = np.lexsort((ts, owner))
+        owner, ts = owner[order], ts[order]
+        ip = np.concatenate([[0], np.cumsum(np.bincount(owner, minlength=n))]).astype(np.int64)
+        pos, cts = dir_cells(ip, ts)
+        assert len(pos) == -(-m // 32)
+        seen = 0
+        for x in range(n):
+            a, b = int(ip[x]), int(ip[x + 1])
+            ja, jb = -(-a // 32), -(-b // 32)
+            K = jb - ja
+            run = ts[a:b]
+            cells = [_cell_scalar(t, run[0], run[-1], K) for t in run] if K > 0 else []
+            want = [a + sum(c < k for c in cells) for k in range(K)]
+            for k in range(K):
+                assert pos[ja + k] == want[k], (trial, x, k)
+                wt = ts[want[k]] if want[k] < b else np.float32(np.inf)
+                assert cts[ja + k].view(np.uint32) == np.float32(wt).view(np.uint32), (trial, x, k)
+            seen += K
+            probes = np.concatenate([vals, run, run + np.float32(0.5)]).astype(np.float32) if K > 0 else []
+            for v in probes:
+                if np.isnan(v):
+                    continue
+                k = _cell_scalar(v, run[0], run[-1], K)
+                below = a + int((run < v).sum())
+                nxt = int(pos[ja + k + 1]) if k + 1 < K else b
+                assert pos[ja + k] <= below <= nxt, (trial, x, v)
+                if v <= cts[ja + k]:
+                    assert below == pos[ja + k], (trial, x, v)
+        assert seen == len(pos)
