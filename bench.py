@@ -708,8 +708,10 @@ def main():
     # memory)
     hist = (args.row == "sample" and len(w.fanouts) > 1 and w.snapshots == 1
             and math.isinf(w.snapshot_len))
-    # time directories serve the window searches of long runs
-    tdir = args.row == "sample" and not args.no_dir
+    # time directories serve the window searches of long runs; with
+    # histories only hop 1 searches, which for c4's runs (mostly short, a
+    # single edge per root) measured the same with and without them
+    tdir = args.row == "sample" and not hist and not args.no_dir
     P.timer_enable(1 << 14)
     g = P.tcsr_build(d_src, d_dst, d_ts, d_eid, w.num_nodes, w.undirected, workspace=ws, hist=hist,
                      dir=tdir)  # warm-up
