@@ -280,6 +280,26 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
                           int64_t num_entries, tgl_node *nodes, float *ts_index,
                           tgl_entry *entries, tgl_span *hist, tgl_cell *dir, void *stream);
 
+/*
+ * Conversions between the entries and the column layout of Section 3.1's
+ * T-CSR (separate neighbour, timestamp and edge-id arrays beside indptr), for
+ * T-CSRs that arrive or leave in columns.
+ *
+ * tgl_tcsr_pack writes entries[p] = {nbr[p] with bit 31 clear, ts[p],
+ * eid[p]} (eid NULL: p).  The hints stay clear; tgl_tcsr_nodes sets them
+ * and writes the per-node data of the packed T-CSR.
+ *   nbr, ts, eid  [device] int32 / float / int64 [num_entries]
+ *   entries       [device] tgl_entry[num_entries], 16-byte aligned, output
+ * tgl_tcsr_unpack writes the neighbour ids (bit 31 cleared) and edge ids of
+ * the entries to nbr and eid, either of which may be NULL (the timestamps are
+ * the T-CSR's ts array already).
+ * num_entries in [0, 2^32 - 1].  Neither synchronises.
+ */
+tgl_status tgl_tcsr_pack(const int32_t *nbr, const float *ts, const int64_t *eid, int64_t num_entries,
+                         tgl_entry *entries, void *stream);
+tgl_status tgl_tcsr_unpack(const tgl_entry *entries, int64_t num_entries, int32_t *nbr, int64_t *eid,
+                           void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Sampler (Algorithm 1; Section 3.1 "Sampling" and "Parallel Sampling")    */
 /* ------------------------------------------------------------------------ */

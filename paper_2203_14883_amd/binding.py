@@ -40,7 +40,7 @@ MODES = {"recent": MOST_RECENT, "most_recent": MOST_RECENT, "uniform": UNIFORM,
 
 # every function declared in include/tgl.h
 EXPORTS = ("tgl_version", "tgl_status_str", "tgl_tcsr_build_workspace", "tgl_tcsr_build",
-           "tgl_index_len", "tgl_tcsr_nodes", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
+           "tgl_index_len", "tgl_tcsr_nodes", "tgl_tcsr_pack", "tgl_tcsr_unpack", "tgl_sample_capacity", "tgl_sample_workspace", "tgl_sample",
            "tgl_sample_ex", "tgl_sample_noalloc", "tgl_pointers_reset", "tgl_mfg_workspace", "tgl_mfg_export",
            "tgl_gather", "tgl_time_encode", "tgl_timer_enable",
            "tgl_timer_disable", "tgl_timer_read", "tgl_timer_reset", "tgl_timer_select")
@@ -107,6 +107,10 @@ def lib() -> C.CDLL:
     L.tgl_index_len.argtypes = [i64]
     L.tgl_tcsr_nodes.restype = i32
     L.tgl_tcsr_nodes.argtypes = [P, P, i64, i64, P, P, P, P, P, P]
+    L.tgl_tcsr_pack.restype = i32
+    L.tgl_tcsr_pack.argtypes = [P, P, P, i64, P, P]
+    L.tgl_tcsr_unpack.restype = i32
+    L.tgl_tcsr_unpack.argtypes = [P, i64, P, P, P]
     L.tgl_sample_capacity.restype = i64
     L.tgl_sample_capacity.argtypes = [i64, i32, P, i32, i32]
     L.tgl_sample_workspace.restype = C.c_size_t
@@ -266,6 +270,50 @@ def tcsr_from_host(indptr, nbr, ts, eid, device="cuda", index: bool = True, hint
     if hist and not hints and m:
         ent.view(torch.int32)[:, 0] &= NBR_MASK     # histories need the entries; keep the hint bits clear
     return TCSR(ip, ent, tsa, nodes, n, tsx, hs, td)
+
+
+def tcsr_from_columns(indptr: torch.Tensor, nbr: torch.Tensor, ts: torch.Tensor, eid: Optional[torch.Tensor],
+                      index: bool = True, hints: bool = True, hist: bool = True, dir: bool = True,
+                      stream=None) -> TCSR:
+    """A T-CSR from device columns (int64 indptr[N+1], int32 nbr, float32 ts,
+    int64 eid or None for eid = position), packed into entries on the device,
+    with its node records and, as asked, search index, hints, histories and
+    time directories.  `ts` becomes the T-CSR's timestamp array."""
+    m = int(nbr.shape[0])
+    for t, dt in ((indptr, torch.int64), (nbr, torch.int32), (ts, torch.float32)):
+        if t.dtype != dt or not t.is_contiguous():
+            raise ValueError("indptr must be int64, nbr int32, ts float32, all contiguous")
+    if ts.shape[0] != m or (eid is not None and (eid.dtype != torch.int64 or not eid.is_contiguous()
+                                                   or eid.shape[0] != m)):
+        raise ValueError("nbr, ts and eid must have the same length")
+    dev = nbr.device
+    n = int(indptr.shape[0]) - 1
+    ent = torch.empty((m, 2), dtype=torch.int64, device=dev)
+    st = _stream(stream)
+    _check(lib().tgl_tcsr_pack(_p(nbr) if m else None, _p(ts) if m else None, _p(eid) if m else None, m,
+                               _p(ent) if m else None, st), "tgl_tcsr_pack")
+    nodes = torch.empty((n, NODE_WORDS), dtype=torch.int32, device=dev)
+    tsx = torch.empty(index_len(m), dtype=torch.float32, device=dev) if index else None
+    hs = torch.empty((m, 2), dtype=torch.int32, device=dev) if hist else None
+    td = torch.empty((index_len(m), 2), dtype=torch.int32, device=dev) if dir else None
+    _check(lib().tgl_tcsr_nodes(_p(indptr), _p(ts) if m else None, n, m, _p(nodes),
+                                _p(tsx) if index and m else None, _p(ent) if (hints or hist) and m else None,
+                                _p(hs) if hist and m else None, _p(td) if dir and m else None, st),
+           "tgl_tcsr_nodes")
+    if hist and not hints and m:
+        ent.view(torch.int32)[:, 0] &= NBR_MASK
+    return TCSR(indptr, ent, ts, nodes, n, tsx, hs, td)
+
+
+def tcsr_columns(g: TCSR, stream=None):
+    """The neighbour ids (hint bits cleared) and edge ids of a device T-CSR's
+    entries as separate int32 and int64 columns, unpacked on the device."""
+    m = g.num_entries
+    nbr = torch.empty(m, dtype=torch.int32, device=g.entries.device)
+    eid = torch.empty(m, dtype=torch.int64, device=g.entries.device)
+    _check(lib().tgl_tcsr_unpack(_p(g.entries) if m else None, m, _p(nbr) if m else None,
+                                 _p(eid) if m else None, _stream(stream)), "tgl_tcsr_unpack")
+    return nbr, eid
 
 
 def tcsr_build_workspace(num_edges: int, num_nodes: int, undirected: bool = True) -> int:

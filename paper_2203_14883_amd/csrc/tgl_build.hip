@@ -718,6 +718,31 @@ __global__ __launch_bounds__(kBlock) void dir_kernel(const int64_t *__restrict__
     }
 }
 
+// Columns to 16-byte entries: entry p = {nbr[p] with bit 31 clear, ts[p],
+// eid[p] (p when eid is null)}.
+__global__ __launch_bounds__(kBlock) void pack_kernel(const int32_t *__restrict__ nbr, const float *__restrict__ ts,
+                                                      const int64_t *__restrict__ eid, int64_t M,
+                                                      int4 *__restrict__ ent) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
+        const int64_t e = eid ? eid[p] : p;
+        ent[p] = make_int4(static_cast<int>(static_cast<uint32_t>(nbr[p]) & TGL_NBR_MASK), __float_as_int(ts[p]),
+                           static_cast<int>(static_cast<uint32_t>(e)),
+                           static_cast<int>(static_cast<uint32_t>(static_cast<uint64_t>(e) >> 32)));
+    }
+}
+
+// 16-byte entries to columns: nbr (bit 31 cleared) and eid, each optional.
+__global__ __launch_bounds__(kBlock) void unpack_kernel(const int4 *__restrict__ ent, int64_t M,
+                                                        int32_t *__restrict__ nbr, int64_t *__restrict__ eid) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
+    for (int64_t p = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; p < M; p += stride) {
+        const int4 v = ent[p];
+        if (nbr) nbr[p] = static_cast<int32_t>(static_cast<uint32_t>(v.x) & TGL_NBR_MASK);
+        if (eid) eid[p] = static_cast<int64_t>(static_cast<uint32_t>(v.z)) | (static_cast<int64_t>(v.w) << 32);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void fill_indptr_kernel(int64_t *__restrict__ indptr, int64_t n,
                                                              int64_t value) {
     const int64_t stride = static_cast<int64_t>(gridDim.x) * kBlock;
@@ -992,6 +1017,32 @@ tgl_status tgl_tcsr_nodes(const int64_t *indptr, const float *ts, int64_t num_no
         dir_kernel<<<grid_for(L), kBlock, 0, st>>>(indptr, ts, reinterpret_cast<const int4 *>(nodes), num_nodes,
                                                    num_entries, L, reinterpret_cast<uint2 *>(dir));
     }
+    return launch_status();
+}
+
+tgl_status tgl_tcsr_pack(const int32_t *nbr, const float *ts, const int64_t *eid, int64_t num_entries,
+                         tgl_entry *entries, void *stream) {
+    if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
+    if (num_entries > 0 && (!nbr || !ts || !entries)) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    if (num_entries > 0)
+        pack_kernel<<<grid_for(num_entries), kBlock, 0, st>>>(nbr, ts, eid, num_entries,
+                                                               reinterpret_cast<int4 *>(entries));
+    return launch_status();
+}
+
+tgl_status tgl_tcsr_unpack(const tgl_entry *entries, int64_t num_entries, int32_t *nbr, int64_t *eid,
+                           void *stream) {
+    if (num_entries < 0 || num_entries > kMaxEntries) return TGL_EINVAL;
+    if (num_entries > 0 && !entries) return TGL_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(entries) & 15u) != 0) return TGL_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    (void)hipGetLastError();
+    if (num_entries > 0 && (nbr || eid))
+        unpack_kernel<<<grid_for(num_entries), kBlock, 0, st>>>(reinterpret_cast<const int4 *>(entries),
+                                                                 num_entries, nbr, eid);
     return launch_status();
 }
 

@@ -156,6 +156,20 @@ def test_nodes_rejects_invalid_arguments():
     assert L.tgl_tcsr_nodes(FAKE, FAKE, 5, 10, FAKE, None, None, None, FAKE + 4, None) == B.EINVAL   # misaligned directory
 
 
+def test_pack_unpack_reject_invalid_arguments():
+    L = P.lib()
+    assert L.tgl_tcsr_pack(FAKE, FAKE, None, -1, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_pack(FAKE, FAKE, None, 2**32, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_pack(None, FAKE, None, 10, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_pack(FAKE, None, None, 10, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_pack(FAKE, FAKE, None, 10, None, None) == B.EINVAL
+    assert L.tgl_tcsr_pack(FAKE, FAKE, None, 10, FAKE + 8, None) == B.EINVAL      # misaligned entries
+    assert L.tgl_tcsr_unpack(FAKE, -1, FAKE, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_unpack(FAKE, 2**32, FAKE, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_unpack(None, 10, FAKE, FAKE, None) == B.EINVAL
+    assert L.tgl_tcsr_unpack(FAKE + 4, 10, FAKE, FAKE, None) == B.EINVAL          # misaligned entries
+
+
 def test_index_len():
     L = P.lib()
     for m, want in [(0, 0), (1, 1), (31, 1), (32, 1), (33, 2), (64, 2), (65, 3), (2**32 - 1, 2**27), (-1, -1)]:

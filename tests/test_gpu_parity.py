@@ -312,6 +312,32 @@ def test_guided_search_on_skewed_runs(torch):
                 assert_hops_equal(got, want, "skewed runs S=%d D=%s %s %s" % (S, D, mode, what))
 
 
+def test_column_view_round_trip(torch):
+    """The column layout of Sec. 3.1 (indptr, nbr, ts, eid as separate arrays)
+    in and out of the entries on the device: columns unpacked from a GPU
+    build equal the oracle's; the oracle's columns packed on the device give
+    the same T-CSR (records, index, hints, histories, directories against
+    their definitions) and the same samples, with and without edge ids."""
+    rng = np.random.default_rng(31)
+    for trial in range(12):
+        N, src, dst, ts, eid, und, roots, rts, fan, mode, S, D, seed, base = _rand_case(rng)
+        if trial == 0:
+            src, dst, ts, eid = src[:0], dst[:0], ts[:0], None
+        announce("columns trial %d N=%d m0=%d eid=%s" % (trial, N, len(src), eid is not None))
+        og = oracle.build_tcsr(src, dst, ts, eid, N, und)
+        g = gpu_build(src, dst, ts, eid, N, und)
+        nbr, e = P.tcsr_columns(g)
+        assert np.array_equal(nbr.cpu().numpy(), og.nbr.astype(np.int32)), "unpacked nbr, trial %d" % trial
+        assert np.array_equal(e.cpu().numpy(), og.eid), "unpacked eid, trial %d" % trial
+        pos_ids = trial % 2 == 1                     # pack without edge ids: eid = position
+        h = P.tcsr_from_columns(upload(og.indptr, np.int64), upload(og.nbr, np.int32), upload(og.ts, np.float32),
+                                None if pos_ids else upload(og.eid, np.int64))
+        want_g = og if not pos_ids else oracle.TCSR(og.indptr, og.nbr, np.arange(len(og.nbr), dtype=np.int64), og.ts)
+        assert_tcsr_equal(tcsr_to_host(h), want_g, "columns trial %d" % trial)
+        want = oracle.sample(want_g, roots, rts, fan, mode, S, D, seed, base)
+        assert_hops_equal(gpu_sample(h, roots, rts, fan, mode, S, D, seed, base), want, "columns trial %d" % trial)
+
+
 def test_chunk_scheduled_batches(torch):
     """Batches of random chunk scheduling (Alg. 2) -- edge ranges that start at
     chunk offsets, not at the batch grid -- fused into one GPU call, against the
