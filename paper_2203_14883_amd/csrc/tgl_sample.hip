@@ -1061,12 +1061,16 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
 // there, and reads no node record and leaves nothing to search.  A hop that
 // is not the last gathers the histories of its picks for the next hop.
 template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR, bool WIN, bool DIR>
-__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !FIRST ? 8 : (NB == 1 ? 7 : 6)))) void hop_single_kernel(const HopArgs p) {
+__global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !FIRST ? 4 : (NB == 1 ? 7 : 6)))) void hop_single_kernel(const HopArgs p) {
     static_assert(FIRST || !PTR, "saved window edges are kept for hop 1 only");
     static_assert(!(PTR && DIR), "saved window edges replace the directory");
     static_assert(!WIN || NB == 1, "histories give windows unbounded below");
     constexpr int GPW = kWave / G;            // roots located per wavefront round
-    constexpr int U = 4;                      // slots per lane whose loads are in flight together
+    // slots per lane whose loads are in flight together.  A hop that takes its
+    // windows from the histories searches nothing, and its registers go to
+    // ten record loads per lane: a chunk of 64 roots with k = 10 then issues
+    // all its gathers at once (4 waves per SIMD instead of 8)
+    constexpr int U = WIN && !FIRST ? 10 : 4;
     const int lane = lane_id();
     const int w = threadIdx.x / kWave;
     const int gl = lane & (G - 1);
