@@ -852,9 +852,17 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
     __shared__ float r_t[kWavesPerBlock][kWave];
     __shared__ int32_t r_x[kWavesPerBlock][kWave];
     __shared__ uint32_t r_e[kWavesPerBlock][kWave * kMultiEdges];   // window edges of each root
+    // The last hop in most-recent mode needs no lower edge for the last
+    // window: its candidates are the newest entries below its upper edge,
+    // and one of them is in the window exactly when its timestamp is at or
+    // above the window's lower bound.  That bound is kept per root and the
+    // gathered entries are checked against it instead of locating the edge.
+    constexpr bool TAIL = MODE == TGL_MOST_RECENT && LAST;
+    __shared__ float r_vw[kWavesPerBlock][TAIL ? kWave : 1];        // lower bound of the last window
 
     const uint32_t M = static_cast<uint32_t>(p.num_entries);
     const int W = p.windows;
+    const int nedge = TAIL ? W : W + 1;       // window edges located per root
     const int k = p.k;
     const int nslots = W * k;                 // slots per root
     const int64_t nv = p.num_roots;
@@ -891,12 +899,13 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
             r_hp[w][lane] = MODE == TGL_UNIFORM ? mix64(p.seedmix ^ (p.root_base + static_cast<uint64_t>(v))) : 0;
             r_t[w][lane] = t;
             r_x[w][lane] = x;
+            if constexpr (TAIL) r_vw[w][lane] = bound_value(t, W, p.delta);
         }
         wave_sync_lds();
         const int64_t rem = nv - c * kWave;
         const int nvalid = rem < kWave ? static_cast<int>(rem) : kWave;
 
-        // ---- phase 2: G lanes per root locate its W + 1 window edges ----
+        // ---- phase 2: G lanes per root locate its W + 1 window edges (W with TAIL) ----
         for (int base = 0; base < nvalid; base += GPW) {
             const int i = base + gw;
             if (i < nvalid) {                       // group-uniform
@@ -909,7 +918,8 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                 // a non-empty run belongs to a node inside the graph
                 const int4 *rec = b > a && b - a <= TGL_NODE_INLINE ? p.nodes + static_cast<int64_t>(xi) * 8 : nullptr;
                 uint32_t top = b;
-                for (int i0 = 0; i0 <= W; i0 += NE) {
+                if (TAIL && gl == 0) r_e[w][i * kMultiEdges + W] = a;   // the last window reaches down to the run start
+                for (int i0 = 0; i0 < nedge; i0 += NE) {
                     float vv[NE];
                     bool act[NE];
                     uint32_t cc[NE];
@@ -917,7 +927,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                     for (int u = 0; u < NE; u++) {
                         vv[u] = bound_value(ti, i0 + u, p.delta);
                         cc[u] = a;
-                        act[u] = i0 + u <= W && !edge_from_summary(a, b, first, last, vv[u], cc[u]);
+                        act[u] = i0 + u < nedge && !edge_from_summary(a, b, first, last, vv[u], cc[u]);
                     }
                     uint32_t cs[NE];
                     if (PTR && !rec && b - a > HeldRun<G>::span) {   // group-uniform: saved positions kept
@@ -931,7 +941,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                     }
 #pragma unroll
                     for (int u = 0; u < NE; u++) {
-                        if (i0 + u <= W) {
+                        if (i0 + u < nedge) {
                             const uint32_t e = act[u] ? cs[u] : cc[u];
                             if (gl == 0) r_e[w][i * kMultiEdges + i0 + u] = e;
                             top = e < top ? e : top;
@@ -964,6 +974,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
         for (int e0 = 0; e0 < total; e0 += U * kWave) {
             uint32_t pick[U];                       // UINT32_MAX: PAD slot
             int iu[U];
+            bool tail[U];                           // TAIL: a slot of the last window
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
@@ -972,6 +983,7 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
                 const int s = act ? cs : 0;
                 const int j = cj;
                 iu[u] = i;
+                tail[u] = TAIL && s == W - 1;
                 cj += dj;
                 cs += ds;
                 ci += di;
@@ -1001,7 +1013,9 @@ __global__ __launch_bounds__(kBlock) void hop_multi_kernel(const HopArgs p) {
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int e = e0 + u * kWave + lane;
-                if (e < total) emit_at<LAST>(orow, static_cast<uint32_t>(e), pick[u] != UINT32_MAX, rec[u], r_t[w][iu[u]]);
+                bool valid = pick[u] != UINT32_MAX;
+                if constexpr (TAIL) valid = valid && (!tail[u] || __int_as_float(rec[u].y) >= r_vw[w][iu[u]]);
+                if (e < total) emit_at<LAST>(orow, static_cast<uint32_t>(e), valid, rec[u], r_t[w][iu[u]]);
             }
         }
         wave_sync_lds();                            // the next chunk rewrites the LDS rows

@@ -262,12 +262,14 @@ def test_long_runs_and_off_grid_window_edges(torch):
         span = np.float32(0.0625) * np.float32(70_000)
         rts = (np.float32(1e6) + rng.random(R, dtype=np.float32) * span).astype(np.float32)
         rts[: R // 3] = ts[rng.integers(0, len(ts), R // 3)]          # query times equal to timestamps
-        for mode in ("recent", "uniform"):
-            announce("long runs S=%d D=%s R=%d mode=%s" % (S, D, R, mode))
-            want = oracle.sample(want_g, roots, rts, [10, 5], mode, S, D, 11, 3)
+        # one hop most recent: the last window's lower edge comes from the
+        # gathered entries' timestamps instead of a search
+        for mode, fan in (("recent", [10, 5]), ("uniform", [10, 5]), ("recent", [10])):
+            announce("long runs S=%d D=%s R=%d mode=%s fan=%s" % (S, D, R, mode, fan))
+            want = oracle.sample(want_g, roots, rts, fan, mode, S, D, 11, 3)
             for gg, what in variants:
-                got = gpu_sample(gg, roots, rts, [10, 5], mode, S, D, 11, 3)
-                assert_hops_equal(got, want, "S=%d D=%s %s %s" % (S, D, mode, what))
+                got = gpu_sample(gg, roots, rts, fan, mode, S, D, 11, 3)
+                assert_hops_equal(got, want, "S=%d D=%s %s %s %s" % (S, D, mode, fan, what))
 
 
 def test_guided_search_on_skewed_runs(torch):
