@@ -9,6 +9,8 @@ once.
   so later wavefronts of a launch run after earlier ones have finished.  The
   per-group counts a hop writes and the offsets it reads from the previous
   hop must then live in different buffers.
+* One run of more than half a billion entries, whose time directory has
+  more cells than float32 counts exactly.
 """
 import math
 
@@ -121,3 +123,50 @@ def test_whole_c2_epoch_deep(torch, fan, mode, S, D):
     assert_hops_equal(got, want, "c2 epoch fan %s %s S=%d" % (fan, mode, S))
     for h in range(len(fan)):
         assert got[h]["num_roots"] == want[h].num_roots
+
+
+def test_run_of_half_a_billion_entries(torch):
+    """One run of 2^29 + 2^20 entries (integer timestamps below 1e7, so heavy
+    ties), whose time directory has 2^24 + 2^15 cells: more than float32
+    holds integers exactly, so the cell count is rounded where the build and
+    the sampler place times in cells, and they must still agree.  The
+    directory is checked slot by slot against its definition; 100,000 roots
+    on the run (and on an empty one), sampled in three snapshots in both
+    modes, are compared with the oracle on the same T-CSR copied to the host."""
+    from gpu_util import check_dir_slots
+    L = (1 << 29) + (1 << 20)
+    dev = torch.device("cuda")
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2029)
+    announce("half-a-billion run: build of %d entries" % L)
+    src = torch.zeros(L, dtype=torch.int32, device=dev)
+    dst = torch.ones(L, dtype=torch.int32, device=dev)
+    ts = torch.randint(0, 10_000_000, (L,), device=dev, generator=gen, dtype=torch.int32).float()
+    g = P.tcsr_build(src, dst, ts, None, 2, undirected=False, hist=False, dir=True)
+    del src, dst
+    assert g.indptr.tolist() == [0, L, L]
+    assert bool((g.ts[1:] >= g.ts[:-1]).all()), "the run is not sorted by time"
+    want_sorted, _ = torch.sort(ts)
+    assert torch.equal(g.ts, want_sorted), "the run's timestamps differ from the input's"
+    del ts, want_sorted
+    torch.cuda.empty_cache()
+    K = -(-L // 32)
+    assert K > (1 << 24)
+    announce("half-a-billion run: directory of %d cells" % K)
+    check_dir_slots(g)
+    announce("half-a-billion run: host copy")
+    tsh = g.ts.cpu().numpy()
+    og = oracle.TCSR(np.array([0, L, L], np.int64), np.ones(L, np.int32), g.entries[:, 1].contiguous().cpu().numpy(), tsh)
+    rng = np.random.default_rng(2029)
+    R = 100_000
+    roots = np.where(rng.random(R) < 0.95, 0, rng.integers(1, 3, R)).astype(np.int32)   # 2: outside the graph
+    rts = rng.uniform(-1e6, 1.1e7, R).astype(np.float32)
+    rts[: R // 4] = tsh[rng.integers(0, L, R // 4)]                                      # on timestamps
+    for mode in ("recent", "uniform"):
+        announce("half-a-billion run: %s" % mode)
+        want = oracle.sample(og, roots, rts, [10], mode, 3, 1e5, 7, 11)
+        got = gpu_sample(g, roots, rts, [10], mode, 3, 1e5, 7, 11)
+        assert_hops_equal(got, want, "half-a-billion run, %s" % mode)
+        assert int((want[0].nbr >= 0).sum()) > R
+    del g, og
+    torch.cuda.empty_cache()
