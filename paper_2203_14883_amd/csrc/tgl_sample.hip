@@ -1074,6 +1074,8 @@ __device__ __forceinline__ void locate_window(const HopArgs &p, int32_t x, uint3
 // which the previous hop gathered with the entry; phase 1 takes it from
 // there, and reads no node record and leaves nothing to search.  A hop that
 // is not the last gathers the histories of its picks for the next hop.
+// DIR (a T-CSR with time directories): phase 2 starts the search of a long
+// run from its directory.
 template <int G, int MODE, bool LAST, bool FIRST, int NB, bool PTR, bool WIN, bool DIR>
 __global__ __launch_bounds__(kBlock) __attribute__((amdgpu_waves_per_eu(WIN && !FIRST ? 4 : (NB == 1 ? 7 : 6)))) void hop_single_kernel(const HopArgs p) {
     static_assert(FIRST || !PTR, "saved window edges are kept for hop 1 only");
