@@ -868,6 +868,18 @@ def main():
         cpu = cpu_baseline(w, args.cpu_batches or min(8 * B, 512), cpu_threads(args.cpu_threads))
         log("CPU oracle: %.3g neighbours/s on %d threads, %.3g on one (%s)"
             % (cpu["value"], cpu["cores"], cpu["single_core"]["value"], cpu["sample"]))
+        if args.workload == "c5":
+            # c5's T-CSR is built from a shuffled COO: the oracle's build of the
+            # same COO, on one core, beside the GPU build
+            import oracle
+            src, dst, ts, eid = w.build_input()
+            t = time.perf_counter()
+            og = oracle.build_tcsr(src, dst, ts, eid, w.num_nodes, w.undirected)
+            cpu["build"] = dict(seconds=time.perf_counter() - t, entries=len(og.nbr), cores=1,
+                                gpu_ms=build_ms, what="oracle_build of the same shuffled COO")
+            log("CPU oracle build of the %d-entry T-CSR from the shuffled COO: %.1f s (GPU: %.1f ms)"
+                % (len(og.nbr), cpu["build"]["seconds"], build_ms))
+            del og, src, dst, ts, eid
 
     line = {
         "metric": METRIC,
