@@ -306,3 +306,19 @@ def test_noalloc_argument_checks():
     assert call(n=20000, fan=(1024, 1024)) == B.ENOSPACE
     need = L.tgl_sample_workspace(20000, 2, B._i32_array((1024, 1024))[1], 1)
     assert need > B.NOALLOC_SCRATCH_BYTES
+
+
+def test_column_view_binding_checks_its_arguments():
+    """tcsr_from_columns refuses columns of the wrong type or length before
+    anything reaches the library."""
+    import torch
+    ip = torch.zeros(3, dtype=torch.int64)
+    nbr = torch.zeros(4, dtype=torch.int32)
+    ts = torch.zeros(4, dtype=torch.float32)
+    eid = torch.zeros(4, dtype=torch.int64)
+    for bad in [dict(indptr=ip.int()), dict(nbr=nbr.long()), dict(ts=ts.double()), dict(ts=ts[:3]),
+                dict(eid=eid[:3]), dict(eid=eid.int())]:
+        a = dict(indptr=ip, nbr=nbr, ts=ts, eid=eid)
+        a.update(bad)
+        with pytest.raises(ValueError):
+            P.tcsr_from_columns(a["indptr"], a["nbr"], a["ts"], a["eid"])
